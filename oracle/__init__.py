@@ -1,0 +1,370 @@
+"""CPU oracle for the population payoff-table rollout path.
+
+TEST INFRASTRUCTURE ONLY: tests/, __graft_entry__.smoke() and the cpu_baseline
+leg of bench.py are the only callers.  The product library never imports,
+links or runs anything here, and nothing here imports the product package.
+
+The arithmetic lives in ``oracle.c`` (plain single-threaded C, built with
+``-ffp-contract=off`` and no fast-math); this module builds it with gcc, wraps
+it with ctypes and adds the payoff table, written out in numpy fp64 from its
+definition: the evaluator's table holds, for each policy combination, the
+mean evaluation result of the simulations run under it (MALib Sec. 3.2,
+Actor-Evaluator-Learner; Appendix C.2 ``run_simulation_and_update_payoff``).
+Here the result is the undiscounted return of the row-side seat and, for team
+games, every (row-side seat, column-side seat) pair of an env is one entry.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_CFLAGS = ["-O2", "-march=x86-64-v3", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", "-std=c11", "-Wall"]
+
+TOL_BF16 = 1e-2
+TOL_F32 = 1e-5
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so (always, when ``force``)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", *_CFLAGS, _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class Config(C.Structure):
+    _fields_ = [
+        ("env_kind", C.c_int32), ("n_agents", C.c_int32), ("n_actions", C.c_int32),
+        ("grid", C.c_int32), ("team", C.c_void_p), ("A", C.c_void_p),
+        ("d", C.c_int32), ("init_mode", C.c_int32),
+        ("W", C.c_void_p), ("emb", C.c_void_p), ("u", C.c_void_p),
+        ("pol_kind", C.c_int32), ("P", C.c_int32), ("n_layers", C.c_int32),
+        ("horizon", C.c_int32), ("dims", C.c_void_p),
+        ("Wl", C.POINTER(C.c_void_p)), ("bl", C.POINTER(C.c_void_p)),
+        ("tab", C.c_void_p), ("seed", C.c_uint64), ("env_offset", C.c_int64),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = C.CDLL(_LIB)
+        L.ora_philox4x64_10.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
+        L.ora_lane.restype = C.c_uint32
+        L.ora_lane.argtypes = [C.c_uint64, C.c_int64, C.c_int64, C.c_int32, C.c_int32,
+                               C.c_int64, C.c_int32]
+        L.ora_uniform.restype = C.c_float
+        L.ora_uniform.argtypes = [C.c_uint32]
+        L.ora_gumbel.restype = C.c_double
+        L.ora_gumbel.argtypes = [C.c_float]
+        L.ora_bf16_bits.restype = C.c_uint16
+        L.ora_bf16_bits.argtypes = [C.c_float]
+        L.ora_bf16_round.restype = C.c_float
+        L.ora_bf16_round.argtypes = [C.c_float]
+        L.ora_exp_ref.restype = C.c_float
+        L.ora_exp_ref.argtypes = [C.c_float]
+        L.ora_tanh_ref.restype = C.c_float
+        L.ora_tanh_ref.argtypes = [C.c_float]
+        L.ora_tanh_range.argtypes = [C.c_uint32, C.c_int64, C.c_void_p]
+        L.ora_tanh_max_ulp.restype = C.c_double
+        L.ora_tanh_max_ulp.argtypes = [C.c_uint32, C.c_int64, C.c_void_p]
+        L.ora_meta_sample.restype = C.c_int
+        L.ora_meta_sample.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int64,
+                                      C.c_int32, C.c_uint64, C.c_int64, C.c_void_p]
+        L.ora_rollout.restype = C.c_int
+        L.ora_rollout.argtypes = [C.POINTER(Config), C.c_int64, C.c_void_p, C.c_void_p,
+                                  C.c_void_p, C.c_double, C.c_void_p, C.c_void_p,
+                                  C.c_void_p, C.c_void_p, C.c_void_p]
+        L.ora_state_elems.restype = C.c_int64
+        L.ora_state_elems.argtypes = [C.c_int32, C.c_int32]
+        L.ora_obs_iter.argtypes = [C.c_void_p, C.c_int32, C.c_void_p]
+        L.ora_obs_pursuit.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p]
+        L.ora_pursuit_step.restype = C.c_int
+        L.ora_pursuit_step.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int32]
+        L.ora_pursuit_reset.argtypes = [C.c_uint64, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p]
+        L.ora_feature_reset.argtypes = [C.c_uint64, C.c_int64, C.c_int32, C.c_void_p]
+        L.ora_feature_step.restype = C.c_float
+        L.ora_feature_step.argtypes = [C.POINTER(Config), C.c_void_p, C.c_void_p, C.c_void_p]
+        L.ora_policy_logits.restype = C.c_int
+        L.ora_policy_logits.argtypes = [C.POINTER(Config), C.c_int32, C.c_void_p, C.c_void_p]
+        L.ora_bf16_range.argtypes = [C.c_uint32, C.c_int64, C.c_void_p]
+        L.ora_uniform_range.argtypes = [C.c_uint32, C.c_int64, C.c_void_p]
+        L.ora_exp_many.argtypes = [C.c_void_p, C.c_int64, C.c_void_p]
+        L.ora_tanh_many.argtypes = [C.c_void_p, C.c_int64, C.c_void_p]
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+# ----------------------------------------------------------------- primitives
+
+def philox(ctr, key):
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, np.uint64)
+    lib().ora_philox4x64_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def lane(seed, g, t, purpose, slot, block, ln):
+    return lib().ora_lane(seed, g, t, purpose, slot, block, ln)
+
+
+def uniform(x):
+    return lib().ora_uniform(int(x))
+
+
+def gumbel(u):
+    return lib().ora_gumbel(float(u))
+
+
+def bf16_bits(x):
+    return lib().ora_bf16_bits(float(x))
+
+
+def bf16_round(x):
+    return lib().ora_bf16_round(float(x))
+
+
+def exp_ref(x):
+    return lib().ora_exp_ref(float(x))
+
+
+def tanh_ref(x):
+    return lib().ora_tanh_ref(float(x))
+
+
+def tanh_range(first_bits: int, n: int) -> np.ndarray:
+    out = np.empty(n, np.float32)
+    lib().ora_tanh_range(first_bits, n, _ptr(out))
+    return out
+
+
+def bf16_range(first_bits: int, n: int) -> np.ndarray:
+    out = np.empty(n, np.uint16)
+    lib().ora_bf16_range(first_bits, n, _ptr(out))
+    return out
+
+
+def uniform_range(first: int, n: int) -> np.ndarray:
+    out = np.empty(n, np.float32)
+    lib().ora_uniform_range(first, n, _ptr(out))
+    return out
+
+
+def exp_many(x) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty_like(x)
+    lib().ora_exp_many(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def tanh_many(x) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty_like(x)
+    lib().ora_tanh_many(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def tanh_max_ulp(first_bits: int, n: int):
+    w = np.zeros(1, np.uint32)
+    e = lib().ora_tanh_max_ulp(first_bits, n, _ptr(w))
+    return e, int(w[0])
+
+
+def meta_sample(sigma, P, n_envs, n_agents, seed, env_offset=0):
+    s = np.ascontiguousarray(sigma, dtype=np.float32).reshape(-1, P)
+    out = np.zeros((n_envs, n_agents), np.int32)
+    rc = lib().ora_meta_sample(_ptr(s), s.shape[0], P, n_envs, n_agents, seed,
+                               env_offset, _ptr(out))
+    if rc != 0:
+        raise ValueError(f"ora_meta_sample rejected its input ({rc})")
+    return out
+
+
+# ---------------------------------------------------------------- configuration
+
+class _Cfg:
+    """Keeps the numpy buffers a ctypes Config points at alive."""
+
+    def __init__(self, wl, horizon=None, env_offset=0, init_mode=None):
+        keep = []
+
+        def arr(a, dt):
+            if a is None:
+                return None
+            a = np.ascontiguousarray(a, dtype=dt)
+            keep.append(a)
+            return a
+
+        cfg = Config()
+        cfg.env_kind = wl.env_kind
+        cfg.n_agents = wl.n_agents
+        cfg.n_actions = wl.n_actions
+        cfg.grid = wl.grid
+        cfg.team = _ptr(arr(wl.team, np.int8))
+        cfg.A = _ptr(arr(wl.A, np.float32))
+        cfg.d = wl.d
+        cfg.init_mode = wl.init_mode if init_mode is None else init_mode
+        cfg.W = _ptr(arr(wl.W, np.float32))
+        cfg.emb = _ptr(arr(wl.emb, np.float32))
+        cfg.u = _ptr(arr(wl.u, np.float32))
+        cfg.pol_kind = wl.pol_kind
+        cfg.P = wl.P
+        L = len(wl.dims) - 1 if wl.dims else 0
+        cfg.n_layers = L
+        cfg.horizon = wl.horizon if horizon is None else horizon
+        cfg.dims = _ptr(arr(np.array(wl.dims or [0], np.int32), np.int32))
+        wl_ptrs = (C.c_void_p * max(L, 1))()
+        bl_ptrs = (C.c_void_p * max(L, 1))()
+        for l in range(L):
+            wl_ptrs[l] = _ptr(arr(wl.weights[l], np.float32))
+            bl_ptrs[l] = _ptr(arr(wl.biases[l], np.float32)) if wl.biases else None
+        keep += [wl_ptrs, bl_ptrs]
+        cfg.Wl = C.cast(wl_ptrs, C.POINTER(C.c_void_p))
+        cfg.bl = C.cast(bl_ptrs, C.POINTER(C.c_void_p))
+        cfg.tab = _ptr(arr(wl.tab_logits, np.float32))
+        cfg.seed = wl.seed
+        cfg.env_offset = env_offset
+        self.cfg = cfg
+        self.keep = keep
+
+
+def state_shape(wl, n):
+    if wl.env_kind == 1:
+        return (n,), np.uint16
+    if wl.env_kind == 2:
+        return (n, 3), np.uint8
+    if wl.env_kind == 3:
+        return (n, wl.d), np.float32
+    return None, None
+
+
+def rollout(wl, env_idx, pids, *, forced=None, tol=None, horizon=None, env_offset=0,
+            want_actions=False, want_logits=False, want_states=False, init_mode=None):
+    """Roll out the selected envs (local indices ``env_idx`` of a batch that
+    starts at global env ``env_offset``) with per-env policy ids ``pids``
+    [n_sel][n_agents].  ``forced`` is an action log [H][n_sel][n_agents] to
+    follow in lockstep (see oracle.c).  Returns a dict."""
+    H = wl.horizon if horizon is None else horizon
+    if tol is None:
+        tol = TOL_F32 if wl.pol_kind == 1 else TOL_BF16
+    idx = np.ascontiguousarray(env_idx, dtype=np.int64)
+    n = idx.shape[0]
+    p = np.ascontiguousarray(pids, dtype=np.int32).reshape(n, wl.n_agents)
+    f = None if forced is None else np.ascontiguousarray(forced, dtype=np.uint8).reshape(
+        H, n, wl.n_agents)
+    cfg = _Cfg(wl, horizon=H, env_offset=env_offset, init_mode=init_mode)
+    ret = np.zeros((n, wl.n_agents), np.float32)
+    acts = np.zeros((H, n, wl.n_agents), np.uint8) if want_actions else None
+    logits = np.zeros((H, n, wl.n_agents, wl.n_actions), np.float32) if want_logits else None
+    states = None
+    if want_states:
+        shp, dt = state_shape(wl, n)
+        if shp is not None:
+            states = np.zeros((H,) + shp, dt)
+    stats = np.zeros(7, np.int64)
+    rc = lib().ora_rollout(C.byref(cfg.cfg), n, _ptr(idx), _ptr(p), _ptr(f), float(tol),
+                           _ptr(ret), _ptr(acts), _ptr(logits), _ptr(states), _ptr(stats))
+    if rc != 0:
+        raise RuntimeError(f"ora_rollout failed ({rc})")
+    return {
+        "returns": ret, "actions": acts, "logits": logits, "states": states,
+        "near_ties": int(stats[0]), "flips": int(stats[1]), "fails": int(stats[2]),
+        "live_frames": int(stats[3]),
+        "first_fail": tuple(int(x) for x in stats[4:7]),
+    }
+
+
+def policy_logits(wl, p, obs):
+    cfg = _Cfg(wl)
+    o = np.ascontiguousarray(obs, dtype=np.float64)
+    out = np.zeros(wl.n_actions, np.float32)
+    if lib().ora_policy_logits(C.byref(cfg.cfg), p, _ptr(o), _ptr(out)) != 0:
+        raise ValueError("bad policy id")
+    return out
+
+
+def feature_step(wl, s, acts):
+    cfg = _Cfg(wl)
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    a = np.ascontiguousarray(acts, dtype=np.int32)
+    out = np.zeros_like(s)
+    r = lib().ora_feature_step(C.byref(cfg.cfg), _ptr(s), _ptr(a), _ptr(out))
+    return out, r
+
+
+def feature_reset(seed, g, d):
+    s = np.zeros(d, np.float32)
+    lib().ora_feature_reset(seed, g, d, _ptr(s))
+    return s
+
+
+def pursuit_reset(seed, g, grid=8):
+    pc = np.zeros(1, np.int32)
+    ec = np.zeros(1, np.int32)
+    lib().ora_pursuit_reset(seed, g, grid, _ptr(pc), _ptr(ec))
+    return int(pc[0]), int(ec[0])
+
+
+def pursuit_step(pc, ec, a0, a1, grid=8):
+    p = np.array([pc], np.int32)
+    e = np.array([ec], np.int32)
+    cap = lib().ora_pursuit_step(_ptr(p), _ptr(e), a0, a1, grid)
+    return int(p[0]), int(e[0]), bool(cap)
+
+
+def obs_pursuit(pc, ec, seat, grid=8):
+    out = np.zeros(75, np.float64)
+    lib().ora_obs_pursuit(pc, ec, seat, grid, _ptr(out))
+    return out
+
+
+def obs_iter(hist, seat):
+    h = np.ascontiguousarray(hist, dtype=np.int32)
+    out = np.zeros(24, np.float64)
+    lib().ora_obs_iter(_ptr(h), seat, _ptr(out))
+    return out
+
+
+# ----------------------------------------------------------------- payoff table
+
+def payoff(returns, pids, team, P):
+    """Payoff table from per-env returns [n_envs][n_agents] and policy ids
+    [n_envs][n_agents]: every (row-side seat a, column-side seat b) of an env adds
+    the return of seat a to cell (pid[a], pid[b]).  Returns (mean, counts, sum,
+    sumsq) in fp64; mean is NaN where the count is zero."""
+    returns = np.asarray(returns, dtype=np.float64)
+    pids = np.asarray(pids, dtype=np.int64)
+    team = np.asarray(team)
+    rows = np.nonzero(team > 0)[0]
+    cols = np.nonzero(team < 0)[0]
+    s = np.zeros((P, P), np.float64)
+    s2 = np.zeros((P, P), np.float64)
+    n = np.zeros((P, P), np.int64)
+    for a in rows:
+        for b in cols:
+            cell = pids[:, a] * P + pids[:, b]
+            g = returns[:, a]
+            s += np.bincount(cell, weights=g, minlength=P * P).reshape(P, P)
+            s2 += np.bincount(cell, weights=g * g, minlength=P * P).reshape(P, P)
+            n += np.bincount(cell, minlength=P * P).reshape(P, P)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        mean = np.where(n > 0, s / np.maximum(n, 1), np.nan)
+    return mean, n, s, s2
