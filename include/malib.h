@@ -1,0 +1,282 @@
+/*
+ * malib.h - C ABI of the MI355X (gfx950) payoff-table rollout library.
+ *
+ * The library fills the empirical payoff table of a policy population: it
+ * simulates many episodes for every policy combination drawn from the
+ * population and reduces their returns into a mean-return matrix with
+ * per-cell counts.  In MALib (arXiv 2106.07551) this is the work of the
+ * Actors and the Evaluator: each agent picks a policy from its pool to form a
+ * combination Comb_t (Sec. 3.1, "Defining the Task Graph"), rollouts sample
+ * X ~ P(s, a, s' | a ~ Comb_t) (Sec. 3.1, rollout equation), and the
+ * Evaluator keeps a payoff table of the evaluation result of every policy
+ * combination, on which e.g. PSRO solves for a meta-strategy (Sec. 3.2,
+ * Actor-Evaluator-Learner).  The single-instance example (Appendix C.2) names
+ * the pieces: PayoffManager, run_simulation_and_update_payoff, and per-agent
+ * policy distributions Dict[AgentID, Dict[PolicyID, float]].
+ *
+ * Conventions shared by every call:
+ *  - Device pointers are HIP device addresses (e.g. torch CUDA tensors'
+ *    data_ptr()); host pointers are ordinary process memory.  Each argument
+ *    says which it is.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    All device work is enqueued on it asynchronously; only malib_payoff_eval
+ *    and malib_profile_read synchronize it.  Device buffers the caller passes
+ *    in (pair assignments, environment parameters) must stay valid until the
+ *    work on the stream has completed.
+ *  - The caller owns every pointer it passes.  malib_pop_create copies and
+ *    re-lays out the weights, so they may be freed after it returns (and after
+ *    the stream has completed).
+ *  - Host-detectable errors (bad sizes, null pointers, unsupported shapes,
+ *    invalid meta-strategies) return a negative status before any device work
+ *    is enqueued, and malib_last_error() gives a message (thread-local).
+ *    Errors the device detects (a policy id outside [0, P), a NaN logit) set a
+ *    flag on the population handle that the next malib_payoff_eval reports
+ *    as MALIB_E_DEVICE.
+ *  - Results depend only on (inputs, seed, env_offset + local env index):
+ *    they are independent of launch geometry, batching and streams.
+ *  - A handle must not be used from two threads at once.
+ */
+#ifndef MALIB_H
+#define MALIB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t malib_status;
+enum {
+    MALIB_OK = 0,
+    MALIB_E_INVAL = -1,        /* invalid argument */
+    MALIB_E_NOMEM = -2,        /* device or host allocation failed */
+    MALIB_E_HIP = -3,          /* a HIP runtime call failed */
+    MALIB_E_UNSUPPORTED = -4,  /* valid but not implemented shape/combination */
+    MALIB_E_DEVICE = -5        /* the device flagged bad data (see above) */
+};
+
+/* ---------------------------------------------------------------- population */
+
+enum {
+    MALIB_POLICY_TABULAR = 0,  /* state-less logits per policy (one-step games) */
+    MALIB_POLICY_MLP_F32 = 1,  /* fp32 MLP, fp32 arithmetic */
+    MALIB_POLICY_MLP_BF16 = 2  /* bf16 MLP: bf16 inputs/weights/hidden, fp32 accumulation */
+};
+
+/*
+ * A population of P policies shared by every seat (a policy pool, Sec. 3.1:
+ * "some of them can share the same policy pool").  MLP policies have two
+ * hidden ReLU layers: logits = W3 relu(W2 relu(W1 x + b1) + b2) + b3, with the
+ * weight of layer l laid out [P][dims[l+1]][dims[l]] (row = output unit).
+ *
+ * Supported shapes:
+ *  - TABULAR: n_layers = 0, tab_logits device fp32 [P][n_actions].
+ *  - MLP_F32: n_layers = 3, dims = {24, h, h, A} with h in {32, 64}, A <= 3;
+ *    used with the iterated matrix game (in = 8 * n_actions).
+ *  - MLP_BF16: n_layers = 3, dims = {in, h, h, A} with 1 <= in <= 512,
+ *    h in {64, 128, 256, 512}, A <= 32.  fp32 weights are rounded to bf16
+ *    (nearest, ties to even) when the handle is created.
+ * 1 <= P <= 256, 1 <= n_actions <= 32.
+ */
+typedef struct {
+    int32_t kind;                 /* MALIB_POLICY_* */
+    int32_t n_policies;           /* P */
+    int32_t n_actions;            /* A (= dims[n_layers] for MLPs) */
+    int32_t n_layers;             /* 3 for MLPs, 0 for TABULAR */
+    const int32_t* dims;          /* host [n_layers + 1] */
+    const float* const* weights;  /* host array of n_layers device pointers (fp32) */
+    const float* const* biases;   /* host array of n_layers device pointers
+                                     fp32 [P][dims[l+1]], or NULL (all zero);
+                                     individual entries may be NULL (zero) */
+    const float* tab_logits;      /* TABULAR: device fp32 [P][n_actions] */
+} malib_pop_desc;
+
+typedef struct malib_pop* malib_pop_t;
+
+/* Create a population handle: validates, allocates, packs the weights for the
+ * policy kernels, allocates the P x P payoff accumulators (zeroed).  The
+ * packing runs on `stream`, which is synchronized before returning, so the
+ * caller's weight buffers may be released right away.  On error *out is set
+ * to NULL. */
+malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_pop_t* out);
+
+/* Free a handle (synchronizes the device first).  NULL is ignored. */
+void malib_pop_destroy(malib_pop_t pop);
+
+/* --------------------------------------------------------------- environment */
+
+enum {
+    MALIB_ENV_MATRIX = 0,       /* one-step 2-player matrix game: r0 = A[a0][a1], r1 = -r0 */
+    MALIB_ENV_ITER_MATRIX = 1,  /* repeated matrix game; obs = one-hot of the last 4 joint actions */
+    MALIB_ENV_PURSUIT = 2,      /* 2-agent pursuit-evasion on a torus grid, capture ends the episode */
+    MALIB_ENV_FEATURE = 3       /* s' = tanh(W s + sum_k emb[k][a_k]), r = u . s' (zero-sum teams) */
+};
+
+enum { MALIB_INIT_PER_ENV = 0, MALIB_INIT_SHARED = 1 };
+
+/*
+ * Environment family and parameters.  Rules (the paper specifies none; these
+ * are the synthetic games used to exercise the rollout path):
+ *  MATRIX / ITER_MATRIX: 2 seats, n_actions <= 3 for ITER_MATRIX, <= 32 for
+ *    MATRIX.  ITER observation of seat k: for lag 1..4 (most recent first) the
+ *    one-hot of its own action then of the opponent's, zeros before t = 0.
+ *  PURSUIT: 2 seats (0 = pursuer, 1 = evader), n_actions = 5 (stay, up, down,
+ *    left, right), grid = 8.  Capture (same cell after the move, or the two
+ *    swapped cells) gives +1 / -1 and ends the episode; finished envs take no
+ *    further actions and count no further frames.  Observation: egocentric
+ *    5x5x3 window (pursuer, evader, self channels), 75 values.
+ *  FEATURE: 2..8 seats, state fp32 [d] with d a multiple of 64, 64 <= d <= 512;
+ *    the fp32 sums are formed in a fixed order (W s as a fused multiply-add
+ *    chain over the input index, then the embeddings in seat order), tanh is
+ *    the library's fixed tanh_ref and r = u . s' is a fused chain over the
+ *    index; seats with team +1 receive r, the others -r.  Every seat observes
+ *    bf16(s_t).
+ */
+typedef struct {
+    int32_t kind;             /* MALIB_ENV_* */
+    int32_t n_agents;         /* seats per env */
+    int32_t n_actions;        /* must equal the population's */
+    int32_t grid;             /* PURSUIT: torus side (8) */
+    const int8_t* team;       /* host [n_agents]: +1 row side, -1 column side;
+                                 NULL means {+1, -1} (two seats) */
+    const float* A;           /* MATRIX / ITER_MATRIX: device fp32 [n_actions][n_actions] */
+    int32_t d;                /* FEATURE: state dimension */
+    int32_t init_mode;        /* MALIB_INIT_*: SHARED starts every env from the
+                                 reset draw of global env 0 (for tests) */
+    const float* W;           /* FEATURE: device fp32 [d][d] (row = output) */
+    const float* emb;         /* FEATURE: device fp32 [n_agents][n_actions][d] */
+    const float* u;           /* FEATURE: device fp32 [d] */
+} malib_env_desc;
+
+/* ---------------------------------------------------------------- rollouts */
+
+/*
+ * Optional parity trace.  Any pointer may be NULL.
+ *  actions: device uint8 [horizon][n_envs * n_agents]; 255 where the env has
+ *           already finished.
+ *  snap_steps: host int32 [n_snap], steps in [0, horizon) to snapshot;
+ *  logits: device fp32 [n_snap][n_envs * n_agents][n_actions], the logits of
+ *          that step (slot order env * n_agents + seat);
+ *  states: device [n_snap][...] the state before that step, in the format
+ *          ITER_MATRIX: uint16 [n_envs] (4-bit joint action a0*3+a1 per lag,
+ *          lag 1 in the low nibble, 15 = none); PURSUIT: uint8 [n_envs][3]
+ *          (pursuer cell, evader cell, done), cell = 8*y + x; FEATURE: fp32
+ *          [n_envs][d]; MATRIX: nothing.
+ *  perm / offsets: device int32 [n_envs * n_agents] / [P + 1]: the slots sorted
+ *          by policy id (stable) and the bucket boundaries (MLP policies only).
+ */
+typedef struct {
+    uint8_t* actions;
+    int32_t n_snap;
+    const int32_t* snap_steps;
+    float* logits;
+    void* states;
+    int32_t* perm;
+    int32_t* offsets;
+} malib_trace;
+
+/*
+ * Simulate n_envs episodes of `horizon` steps and add their returns to the
+ * handle's payoff table (run_simulation_and_update_payoff, Appendix C.2).
+ *  pair_assign: device int32 [n_envs][n_agents], the policy id of every seat
+ *               (one policy combination per env, Sec. 3.1).
+ *  seed, env_offset: the action noise, resets and everything random depend
+ *               only on (seed, env_offset + e) for local env e.
+ *  returns:     device fp32 [n_agents][n_envs] per-seat undiscounted returns,
+ *               or NULL.
+ *  trace:       NULL or a parity trace (above).
+ * Every step runs: grouped policy forward (slots bucketed by policy id),
+ * Gumbel-max action sampling on Philox4x64-10 noise, environment step with
+ * return accumulation; after the last step the returns are reduced into the
+ * P x P table: each (row-side seat a, column-side seat b) pair of an env adds
+ * the return of seat a to cell (pid[a], pid[b]).
+ * Limits: n_envs >= 1, n_envs * n_agents <= 2^26, 1 <= horizon <= 100000.
+ */
+malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env,
+                                 int64_t n_envs, const int32_t* pair_assign,
+                                 uint64_t seed, int64_t env_offset, int32_t horizon,
+                                 float* returns, const malib_trace* trace, void* stream);
+
+/* ------------------------------------------------------------- payoff table */
+
+typedef struct {
+    int64_t live_frames;   /* live agent-frames (env, seat, step) since the last reset */
+    int64_t envs;          /* envs simulated since the last reset */
+    int32_t device_flags;  /* bit 0: policy id out of range; bit 1: NaN logit */
+} malib_eval_stats;
+
+/*
+ * The payoff table (the PayoffManager of Appendix C.2): synchronizes `stream`,
+ * then writes, each optional,
+ *  mean:   host fp64 [P][P], sum / count, NaN where count == 0;
+ *  counts: host int64 [P][P];
+ *  stderr_out: host fp64 [P][P], standard error of the mean (NaN if count < 2);
+ *  stats:  host, see above.
+ * Sums are kept in 64-bit fixed point (2^-32 units for returns, 2^-20 for
+ * squares), so the table is exact and independent of reduction order.
+ * reset != 0 zeroes the table afterwards.  Returns MALIB_E_DEVICE (after
+ * writing the outputs and clearing the flags) if the device flagged bad data.
+ */
+malib_status malib_payoff_eval(malib_pop_t pop, void* stream, int32_t reset,
+                               double* mean, int64_t* counts, double* stderr_out,
+                               malib_eval_stats* stats);
+
+/* ------------------------------------------------------------ meta-strategy */
+
+/*
+ * Draw the policy id of every seat from a meta-strategy (the per-agent policy
+ * distribution of Appendix C.2; Comb_{t+1} ~ G(...) in Sec. 3.1).
+ *  sigma: host fp32 [n_sigma][n_policies], non-negative, finite, positive sum
+ *         per row (rows need not be normalized); n_sigma is 1 (shared by all
+ *         seats) or n_agents (row k for seat k).
+ *  pair_assign_out: device int32 [n_envs][n_agents].
+ * Seat k of global env g = env_offset + e takes pid = min{m : x < T_m}, where
+ * x is the first 32-bit lane of the Philox block (g, 0, 2<<32 | k, 0) and T_m
+ * = floor(2^32 * C_m) from the fp64 cumulative sum C of the normalized row
+ * (T_{P-1} = 2^32).  Policies with zero mass are never drawn.  The
+ * thresholds are computed on the host and uploaded on `stream`, which is
+ * synchronized once before the sampling kernel is enqueued.
+ */
+malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t n_policies,
+                               int64_t n_envs, int32_t n_agents, uint64_t seed,
+                               int64_t env_offset, int32_t* pair_assign_out, void* stream);
+
+/* Message for the last non-OK status returned on this thread. */
+const char* malib_last_error(void);
+
+/* ---------------------------------------------------------------- profiling */
+
+enum {
+    MALIB_K_POLICY = 0,   /* grouped policy forward */
+    MALIB_K_SAMPLE = 1,   /* Gumbel-max action sampling */
+    MALIB_K_ENV = 2,      /* environment step + return accumulation */
+    MALIB_K_SETUP = 3,    /* bucketing + reset */
+    MALIB_K_PAYOFF = 4,   /* payoff reduction */
+    MALIB_K_COUNT = 5
+};
+
+/* Enable (1) or disable (0) HIP-event timing of every kernel launch of the
+ * handle, on the stream the kernel runs on.  Enabling clears the totals. */
+malib_status malib_profile_enable(malib_pop_t pop, int32_t enable);
+
+/* Total elapsed milliseconds and launch count of one kernel class since the
+ * profile was enabled; synchronizes the recorded events. */
+malib_status malib_profile_read(malib_pop_t pop, int32_t kernel, double* total_ms,
+                                int64_t* launches);
+
+/* ------------------------------------------------------------- diagnostics */
+
+/* y[i] = tanh_ref(x[i]) on the device: the fixed tanh of the feature
+ * dynamics, exposed so it can be compared bit for bit.  x, y: device fp32 [n]. */
+malib_status malib_debug_tanh_ref(const float* x, float* y, int64_t n, void* stream);
+
+/* Philox4x64-10 blocks on the device: out[i] = philox(ctr[i], (key0, key1)).
+ * ctr, out: device uint64 [n][4]. */
+malib_status malib_debug_philox(const uint64_t* ctr, uint64_t key0, uint64_t key1,
+                                uint64_t* out, int64_t n, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MALIB_H */

@@ -1,0 +1,248 @@
+"""ctypes binding of libmalib.so (argument marshalling only).
+
+Device buffers are torch CUDA (HIP) tensors; streams are torch streams.  Every
+call goes straight to the C ABI of ``include/malib.h``; names follow it.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmalib.so")
+
+MALIB_OK, E_INVAL, E_NOMEM, E_HIP, E_UNSUPPORTED, E_DEVICE = 0, -1, -2, -3, -4, -5
+POLICY_TABULAR, POLICY_MLP_F32, POLICY_MLP_BF16 = 0, 1, 2
+ENV_MATRIX, ENV_ITER_MATRIX, ENV_PURSUIT, ENV_FEATURE = 0, 1, 2, 3
+INIT_PER_ENV, INIT_SHARED = 0, 1
+K_POLICY, K_SAMPLE, K_ENV, K_SETUP, K_PAYOFF = 0, 1, 2, 3, 4
+
+# every function declared in include/malib.h
+EXPORTS = [
+    "malib_pop_create", "malib_pop_destroy", "malib_rollout_batch", "malib_payoff_eval",
+    "malib_meta_sample", "malib_last_error", "malib_profile_enable", "malib_profile_read",
+    "malib_debug_tanh_ref", "malib_debug_philox",
+]
+
+
+class MalibError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"malib status {status}: {msg}")
+        self.status = status
+
+
+class PopDesc(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("n_policies", C.c_int32), ("n_actions", C.c_int32),
+                ("n_layers", C.c_int32), ("dims", C.POINTER(C.c_int32)),
+                ("weights", C.POINTER(C.c_void_p)), ("biases", C.POINTER(C.c_void_p)),
+                ("tab_logits", C.c_void_p)]
+
+
+class EnvDesc(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("n_agents", C.c_int32), ("n_actions", C.c_int32),
+                ("grid", C.c_int32), ("team", C.POINTER(C.c_int8)), ("A", C.c_void_p),
+                ("d", C.c_int32), ("init_mode", C.c_int32), ("W", C.c_void_p),
+                ("emb", C.c_void_p), ("u", C.c_void_p)]
+
+
+class TraceDesc(C.Structure):
+    _fields_ = [("actions", C.c_void_p), ("n_snap", C.c_int32),
+                ("snap_steps", C.POINTER(C.c_int32)), ("logits", C.c_void_p),
+                ("states", C.c_void_p), ("perm", C.c_void_p), ("offsets", C.c_void_p)]
+
+
+class EvalStats(C.Structure):
+    _fields_ = [("live_frames", C.c_int64), ("envs", C.c_int64), ("device_flags", C.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libmalib.so; raises if it has not been built (no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                              "(hipcc, gfx950); there is no CPU fallback")
+        L = C.CDLL(LIB_PATH)
+        vp, i32, i64, u64 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64
+        L.malib_pop_create.argtypes = [C.POINTER(PopDesc), vp, C.POINTER(vp)]
+        L.malib_pop_create.restype = i32
+        L.malib_pop_destroy.argtypes = [vp]
+        L.malib_pop_destroy.restype = None
+        L.malib_rollout_batch.argtypes = [vp, C.POINTER(EnvDesc), i64, vp, u64, i64, i32, vp,
+                                          C.POINTER(TraceDesc), vp]
+        L.malib_rollout_batch.restype = i32
+        L.malib_payoff_eval.argtypes = [vp, vp, i32, vp, vp, vp, C.POINTER(EvalStats)]
+        L.malib_payoff_eval.restype = i32
+        L.malib_meta_sample.argtypes = [vp, i32, i32, i64, i32, u64, i64, vp, vp]
+        L.malib_meta_sample.restype = i32
+        L.malib_last_error.argtypes = []
+        L.malib_last_error.restype = C.c_char_p
+        L.malib_profile_enable.argtypes = [vp, i32]
+        L.malib_profile_enable.restype = i32
+        L.malib_profile_read.argtypes = [vp, i32, C.POINTER(C.c_double), C.POINTER(i64)]
+        L.malib_profile_read.restype = i32
+        L.malib_debug_tanh_ref.argtypes = [vp, vp, i64, vp]
+        L.malib_debug_tanh_ref.restype = i32
+        L.malib_debug_philox.argtypes = [vp, u64, u64, vp, i64, vp]
+        L.malib_debug_philox.restype = i32
+        _lib = L
+    return _lib
+
+
+def _check(st: int):
+    if st != MALIB_OK:
+        raise MalibError(st, lib().malib_last_error().decode())
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _dptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    assert t.is_cuda and t.is_contiguous(), "expected a contiguous device tensor"
+    return t.data_ptr()
+
+
+class Population:
+    """A policy population handle (malib_pop_create / malib_pop_destroy) with its
+    payoff table."""
+
+    def __init__(self, kind: int, n_policies: int, n_actions: int, *, dims=None,
+                 weights: Sequence = (), biases: Optional[Sequence] = None,
+                 tab_logits=None, stream=None):
+        d = PopDesc()
+        d.kind, d.n_policies, d.n_actions = kind, n_policies, n_actions
+        self._keep = []
+        if kind == POLICY_TABULAR:
+            d.n_layers = 0
+            d.tab_logits = _dptr(tab_logits)
+        else:
+            d.n_layers = len(dims) - 1
+            dd = (C.c_int32 * len(dims))(*dims)
+            ww = (C.c_void_p * d.n_layers)(*[_dptr(w) for w in weights])
+            self._keep += [dd, ww]
+            d.dims = C.cast(dd, C.POINTER(C.c_int32))
+            d.weights = C.cast(ww, C.POINTER(C.c_void_p))
+            if biases is not None:
+                bb = (C.c_void_p * d.n_layers)(*[_dptr(b) for b in biases])
+                self._keep.append(bb)
+                d.biases = C.cast(bb, C.POINTER(C.c_void_p))
+        h = C.c_void_p()
+        _check(lib().malib_pop_create(C.byref(d), _stream(stream), C.byref(h)))
+        self.handle = h
+        self.P = n_policies
+        self.A = n_actions
+        self._keep = []
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().malib_pop_destroy(self.handle)
+            self.handle = None
+
+    __del__ = close
+
+    def rollout(self, env: "Env", n_envs: int, pair_assign, seed: int, horizon: int, *,
+                env_offset: int = 0, returns=None, trace: "Trace" = None, stream=None):
+        tr = trace.desc if trace is not None else None
+        _check(lib().malib_rollout_batch(
+            self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
+            horizon, _dptr(returns), C.byref(tr) if tr is not None else None,
+            _stream(stream)))
+
+    def payoff(self, reset: bool = False, stream=None, check: bool = True):
+        P = self.P
+        mean = np.zeros((P, P), np.float64)
+        counts = np.zeros((P, P), np.int64)
+        se = np.zeros((P, P), np.float64)
+        st = EvalStats()
+        rc = lib().malib_payoff_eval(self.handle, _stream(stream), int(reset),
+                                     mean.ctypes.data, counts.ctypes.data, se.ctypes.data,
+                                     C.byref(st))
+        if check:
+            _check(rc)
+        out = {"mean": mean, "counts": counts, "stderr": se, "live_frames": st.live_frames,
+               "envs": st.envs, "device_flags": st.device_flags, "status": rc}
+        return out
+
+    def profile_enable(self, on: bool = True):
+        _check(lib().malib_profile_enable(self.handle, int(on)))
+
+    def profile_read(self, kernel: int):
+        ms = C.c_double()
+        n = C.c_int64()
+        _check(lib().malib_profile_read(self.handle, kernel, C.byref(ms), C.byref(n)))
+        return ms.value, n.value
+
+
+class Env:
+    """An environment description (malib_env_desc); keeps its device tensors alive."""
+
+    def __init__(self, kind: int, n_agents: int, n_actions: int, *, team=None, A=None,
+                 grid: int = 0, d: int = 0, W=None, emb=None, u=None,
+                 init_mode: int = INIT_PER_ENV):
+        e = EnvDesc()
+        e.kind, e.n_agents, e.n_actions, e.grid, e.d, e.init_mode = (
+            kind, n_agents, n_actions, grid, d, init_mode)
+        self._keep = [A, W, emb, u]
+        if team is not None:
+            tt = (C.c_int8 * n_agents)(*[int(x) for x in team])
+            self._keep.append(tt)
+            e.team = C.cast(tt, C.POINTER(C.c_int8))
+        e.A, e.W, e.emb, e.u = _dptr(A), _dptr(W), _dptr(emb), _dptr(u)
+        self.desc = e
+        self.n_agents = n_agents
+
+
+class Trace:
+    """Parity trace buffers (malib_trace); any of them may be omitted."""
+
+    def __init__(self, *, actions=None, snap_steps=(), logits=None, states=None, perm=None,
+                 offsets=None):
+        t = TraceDesc()
+        t.actions = _dptr(actions)
+        steps = list(snap_steps)
+        t.n_snap = len(steps)
+        ss = (C.c_int32 * max(1, len(steps)))(*steps)
+        t.snap_steps = C.cast(ss, C.POINTER(C.c_int32))
+        t.logits, t.states = _dptr(logits), _dptr(states)
+        t.perm, t.offsets = _dptr(perm), _dptr(offsets)
+        self._keep = [ss, actions, logits, states, perm, offsets]
+        self.desc = t
+
+
+def meta_sample(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *,
+                env_offset: int = 0, out=None, stream=None):
+    """malib_meta_sample: policy id per (env, seat) drawn from sigma [n_sigma][P]."""
+    import torch
+    s = np.ascontiguousarray(sigma, dtype=np.float32).reshape(-1, n_policies)
+    if out is None:
+        out = torch.empty((n_envs, n_agents), dtype=torch.int32, device="cuda")
+    _check(lib().malib_meta_sample(s.ctypes.data, s.shape[0], n_policies, n_envs, n_agents,
+                                   seed, env_offset, _dptr(out), _stream(stream)))
+    return out
+
+
+def debug_tanh_ref(x, y=None, stream=None):
+    import torch
+    if y is None:
+        y = torch.empty_like(x)
+    _check(lib().malib_debug_tanh_ref(_dptr(x), _dptr(y), x.numel(), _stream(stream)))
+    return y
+
+
+def debug_philox(ctr, key0: int, key1: int, stream=None):
+    import torch
+    out = torch.empty_like(ctr)
+    _check(lib().malib_debug_philox(_dptr(ctr), key0, key1, _dptr(out), ctr.shape[0],
+                                    _stream(stream)))
+    return out

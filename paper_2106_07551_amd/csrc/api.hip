@@ -1,0 +1,657 @@
+// C ABI of libmalib: argument validation, device buffers, the rollout step
+// loop and the payoff table.  Everything after validation is enqueued on the
+// caller's stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "device.hpp"
+#include "internal.hpp"
+
+using namespace malib;
+
+struct malib_pop : public Pop {};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+malib_status fail(malib_status code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                     \
+    do {                                                                                  \
+        hipError_t e_ = (expr);                                                           \
+        if (e_ != hipSuccess)                                                             \
+            return fail(e_ == hipErrorOutOfMemory ? MALIB_E_NOMEM : MALIB_E_HIP,          \
+                        "%s failed: %s", #expr, hipGetErrorString(e_));                   \
+    } while (0)
+
+hipError_t ensure(DevBuf& b, size_t bytes)
+{
+    if (bytes <= b.bytes)
+        return hipSuccess;
+    if (b.ptr) {
+        hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess)
+            return e;
+        e = hipFree(b.ptr);
+        if (e != hipSuccess)
+            return e;
+        b.ptr = nullptr;
+        b.bytes = 0;
+    }
+    size_t want = std::max(bytes, (size_t)256);
+    hipError_t e = hipMalloc(&b.ptr, want);
+    if (e == hipSuccess)
+        b.bytes = want;
+    return e;
+}
+
+void release(DevBuf& b)
+{
+    if (b.ptr)
+        (void)hipFree(b.ptr);
+    b.ptr = nullptr;
+    b.bytes = 0;
+}
+
+int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+// ---- profiling: one event pair per launch of a kernel class
+int prof_begin(Pop& p, int kind, hipStream_t s)
+{
+    if (!p.prof.on)
+        return -1;
+    if (p.prof.used == p.prof.pool.size()) {
+        EventPair ev;
+        if (hipEventCreate(&ev.start) != hipSuccess || hipEventCreate(&ev.stop) != hipSuccess)
+            return -1;
+        p.prof.pool.push_back(ev);
+    }
+    int i = (int)p.prof.used++;
+    p.prof.kind.push_back(kind);
+    (void)hipEventRecord(p.prof.pool[i].start, s);
+    return i;
+}
+
+void prof_end(Pop& p, int i, hipStream_t s)
+{
+    if (i >= 0)
+        (void)hipEventRecord(p.prof.pool[i].stop, s);
+}
+
+int64_t state_bytes_per_env(int kind, int d)
+{
+    switch (kind) {
+    case MALIB_ENV_ITER_MATRIX: return 2;
+    case MALIB_ENV_PURSUIT: return 2;
+    case MALIB_ENV_FEATURE: return 4 * (int64_t)d;
+    default: return 0;
+    }
+}
+
+int64_t snap_bytes_per_env(int kind, int d)
+{
+    switch (kind) {
+    case MALIB_ENV_ITER_MATRIX: return 2;
+    case MALIB_ENV_PURSUIT: return 3;
+    case MALIB_ENV_FEATURE: return 4 * (int64_t)d;
+    default: return 0;
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* malib_last_error(void) { return g_last_error.c_str(); }
+
+// ------------------------------------------------------------------- create
+
+malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_pop_t* out)
+{
+    if (!out)
+        return fail(MALIB_E_INVAL, "out is NULL");
+    *out = nullptr;
+    if (!desc)
+        return fail(MALIB_E_INVAL, "desc is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    const int P = desc->n_policies, A = desc->n_actions;
+    if (P < 1 || P > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d], got %d", kMaxP, P);
+    if (A < 1 || A > kMaxActions)
+        return fail(MALIB_E_INVAL, "n_actions must be in [1, %d], got %d", kMaxActions, A);
+    int in = 0, hid = 0;
+    if (desc->kind == MALIB_POLICY_TABULAR) {
+        if (!desc->tab_logits)
+            return fail(MALIB_E_INVAL, "tabular population needs tab_logits");
+    } else if (desc->kind == MALIB_POLICY_MLP_F32 || desc->kind == MALIB_POLICY_MLP_BF16) {
+        if (desc->n_layers != 3)
+            return fail(MALIB_E_UNSUPPORTED, "MLP populations have 3 layers, got %d",
+                        desc->n_layers);
+        if (!desc->dims || !desc->weights)
+            return fail(MALIB_E_INVAL, "MLP population needs dims and weights");
+        for (int l = 0; l < 3; ++l)
+            if (!desc->weights[l])
+                return fail(MALIB_E_INVAL, "weights[%d] is NULL", l);
+        in = desc->dims[0];
+        hid = desc->dims[1];
+        if (desc->dims[2] != hid)
+            return fail(MALIB_E_UNSUPPORTED, "hidden layers must have equal width (%d, %d)",
+                        desc->dims[1], desc->dims[2]);
+        if (desc->dims[3] != A)
+            return fail(MALIB_E_INVAL, "dims[3] (%d) must equal n_actions (%d)", desc->dims[3],
+                        A);
+        if (desc->kind == MALIB_POLICY_MLP_F32) {
+            if (!(hid == 32 || hid == 64))
+                return fail(MALIB_E_UNSUPPORTED, "fp32 MLP hidden width must be 32 or 64");
+            if (in != 24 || A > 3)
+                return fail(MALIB_E_UNSUPPORTED,
+                            "fp32 MLP policies take the iterated-game observation (24 inputs, "
+                            "<= 3 actions)");
+        } else {
+            if (!(hid == 64 || hid == 128 || hid == 256 || hid == 512))
+                return fail(MALIB_E_UNSUPPORTED, "bf16 MLP hidden width must be 64/128/256/512");
+            if (in < 1 || in > 512)
+                return fail(MALIB_E_UNSUPPORTED, "bf16 MLP input width must be in [1, 512]");
+        }
+    } else {
+        return fail(MALIB_E_INVAL, "unknown policy kind %d", desc->kind);
+    }
+
+    malib_pop* p = new (std::nothrow) malib_pop();
+    if (!p)
+        return fail(MALIB_E_NOMEM, "host allocation failed");
+    auto cleanup = [&](malib_status st) {
+        malib_pop_destroy(p);
+        return st;
+    };
+#define TRY(expr)                                                                         \
+    do {                                                                                  \
+        hipError_t e_ = (expr);                                                           \
+        if (e_ != hipSuccess)                                                             \
+            return cleanup(fail(e_ == hipErrorOutOfMemory ? MALIB_E_NOMEM : MALIB_E_HIP,  \
+                                "%s failed: %s", #expr, hipGetErrorString(e_)));          \
+    } while (0)
+    TRY(hipGetDevice(&p->device));
+    p->kind = desc->kind;
+    p->P = P;
+    p->A = A;
+    p->in_dim = in;
+    p->hid = hid;
+    if (desc->kind == MALIB_POLICY_TABULAR) {
+        TRY(hipMalloc((void**)&p->tab, sizeof(float) * P * A));
+        TRY(hipMemcpyAsync(p->tab, desc->tab_logits, sizeof(float) * P * A,
+                           hipMemcpyDeviceToDevice, s));
+    } else {
+        const int dims[4] = {in, hid, hid, A};
+        p->in_pad = round_up(in, 16);
+        for (int l = 0; l < 3; ++l) {
+            int fi = dims[l], fo = dims[l + 1];
+            size_t nb = sizeof(float) * (size_t)P * fo;
+            TRY(hipMalloc((void**)&p->b[l], nb));
+            if (desc->biases && desc->biases[l])
+                TRY(hipMemcpyAsync(p->b[l], desc->biases[l], nb, hipMemcpyDeviceToDevice, s));
+            else
+                TRY(hipMemsetAsync(p->b[l], 0, nb, s));
+            if (desc->kind == MALIB_POLICY_MLP_F32) {
+                size_t wb = sizeof(float) * (size_t)P * fo * fi;
+                TRY(hipMalloc(&p->w[l], wb));
+                TRY(hipMemcpyAsync(p->w[l], desc->weights[l], wb, hipMemcpyDeviceToDevice, s));
+            } else {
+                int ip = l == 0 ? p->in_pad : round_up(fi, 16);
+                int op = round_up(fo, 32);
+                size_t wb = (size_t)P * (op / 32) * (ip / 16) * 64 * 16;
+                TRY(hipMalloc(&p->w[l], wb));
+                TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, p->w[l], s));
+            }
+        }
+    }
+    size_t acc = sizeof(unsigned long long) * (size_t)P * P;
+    TRY(hipMalloc((void**)&p->sum, acc));
+    TRY(hipMalloc((void**)&p->sumsq, acc));
+    TRY(hipMalloc((void**)&p->cnt, acc));
+    TRY(hipMalloc((void**)&p->dev_flags, sizeof(int)));
+    TRY(hipMalloc((void**)&p->dev_frames, sizeof(unsigned long long)));
+    TRY(hipMemsetAsync(p->sum, 0, acc, s));
+    TRY(hipMemsetAsync(p->sumsq, 0, acc, s));
+    TRY(hipMemsetAsync(p->cnt, 0, acc, s));
+    TRY(hipMemsetAsync(p->dev_flags, 0, sizeof(int), s));
+    TRY(hipMemsetAsync(p->dev_frames, 0, sizeof(unsigned long long), s));
+    TRY(hipStreamSynchronize(s));
+#undef TRY
+    *out = p;
+    return MALIB_OK;
+}
+
+void malib_pop_destroy(malib_pop_t p)
+{
+    if (!p)
+        return;
+    (void)hipDeviceSynchronize();
+    for (int l = 0; l < 3; ++l) {
+        if (p->w[l])
+            (void)hipFree(p->w[l]);
+        if (p->b[l])
+            (void)hipFree(p->b[l]);
+    }
+    if (p->tab)
+        (void)hipFree(p->tab);
+    for (void* q : {(void*)p->sum, (void*)p->sumsq, (void*)p->cnt, (void*)p->dev_flags,
+                    (void*)p->dev_frames})
+        if (q)
+            (void)hipFree(q);
+    for (DevBuf* b : {&p->perm, &p->hist, &p->base, &p->offsets, &p->tile_off, &p->logits,
+                      &p->actions, &p->ret, &p->state0, &p->state1, &p->wt, &p->done,
+                      &p->thresholds})
+        release(*b);
+    for (auto& ev : p->prof.pool) {
+        (void)hipEventDestroy(ev.start);
+        (void)hipEventDestroy(ev.stop);
+    }
+    delete p;
+}
+
+// ------------------------------------------------------------------ rollout
+
+malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
+                                 const int32_t* pair_assign, uint64_t seed, int64_t env_offset,
+                                 int32_t horizon, float* returns, const malib_trace* trace,
+                                 void* stream)
+{
+    if (!pop)
+        return fail(MALIB_E_INVAL, "pop is NULL");
+    if (!env)
+        return fail(MALIB_E_INVAL, "env is NULL");
+    if (!pair_assign)
+        return fail(MALIB_E_INVAL, "pair_assign is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    const int n_agents = env->n_agents;
+    if (n_agents < 1 || n_agents > kMaxAgents)
+        return fail(MALIB_E_INVAL, "n_agents must be in [1, %d]", kMaxAgents);
+    if (env->n_actions != pop->A)
+        return fail(MALIB_E_INVAL, "env n_actions (%d) differs from the population's (%d)",
+                    env->n_actions, pop->A);
+    if (n_envs < 1)
+        return fail(MALIB_E_INVAL, "n_envs must be >= 1");
+    if (n_envs * n_agents > ((int64_t)1 << 26))
+        return fail(MALIB_E_INVAL, "n_envs * n_agents exceeds 2^26");
+    if (horizon < 1 || horizon > 100000)
+        return fail(MALIB_E_INVAL, "horizon must be in [1, 100000]");
+    if (env_offset < 0)
+        return fail(MALIB_E_INVAL, "env_offset must be >= 0");
+    if (env->init_mode != MALIB_INIT_PER_ENV && env->init_mode != MALIB_INIT_SHARED)
+        return fail(MALIB_E_INVAL, "unknown init_mode %d", env->init_mode);
+    int8_t team[kMaxAgents];
+    if (env->team) {
+        for (int k = 0; k < n_agents; ++k) {
+            team[k] = env->team[k];
+            if (team[k] != 1 && team[k] != -1)
+                return fail(MALIB_E_INVAL, "team entries must be +1 or -1");
+        }
+    } else {
+        if (n_agents != 2)
+            return fail(MALIB_E_INVAL, "team may be NULL only for two seats");
+        team[0] = 1;
+        team[1] = -1;
+    }
+    EnvArgs ea{};
+    ea.kind = env->kind;
+    ea.n_agents = n_agents;
+    ea.A = env->n_actions;
+    ea.grid = env->grid;
+    ea.d = env->d;
+    ea.init_mode = env->init_mode;
+    for (int k = 0; k < n_agents; ++k) {
+        if (team[k] > 0)
+            ea.team_row |= 1u << k;
+        else
+            ea.team_col |= 1u << k;
+    }
+    ea.Amat = env->A;
+    ea.W = env->W;
+    ea.emb = env->emb;
+    ea.u = env->u;
+    switch (env->kind) {
+    case MALIB_ENV_MATRIX:
+    case MALIB_ENV_ITER_MATRIX:
+        if (n_agents != 2)
+            return fail(MALIB_E_INVAL, "matrix games have two seats");
+        if (!env->A)
+            return fail(MALIB_E_INVAL, "matrix games need A");
+        if (env->kind == MALIB_ENV_ITER_MATRIX && env->n_actions > 3)
+            return fail(MALIB_E_UNSUPPORTED, "iterated matrix game supports <= 3 actions");
+        if (env->kind == MALIB_ENV_ITER_MATRIX && pop->kind != MALIB_POLICY_TABULAR &&
+            pop->in_dim != 8 * env->n_actions)
+            return fail(MALIB_E_INVAL, "policy input width must be 8 * n_actions");
+        if (env->kind == MALIB_ENV_MATRIX && pop->kind != MALIB_POLICY_TABULAR)
+            return fail(MALIB_E_UNSUPPORTED, "the one-step matrix game has no observation; "
+                                             "use tabular policies");
+        break;
+    case MALIB_ENV_PURSUIT:
+        if (n_agents != 2 || env->n_actions != 5 || env->grid < 5 || env->grid > 16)
+            return fail(MALIB_E_INVAL, "pursuit: 2 seats, 5 actions, 5 <= grid <= 16");
+        if (pop->kind == MALIB_POLICY_MLP_F32)
+            return fail(MALIB_E_UNSUPPORTED, "pursuit needs bf16 or tabular policies");
+        if (pop->kind == MALIB_POLICY_MLP_BF16 && pop->in_dim != 75)
+            return fail(MALIB_E_INVAL, "pursuit observation has 75 inputs");
+        break;
+    case MALIB_ENV_FEATURE:
+        if (!(env->d == 64 || env->d == 128 || env->d == 256 || env->d == 512))
+            return fail(MALIB_E_UNSUPPORTED, "feature dimension must be 64/128/256/512");
+        if (!env->W || !env->emb || !env->u)
+            return fail(MALIB_E_INVAL, "feature dynamics need W, emb and u");
+        if (pop->kind == MALIB_POLICY_MLP_F32)
+            return fail(MALIB_E_UNSUPPORTED, "feature games need bf16 or tabular policies");
+        if (pop->kind == MALIB_POLICY_MLP_BF16 && pop->in_dim != env->d)
+            return fail(MALIB_E_INVAL, "policy input width must equal d");
+        break;
+    default:
+        return fail(MALIB_E_INVAL, "unknown environment kind %d", env->kind);
+    }
+    if (ea.team_row == 0 || ea.team_col == 0)
+        return fail(MALIB_E_INVAL, "both sides need at least one seat");
+    std::vector<int> snap_of(horizon, -1);
+    if (trace && trace->n_snap > 0) {
+        if (!trace->snap_steps)
+            return fail(MALIB_E_INVAL, "trace: snap_steps is NULL");
+        for (int i = 0; i < trace->n_snap; ++i) {
+            int st = trace->snap_steps[i];
+            if (st < 0 || st >= horizon)
+                return fail(MALIB_E_INVAL, "trace: snapshot step %d outside [0, %d)", st,
+                            horizon);
+            snap_of[st] = i;
+        }
+    }
+
+    // ---- buffers
+    const int64_t ns = n_envs * n_agents;
+    const bool mlp = pop->kind != MALIB_POLICY_TABULAR;
+    const int tile_rows = pop->kind == MALIB_POLICY_MLP_F32 ? kF32TileRows : kTileRows;
+    const int n_chunks = (int)((ns + kBucketChunk - 1) / kBucketChunk);
+    HIP_TRY(ensure(pop->logits, sizeof(float) * ns * pop->A));
+    HIP_TRY(ensure(pop->actions, ns));
+    HIP_TRY(ensure(pop->ret, sizeof(float) * ns));
+    int64_t sb = state_bytes_per_env(env->kind, env->d) * n_envs;
+    if (sb > 0) {
+        HIP_TRY(ensure(pop->state0, sb));
+        if (env->kind == MALIB_ENV_FEATURE)
+            HIP_TRY(ensure(pop->state1, sb));
+    }
+    if (env->kind == MALIB_ENV_PURSUIT)
+        HIP_TRY(ensure(pop->done, n_envs));
+    if (env->kind == MALIB_ENV_FEATURE)
+        HIP_TRY(ensure(pop->wt, sizeof(float) * env->d * env->d));
+    if (mlp) {
+        HIP_TRY(ensure(pop->perm, sizeof(int32_t) * ns));
+        HIP_TRY(ensure(pop->hist, sizeof(int32_t) * (size_t)pop->P * n_chunks));
+        HIP_TRY(ensure(pop->base, sizeof(int32_t) * (size_t)pop->P * n_chunks));
+        HIP_TRY(ensure(pop->offsets, sizeof(int32_t) * (pop->P + 1)));
+        HIP_TRY(ensure(pop->tile_off, sizeof(int32_t) * (pop->P + 1)));
+    }
+    ea.WT = (const float*)pop->wt.ptr;
+    float* ret = (float*)pop->ret.ptr;
+    float* logits = (float*)pop->logits.ptr;
+    uint8_t* actions = (uint8_t*)pop->actions.ptr;
+    uint8_t* done = env->kind == MALIB_ENV_PURSUIT ? (uint8_t*)pop->done.ptr : nullptr;
+    void* cur = pop->state0.ptr;
+    void* nxt = env->kind == MALIB_ENV_FEATURE ? pop->state1.ptr : pop->state0.ptr;
+    int32_t* perm = (int32_t*)pop->perm.ptr;
+    int32_t* offsets = (int32_t*)pop->offsets.ptr;
+    int32_t* tile_off = (int32_t*)pop->tile_off.ptr;
+
+    // ---- set-up: bucketing, reset, returns
+    int pi = prof_begin(*pop, MALIB_K_SETUP, s);
+    HIP_TRY(hipMemsetAsync(ret, 0, sizeof(float) * ns, s));
+    if (mlp)
+        HIP_TRY(launch_bucket(pair_assign, ns, pop->P, tile_rows, (int32_t*)pop->hist.ptr,
+                              (int32_t*)pop->base.ptr, perm, offsets, tile_off, pop->dev_flags,
+                              s));
+    HIP_TRY(launch_reset(ea, n_envs, seed, env_offset, cur, done, s));
+    if (env->kind == MALIB_ENV_FEATURE)
+        HIP_TRY(launch_transpose(env->W, (float*)pop->wt.ptr, env->d, s));
+    prof_end(*pop, pi, s);
+    if (trace && mlp) {
+        if (trace->perm)
+            HIP_TRY(hipMemcpyAsync(trace->perm, perm, sizeof(int32_t) * ns,
+                                   hipMemcpyDeviceToDevice, s));
+        if (trace->offsets)
+            HIP_TRY(hipMemcpyAsync(trace->offsets, offsets, sizeof(int32_t) * (pop->P + 1),
+                                   hipMemcpyDeviceToDevice, s));
+    }
+
+    // ---- the step loop
+    const int64_t snap_b = snap_bytes_per_env(env->kind, env->d) * n_envs;
+    for (int t = 0; t < horizon; ++t) {
+        int si = snap_of[t];
+        if (si >= 0 && trace->states && snap_b > 0) {
+            uint8_t* dst = (uint8_t*)trace->states + (int64_t)si * snap_b;
+            if (env->kind == MALIB_ENV_PURSUIT)
+                HIP_TRY(launch_snapshot_pursuit(cur, done, n_envs, dst, s));
+            else
+                HIP_TRY(hipMemcpyAsync(dst, cur, snap_b, hipMemcpyDeviceToDevice, s));
+        }
+        pi = prof_begin(*pop, MALIB_K_POLICY, s);
+        if (pop->kind == MALIB_POLICY_TABULAR)
+            HIP_TRY(launch_tabular(pop->tab, pair_assign, ns, pop->A, pop->P, pop->dev_flags,
+                                   logits, s));
+        else if (pop->kind == MALIB_POLICY_MLP_F32)
+            HIP_TRY(launch_mlp_f32(*pop, perm, offsets, tile_off, ns, n_agents, cur, logits, s));
+        else
+            HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d, perm, offsets,
+                                    tile_off, ns, cur, done, logits, s));
+        prof_end(*pop, pi, s);
+        if (si >= 0 && trace->logits)
+            HIP_TRY(hipMemcpyAsync(trace->logits + (int64_t)si * ns * pop->A, logits,
+                                   sizeof(float) * ns * pop->A, hipMemcpyDeviceToDevice, s));
+        pi = prof_begin(*pop, MALIB_K_SAMPLE, s);
+        uint8_t* log = (trace && trace->actions) ? trace->actions + (int64_t)t * ns : nullptr;
+        HIP_TRY(launch_gumbel(logits, n_envs, n_agents, pop->A, seed, env_offset, t, done,
+                              actions, log, pop->dev_flags, s));
+        prof_end(*pop, pi, s);
+        pi = prof_begin(*pop, MALIB_K_ENV, s);
+        HIP_TRY(launch_env_step(ea, n_envs, actions, cur, nxt, done, ret, pop->dev_frames, s));
+        prof_end(*pop, pi, s);
+        std::swap(cur, nxt);
+        if (env->kind != MALIB_ENV_FEATURE)
+            nxt = cur;
+    }
+
+    // ---- payoff reduction
+    pi = prof_begin(*pop, MALIB_K_PAYOFF, s);
+    HIP_TRY(launch_payoff(ret, pair_assign, n_envs, n_agents, team, pop->P, pop->sum,
+                          pop->sumsq, pop->cnt, s));
+    prof_end(*pop, pi, s);
+    if (returns)
+        HIP_TRY(hipMemcpyAsync(returns, ret, sizeof(float) * ns, hipMemcpyDeviceToDevice, s));
+    if (env->kind != MALIB_ENV_PURSUIT)
+        pop->host_frames += ns * (int64_t)horizon;
+    pop->envs += n_envs;
+    return MALIB_OK;
+}
+
+// ------------------------------------------------------------------- payoff
+
+malib_status malib_payoff_eval(malib_pop_t pop, void* stream, int32_t reset, double* mean,
+                               int64_t* counts, double* stderr_out, malib_eval_stats* stats)
+{
+    if (!pop)
+        return fail(MALIB_E_INVAL, "pop is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(hipStreamSynchronize(s));
+    const size_t PP = (size_t)pop->P * pop->P;
+    std::vector<long long> sum(PP), sq(PP), cnt(PP);
+    int flags = 0;
+    unsigned long long frames = 0;
+    HIP_TRY(hipMemcpy(sum.data(), pop->sum, 8 * PP, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(sq.data(), pop->sumsq, 8 * PP, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(cnt.data(), pop->cnt, 8 * PP, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(&flags, pop->dev_flags, sizeof(int), hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(&frames, pop->dev_frames, sizeof(frames), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < PP; ++i) {
+        double n = (double)cnt[i];
+        double m = cnt[i] > 0 ? ldexp((double)sum[i], -32) / n : NAN;
+        if (mean)
+            mean[i] = m;
+        if (counts)
+            counts[i] = cnt[i];
+        if (stderr_out) {
+            if (cnt[i] < 2) {
+                stderr_out[i] = NAN;
+            } else {
+                double s2 = ldexp((double)sq[i], -20);
+                double var = (s2 - n * m * m) / (n - 1.0);
+                stderr_out[i] = sqrt(var > 0.0 ? var / n : 0.0);
+            }
+        }
+    }
+    if (stats) {
+        stats->live_frames = pop->host_frames + (int64_t)frames;
+        stats->envs = pop->envs;
+        stats->device_flags = flags;
+    }
+    if (reset) {
+        HIP_TRY(hipMemset(pop->sum, 0, 8 * PP));
+        HIP_TRY(hipMemset(pop->sumsq, 0, 8 * PP));
+        HIP_TRY(hipMemset(pop->cnt, 0, 8 * PP));
+        HIP_TRY(hipMemset(pop->dev_frames, 0, sizeof(unsigned long long)));
+        pop->host_frames = 0;
+        pop->envs = 0;
+    }
+    if (flags) {
+        HIP_TRY(hipMemset(pop->dev_flags, 0, sizeof(int)));
+        HIP_TRY(hipDeviceSynchronize());
+        return fail(MALIB_E_DEVICE, "device flagged bad data (flags 0x%x:%s%s)", flags,
+                    (flags & kErrPid) ? " policy id out of range" : "",
+                    (flags & kErrNaN) ? " NaN logit" : "");
+    }
+    if (reset)
+        HIP_TRY(hipDeviceSynchronize());
+    return MALIB_OK;
+}
+
+// -------------------------------------------------------------- meta-sample
+
+malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, int64_t n_envs,
+                               int32_t n_agents, uint64_t seed, int64_t env_offset,
+                               int32_t* out, void* stream)
+{
+    if (!sigma || !out)
+        return fail(MALIB_E_INVAL, "sigma and pair_assign_out must not be NULL");
+    if (P < 1 || P > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
+    if (n_agents < 1 || n_agents > kMaxAgents)
+        return fail(MALIB_E_INVAL, "n_agents must be in [1, %d]", kMaxAgents);
+    if (n_sigma != 1 && n_sigma != n_agents)
+        return fail(MALIB_E_INVAL, "n_sigma must be 1 or n_agents");
+    if (n_envs < 0 || n_envs * n_agents > ((int64_t)1 << 26) || env_offset < 0)
+        return fail(MALIB_E_INVAL, "bad n_envs / env_offset");
+    std::vector<unsigned long long> thr((size_t)n_sigma * P);
+    for (int r = 0; r < n_sigma; ++r) {
+        const float* row = sigma + (size_t)r * P;
+        double total = 0.0;
+        for (int m = 0; m < P; ++m) {
+            if (!isfinite(row[m]) || row[m] < 0.0f)
+                return fail(MALIB_E_INVAL, "sigma[%d][%d] is negative or not finite", r, m);
+            total += (double)row[m];
+        }
+        if (!(total > 0.0))
+            return fail(MALIB_E_INVAL, "sigma row %d has zero mass", r);
+        double run = 0.0;
+        for (int m = 0; m < P; ++m) {
+            run += (double)row[m];
+            double c = floor(run / total * 4294967296.0);
+            thr[(size_t)r * P + m] = (unsigned long long)std::min(c, 4294967296.0);
+        }
+        thr[(size_t)r * P + P - 1] = 4294967296ull;
+    }
+    if (n_envs == 0)
+        return MALIB_OK;
+    hipStream_t s = (hipStream_t)stream;
+    // Thresholds live in a device buffer that is freed in stream order; the
+    // copy is staged synchronously from pageable memory before returning.
+    unsigned long long* d_thr = nullptr;
+    size_t nb = sizeof(unsigned long long) * thr.size();
+    HIP_TRY(hipMallocAsync((void**)&d_thr, nb, s));
+    HIP_TRY(hipMemcpyAsync(d_thr, thr.data(), nb, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(launch_meta_sample(d_thr, n_sigma, P, n_envs, n_agents, seed, env_offset, out, s));
+    HIP_TRY(hipFreeAsync(d_thr, s));
+    return MALIB_OK;
+}
+
+// ---------------------------------------------------------------- profiling
+
+malib_status malib_profile_enable(malib_pop_t pop, int32_t enable)
+{
+    if (!pop)
+        return fail(MALIB_E_INVAL, "pop is NULL");
+    pop->prof.on = enable != 0;
+    pop->prof.used = 0;
+    pop->prof.kind.clear();
+    return MALIB_OK;
+}
+
+malib_status malib_profile_read(malib_pop_t pop, int32_t kernel, double* total_ms,
+                                int64_t* launches)
+{
+    if (!pop)
+        return fail(MALIB_E_INVAL, "pop is NULL");
+    if (kernel < 0 || kernel >= MALIB_K_COUNT)
+        return fail(MALIB_E_INVAL, "unknown kernel class %d", kernel);
+    double ms = 0.0;
+    int64_t n = 0;
+    for (size_t i = 0; i < pop->prof.used; ++i) {
+        if (pop->prof.kind[i] != kernel)
+            continue;
+        HIP_TRY(hipEventSynchronize(pop->prof.pool[i].stop));
+        float e = 0.0f;
+        HIP_TRY(hipEventElapsedTime(&e, pop->prof.pool[i].start, pop->prof.pool[i].stop));
+        ms += e;
+        ++n;
+    }
+    if (total_ms)
+        *total_ms = ms;
+    if (launches)
+        *launches = n;
+    return MALIB_OK;
+}
+
+// -------------------------------------------------------------- diagnostics
+
+malib_status malib_debug_tanh_ref(const float* x, float* y, int64_t n, void* stream)
+{
+    if (!x || !y || n < 0)
+        return fail(MALIB_E_INVAL, "bad arguments");
+    if (n == 0)
+        return MALIB_OK;
+    HIP_TRY(launch_debug_tanh(x, y, n, (hipStream_t)stream));
+    return MALIB_OK;
+}
+
+malib_status malib_debug_philox(const uint64_t* ctr, uint64_t key0, uint64_t key1,
+                                uint64_t* out, int64_t n, void* stream)
+{
+    if (!ctr || !out || n < 0)
+        return fail(MALIB_E_INVAL, "bad arguments");
+    if (n == 0)
+        return MALIB_OK;
+    HIP_TRY(launch_debug_philox(ctr, key0, key1, out, n, (hipStream_t)stream));
+    return MALIB_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,135 @@
+// Device primitives shared by the gfx950 kernels: the counter-based random
+// stream, the uniform and Gumbel transforms, bf16 rounding and the fixed
+// tanh of the feature dynamics.  All of it is written for a single fp32
+// environment: no fast-math, no contraction (-ffp-contract=off), correctly
+// rounded fp32 division, fp32 denormals preserved.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace malib {
+
+// Random-stream purposes (third counter word, high half).
+enum : uint32_t { kPurposeAction = 0, kPurposeReset = 1, kPurposeMeta = 2 };
+
+struct u64x4 {
+    uint64_t x, y, z, w;
+};
+
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds, each two
+// 64x64->128-bit products with the round constants, the high halves xor-ed
+// with the other counter words and the key; the key advances by the Weyl
+// increments between rounds.
+__device__ __forceinline__ u64x4 philox4x64_10(u64x4 c, uint64_t k0, uint64_t k1)
+{
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
+        uint64_t lo0 = m0 * c.x, hi0 = __umul64hi(m0, c.x);
+        uint64_t lo1 = m1 * c.z, hi1 = __umul64hi(m1, c.z);
+        u64x4 n;
+        n.x = hi1 ^ c.y ^ k0;
+        n.y = lo1;
+        n.z = hi0 ^ c.w ^ k1;
+        n.w = lo0;
+        c = n;
+        k0 += 0x9E3779B97F4A7C15ull;
+        k1 += 0xBB67AE8584CAA73Bull;
+    }
+    return c;
+}
+
+// The block of the stream at (global env g, step t, purpose, slot, block):
+// counter (g, t, purpose<<32 | slot, block), key (seed, 0).
+__device__ __forceinline__ u64x4 stream_block(uint64_t seed, uint64_t g, uint64_t t,
+                                              uint32_t purpose, uint32_t slot, uint64_t block)
+{
+    u64x4 c{g, t, ((uint64_t)purpose << 32) | slot, block};
+    return philox4x64_10(c, seed, 0);
+}
+
+// 32-bit lane j (0..7) of a block: lane 2w = low half of word w, 2w+1 = high.
+__device__ __forceinline__ uint32_t block_lane(const u64x4& b, int j)
+{
+    uint64_t w = (j >> 1) == 0 ? b.x : (j >> 1) == 1 ? b.y : (j >> 1) == 2 ? b.z : b.w;
+    return (j & 1) ? (uint32_t)(w >> 32) : (uint32_t)w;
+}
+
+// Uniform in (0,1): odd integer 2*(x>>9)+1 (< 2^24, exact in fp32) times 2^-24.
+__device__ __forceinline__ float uniform01(uint32_t x)
+{
+    return (float)(2u * (x >> 9) + 1u) * 0x1p-24f;
+}
+
+// bf16 bits of x, round to nearest even; NaN -> quiet NaN with x's sign.
+__device__ __forceinline__ uint16_t bf16_bits(float x)
+{
+    uint32_t b = __float_as_uint(x);
+    if ((b & 0x7FFFFFFFu) > 0x7F800000u)
+        return (uint16_t)(((b >> 16) & 0x8000u) | 0x7FC0u);
+    b += 0x7FFFu + ((b >> 16) & 1u);
+    return (uint16_t)(b >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
+{
+    return (uint32_t)bf16_bits(lo) | ((uint32_t)bf16_bits(hi) << 16);
+}
+
+// exp_ref: Cody-Waite reduction x = n ln2 + r with ln2 split into a high part
+// (trailing zero bits) and a low part, degree-7 Taylor polynomial of e^r in
+// fused Horner form, exact scaling by 2^n.
+__device__ __forceinline__ float exp_ref(float x)
+{
+    const float log2e = 0x1.715476p+0f;
+    const float ln2_hi = 0x1.62e4p-1f;
+    const float ln2_lo = 0x1.7f7d1cp-20f;
+    float n = rintf(x * log2e);
+    float r = __builtin_fmaf(-n, ln2_hi, x);
+    r = __builtin_fmaf(-n, ln2_lo, r);
+    float p = 0x1.a01a02p-13f;            // 1/7!
+    p = __builtin_fmaf(p, r, 0x1.6c16c2p-10f);  // 1/6!
+    p = __builtin_fmaf(p, r, 0x1.111112p-7f);   // 1/5!
+    p = __builtin_fmaf(p, r, 0x1.555556p-5f);   // 1/4!
+    p = __builtin_fmaf(p, r, 0x1.555556p-3f);   // 1/3!
+    p = __builtin_fmaf(p, r, 0x1p-1f);
+    p = __builtin_fmaf(p, r, 0x1p+0f);
+    p = __builtin_fmaf(p, r, 0x1p+0f);
+    return ldexpf(p, (int)n);
+}
+
+// tanh_ref: |x| < 0.55 -> x + x^3 p(x^2) with p the Taylor series of
+// (tanh x - x)/x^3 through the x^19 term; 0.55 <= |x| <= 9.01 ->
+// sign(x) (1 - 2/(exp_ref(2|x|) + 1)); |x| > 9.01 -> sign(x); NaN and signed
+// zeros unchanged.
+__device__ __forceinline__ float tanh_ref(float x)
+{
+    if (__builtin_isnan(x) || x == 0.0f)
+        return x;
+    float ax = __builtin_fabsf(x);
+    if (ax > 9.01f)
+        return __builtin_copysignf(1.0f, x);
+    if (ax < 0.55f) {
+        float y = x * x;
+        float p = -0x1.f57d78p-13f;
+        p = __builtin_fmaf(p, y, 0x1.355824p-11f);
+        p = __builtin_fmaf(p, y, -0x1.7da364p-10f);
+        p = __builtin_fmaf(p, y, 0x1.d6d3dp-9f);
+        p = __builtin_fmaf(p, y, -0x1.226e36p-7f);
+        p = __builtin_fmaf(p, y, 0x1.664f48p-6f);
+        p = __builtin_fmaf(p, y, -0x1.ba1ba2p-5f);
+        p = __builtin_fmaf(p, y, 0x1.111112p-3f);
+        p = __builtin_fmaf(p, y, -0x1.555556p-2f);
+        float x3 = x * y;
+        return __builtin_fmaf(x3, p, x);
+    }
+    float e = exp_ref(2.0f * ax);
+    float t = 1.0f - 2.0f / (e + 1.0f);
+    return __builtin_copysignf(t, x);
+}
+
+// Device error flags (bit values of malib_eval_stats.device_flags).
+enum : int { kErrPid = 1, kErrNaN = 2 };
+
+}  // namespace malib

@@ -1,0 +1,122 @@
+// Internal interfaces of libmalib: the population handle and the kernel
+// launchers (one translation unit per kernel family).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "malib.h"
+
+namespace malib {
+
+constexpr int kMaxP = 256;
+constexpr int kMaxActions = 32;
+constexpr int kMaxAgents = 8;
+constexpr int kTileRows = 128;     // rows per bf16 MFMA policy tile
+constexpr int kF32TileRows = 64;   // rows per fp32 policy tile (one wavefront)
+constexpr int kBucketChunk = 2048; // slots per bucketing workgroup
+
+// Growable device buffer owned by a handle.
+struct DevBuf {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+};
+
+struct EventPair {
+    hipEvent_t start, stop;
+};
+
+struct Profile {
+    bool on = false;
+    std::vector<EventPair> pool;
+    size_t used = 0;
+    std::vector<int> kind;        // kernel class of each used pair
+};
+
+struct Pop {
+    int kind = 0;
+    int P = 0;
+    int A = 0;
+    int in_dim = 0, hid = 0;
+    int in_pad = 0;               // bf16: input padded to a multiple of 16
+    int device = 0;
+    // packed weights
+    void* w[3] = {nullptr, nullptr, nullptr};   // bf16 fragment layout or fp32 [P][out][in]
+    float* b[3] = {nullptr, nullptr, nullptr};  // fp32 [P][out] (zero-filled when absent)
+    float* tab = nullptr;                       // fp32 [P][A]
+    // payoff accumulators: [P*P] each
+    unsigned long long* sum = nullptr;   // int64 fixed point 2^-32 (two's complement)
+    unsigned long long* sumsq = nullptr; // int64 fixed point 2^-20
+    unsigned long long* cnt = nullptr;
+    int* dev_flags = nullptr;
+    unsigned long long* dev_frames = nullptr;
+    int64_t host_frames = 0;   // frames of env families with no early termination
+    int64_t envs = 0;
+    // scratch, grown on demand
+    DevBuf perm, hist, base, offsets, tile_off, logits, actions, ret, state0, state1, wt,
+        done, thresholds;
+    Profile prof;
+};
+
+// Bucketing of slots by policy id (stable counting sort) + tile table.
+hipError_t launch_bucket(const int32_t* pids, int64_t n_slots, int P, int tile_rows,
+                         int32_t* hist, int32_t* base, int32_t* perm, int32_t* offsets,
+                         int32_t* tile_off, int* flags, hipStream_t s);
+
+// Meta-strategy sampling from precomputed thresholds [n_sigma][P].
+hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
+                              int64_t n_envs, int n_agents, uint64_t seed, int64_t env_offset,
+                              int32_t* out, hipStream_t s);
+
+// Gumbel-max action sampling.
+hipError_t launch_gumbel(const float* logits, int64_t n_envs, int n_agents, int A,
+                         uint64_t seed, int64_t env_offset, int t, const uint8_t* done,
+                         uint8_t* actions, uint8_t* log, int* flags, hipStream_t s);
+
+// Environment kernels.
+struct EnvArgs {
+    int kind, n_agents, A, grid, d, init_mode;
+    uint32_t team_row;   // bit k set: seat k is on the row side (team +1)
+    uint32_t team_col;   // bit k set: seat k is on the column side (team -1)
+    const float* Amat;
+    const float* W;
+    const float* WT;     // transposed W (scratch)
+    const float* emb;
+    const float* u;
+};
+hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,
+                        void* state, uint8_t* done, hipStream_t s);
+hipError_t launch_transpose(const float* W, float* WT, int d, hipStream_t s);
+hipError_t launch_env_step(const EnvArgs& e, int64_t n_envs, const uint8_t* actions,
+                           const void* state_in, void* state_out, uint8_t* done, float* ret,
+                           unsigned long long* frames, hipStream_t s);
+hipError_t launch_snapshot_pursuit(const void* state, const uint8_t* done, int64_t n_envs,
+                                   uint8_t* out, hipStream_t s);
+
+// Payoff reduction (once per batch).
+hipError_t launch_payoff(const float* ret, const int32_t* pids, int64_t n_envs, int n_agents,
+                         const int8_t* team, int P, unsigned long long* sum,
+                         unsigned long long* sumsq, unsigned long long* cnt, hipStream_t s);
+
+// Policy forwards.
+hipError_t launch_pack_bf16(const float* w, int P, int out, int in, int out_pad, int in_pad,
+                            void* dst, hipStream_t s);
+hipError_t launch_tabular(const float* tab, const int32_t* pids, int64_t n_slots, int A, int P,
+                          int* flags, float* logits, hipStream_t s);
+hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int32_t* offsets,
+                          const int32_t* tile_off, int64_t n_slots, int n_agents,
+                          const void* state, float* logits, hipStream_t s);
+hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid, int d,
+                           const int32_t* perm, const int32_t* offsets,
+                           const int32_t* tile_off, int64_t n_slots, const void* state,
+                           const uint8_t* done, float* logits, hipStream_t s);
+
+// Diagnostics.
+hipError_t launch_debug_tanh(const float* x, float* y, int64_t n, hipStream_t s);
+hipError_t launch_debug_philox(const uint64_t* ctr, uint64_t k0, uint64_t k1, uint64_t* out,
+                               int64_t n, hipStream_t s);
+
+}  // namespace malib

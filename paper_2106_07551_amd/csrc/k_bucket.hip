@@ -1,0 +1,176 @@
+// Bucketing of agent slots by policy id: a stable counting sort, so that the
+// grouped policy forward can run each policy's rows as dense tiles with one
+// set of weights.
+//
+//   bucket_hist    per-chunk histograms        hist[p][chunk]
+//   bucket_scan    exclusive scan (pid-major)  base[p][chunk], offsets[P+1],
+//                  tile table tile_off[P+1] (tiles of `tile_rows` rows per policy)
+//   bucket_scatter stable scatter              perm[offsets[p] + rank] = slot
+//
+// Slots are processed in slot order inside each chunk (four waves over
+// consecutive quarters; inside a wave, 64-slot segments in order, peeling one
+// policy id per iteration with a ballot), so equal ids keep slot order.
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace malib {
+
+constexpr int kBucketThreads = 256;
+constexpr int kWaves = kBucketThreads / 64;
+constexpr int kPerWave = kBucketChunk / kWaves;
+
+__device__ __forceinline__ int load_pid(const int32_t* pids, int64_t i, int P, int* flags)
+{
+    int p = pids[i];
+    if (p < 0 || p >= P) {
+        atomicOr(flags, kErrPid);
+        p = 0;
+    }
+    return p;
+}
+
+__global__ __launch_bounds__(kBucketThreads) void bucket_hist_kernel(
+    const int32_t* __restrict__ pids, int64_t n_slots, int P, int n_chunks,
+    int32_t* __restrict__ hist, int* flags)
+{
+    __shared__ int h[kMaxP];
+    for (int p = threadIdx.x; p < P; p += kBucketThreads)
+        h[p] = 0;
+    __syncthreads();
+    int64_t base = (int64_t)blockIdx.x * kBucketChunk;
+    for (int j = threadIdx.x; j < kBucketChunk; j += kBucketThreads) {
+        int64_t i = base + j;
+        if (i < n_slots)
+            atomicAdd(&h[load_pid(pids, i, P, flags)], 1);
+    }
+    __syncthreads();
+    for (int p = threadIdx.x; p < P; p += kBucketThreads)
+        hist[(int64_t)p * n_chunks + blockIdx.x] = h[p];
+}
+
+// Single workgroup of 1024 threads: exclusive scan of hist in pid-major order.
+__global__ __launch_bounds__(1024) void bucket_scan_kernel(
+    const int32_t* __restrict__ hist, int P, int n_chunks, int tile_rows,
+    int32_t* __restrict__ base, int32_t* __restrict__ offsets, int32_t* __restrict__ tile_off)
+{
+    __shared__ int wsum[16];
+    __shared__ int carry_s;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0)
+        carry_s = 0;
+    __syncthreads();
+    int64_t total = (int64_t)P * n_chunks;
+    for (int64_t start = 0; start < total; start += 1024) {
+        int64_t i = start + tid;
+        int v = i < total ? hist[i] : 0;
+        // inclusive scan inside the wave
+        int x = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            int y = __shfl_up(x, off, 64);
+            if (lane >= off)
+                x += y;
+        }
+        if (lane == 63)
+            wsum[wave] = x;
+        __syncthreads();
+        int wpre = 0;
+        for (int w = 0; w < wave; ++w)
+            wpre += wsum[w];
+        int carry = carry_s;
+        if (i < total)
+            base[i] = carry + wpre + x - v;
+        __syncthreads();
+        if (tid == 1023)
+            carry_s = carry + wpre + x;
+        __syncthreads();
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int toff = 0;
+        for (int p = 0; p < P; ++p) {
+            int start = base[(int64_t)p * n_chunks];
+            int end = p + 1 < P ? base[(int64_t)(p + 1) * n_chunks] : carry_s;
+            offsets[p] = start;
+            tile_off[p] = toff;
+            toff += (end - start + tile_rows - 1) / tile_rows;
+        }
+        offsets[P] = carry_s;
+        tile_off[P] = toff;
+    }
+}
+
+__global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
+    const int32_t* __restrict__ pids, int64_t n_slots, int P, int n_chunks,
+    const int32_t* __restrict__ base, int32_t* __restrict__ perm)
+{
+    __shared__ int wcnt[kWaves][kMaxP];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int p = lane; p < P; p += 64)
+        wcnt[wave][p] = 0;
+    __syncthreads();
+    const int64_t wbase = (int64_t)blockIdx.x * kBucketChunk + (int64_t)wave * kPerWave;
+    // per-wave counts of its quarter
+    for (int j = lane; j < kPerWave; j += 64) {
+        int64_t i = wbase + j;
+        if (i < n_slots) {
+            int p = pids[i];
+            p = (p < 0 || p >= P) ? 0 : p;
+            atomicAdd(&wcnt[wave][p], 1);
+        }
+    }
+    __syncthreads();
+    // running destination of each policy for this wave
+    __shared__ int run[kWaves][kMaxP];
+    for (int p = tid; p < P; p += kBucketThreads) {
+        int acc = base[(int64_t)p * n_chunks + blockIdx.x];
+        for (int w = 0; w < kWaves; ++w) {
+            run[w][p] = acc;
+            acc += wcnt[w][p];
+        }
+    }
+    __syncthreads();
+    const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int seg = 0; seg < kPerWave; seg += 64) {
+        int64_t i = wbase + seg + lane;
+        bool valid = i < n_slots;
+        int p = 0;
+        if (valid) {
+            p = pids[i];
+            p = (p < 0 || p >= P) ? 0 : p;
+        }
+        bool pending = valid;
+        while (__ballot(pending) != 0ull) {
+            unsigned long long act = __ballot(pending);
+            int leader = __ffsll((unsigned long long)act) - 1;
+            int lp = __shfl(p, leader, 64);
+            bool mine = pending && p == lp;
+            unsigned long long m = __ballot(mine);
+            int dst0 = run[wave][lp];
+            if (mine) {
+                int rank = __popcll(m & lt_mask);
+                perm[dst0 + rank] = (int32_t)i;
+            }
+            if (lane == leader)
+                run[wave][lp] = dst0 + __popcll(m);
+            if (mine)
+                pending = false;
+        }
+    }
+}
+
+hipError_t launch_bucket(const int32_t* pids, int64_t n_slots, int P, int tile_rows,
+                         int32_t* hist, int32_t* base, int32_t* perm, int32_t* offsets,
+                         int32_t* tile_off, int* flags, hipStream_t s)
+{
+    int n_chunks = (int)((n_slots + kBucketChunk - 1) / kBucketChunk);
+    bucket_hist_kernel<<<n_chunks, kBucketThreads, 0, s>>>(pids, n_slots, P, n_chunks, hist,
+                                                           flags);
+    bucket_scan_kernel<<<1, 1024, 0, s>>>(hist, P, n_chunks, tile_rows, base, offsets,
+                                          tile_off);
+    bucket_scatter_kernel<<<n_chunks, kBucketThreads, 0, s>>>(pids, n_slots, P, n_chunks,
+                                                              base, perm);
+    return hipGetLastError();
+}
+
+}  // namespace malib

@@ -1,0 +1,418 @@
+// Environment kernels: reset, one step of each family with return
+// accumulation, and the payoff-table reduction.
+//
+// State layouts (struct of arrays, coalesced per env index):
+//   ITER_MATRIX  uint16 [n_envs]         joint action per lag in 4-bit fields,
+//                                        lag 1 in the low nibble, 15 = none
+//   PURSUIT      uint8  [2][n_envs]      pursuer cell, evader cell; done [n_envs]
+//   FEATURE      fp32   [n_envs][d]      double-buffered between steps
+// Returns: fp32 [n_agents][n_envs].
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace malib {
+
+// ---------------------------------------------------------------- reset
+
+__global__ void reset_iter_kernel(uint16_t* __restrict__ hist, int64_t n)
+{
+    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e < n)
+        hist[e] = 0xFFFF;
+}
+
+// Pursuer cell = top 6 bits of lane 0; evader = pursuer + 1 + floor(lane1 *
+// 63 / 2^32) mod 64, so the two never start on the same cell.
+__global__ void reset_pursuit_kernel(uint8_t* __restrict__ pos, uint8_t* __restrict__ done,
+                                     int64_t n, int grid, uint64_t seed, int64_t env_offset,
+                                     int shared)
+{
+    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n)
+        return;
+    uint64_t g = shared ? 0 : (uint64_t)(env_offset + e);
+    u64x4 b = stream_block(seed, g, 0, kPurposeReset, 0, 0);
+    uint32_t x0 = (uint32_t)b.x, x1 = (uint32_t)(b.x >> 32);
+    uint32_t cells = (uint32_t)(grid * grid);
+    uint32_t pc = x0 >> 26;
+    uint32_t shift = (uint32_t)(((uint64_t)x1 * (uint64_t)(cells - 1)) >> 32);
+    uint32_t ec = (pc + 1 + shift) % cells;
+    pos[e] = (uint8_t)pc;
+    pos[n + e] = (uint8_t)ec;
+    done[e] = 0;
+}
+
+// s0[k] = (2*(x_k>>9)+1 - 2^23) * 2^-23 with x_k lane k%8 of block k/8.
+// One thread per (env, block of 8 coordinates).
+__global__ void reset_feature_kernel(float* __restrict__ s, int64_t n, int d, uint64_t seed,
+                                     int64_t env_offset, int shared)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int nb = d / 8;
+    if (i >= n * nb)
+        return;
+    int64_t e = i / nb;
+    int blk = (int)(i - e * nb);
+    uint64_t g = shared ? 0 : (uint64_t)(env_offset + e);
+    u64x4 b = stream_block(seed, g, 0, kPurposeReset, 0, (uint64_t)blk);
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        int32_t odd = (int32_t)(2u * (block_lane(b, j) >> 9) + 1u);
+        v[j] = (float)(odd - (1 << 23)) * 0x1p-23f;
+    }
+    float4* dst = reinterpret_cast<float4*>(s + e * d + blk * 8);
+    dst[0] = make_float4(v[0], v[1], v[2], v[3]);
+    dst[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,
+                        void* state, uint8_t* done, hipStream_t s)
+{
+    int shared = e.init_mode == MALIB_INIT_SHARED;
+    if (e.kind == MALIB_ENV_ITER_MATRIX) {
+        reset_iter_kernel<<<(int)((n_envs + 255) / 256), 256, 0, s>>>((uint16_t*)state, n_envs);
+    } else if (e.kind == MALIB_ENV_PURSUIT) {
+        reset_pursuit_kernel<<<(int)((n_envs + 255) / 256), 256, 0, s>>>(
+            (uint8_t*)state, done, n_envs, e.grid, seed, env_offset, shared);
+    } else if (e.kind == MALIB_ENV_FEATURE) {
+        int64_t total = n_envs * (e.d / 8);
+        reset_feature_kernel<<<(int)((total + 255) / 256), 256, 0, s>>>(
+            (float*)state, n_envs, e.d, seed, env_offset, shared);
+    }
+    return hipGetLastError();
+}
+
+__global__ void transpose_kernel(const float* __restrict__ W, float* __restrict__ WT, int d)
+{
+    __shared__ float tile[32][33];
+    int bx = blockIdx.x * 32, by = blockIdx.y * 32;
+    int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;   // 32 x 8
+    for (int r = ty; r < 32; r += 8)
+        tile[r][tx] = W[(int64_t)(by + r) * d + bx + tx];
+    __syncthreads();
+    for (int r = ty; r < 32; r += 8)
+        WT[(int64_t)(bx + r) * d + by + tx] = tile[tx][r];
+}
+
+hipError_t launch_transpose(const float* W, float* WT, int d, hipStream_t s)
+{
+    dim3 grid(d / 32, d / 32);
+    transpose_kernel<<<grid, 256, 0, s>>>(W, WT, d);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------- matrix / iterated / pursuit
+
+// One thread per env.  MATRIX and ITER_MATRIX: r0 = A[a0][a1], r1 = -r0;
+// ITER also shifts the joint action into its history.
+__global__ void step_matrix_kernel(const float* __restrict__ Amat, int A, int iter,
+                                   int64_t n, const uint8_t* __restrict__ act,
+                                   uint16_t* __restrict__ hist, float* __restrict__ ret)
+{
+    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n)
+        return;
+    int a0 = act[2 * e], a1 = act[2 * e + 1];
+    float v = Amat[a0 * A + a1];
+    ret[e] = ret[e] + v;
+    ret[n + e] = ret[n + e] + (-v);
+    if (iter) {
+        uint32_t h = hist[e];
+        hist[e] = (uint16_t)(((h << 4) | (uint32_t)(a0 * 3 + a1)) & 0xFFFFu);
+    }
+}
+
+__device__ __forceinline__ uint32_t torus_move(uint32_t cell, int a, int grid)
+{
+    int x = (int)cell % grid, y = (int)cell / grid;
+    if (a == 1)
+        y = (y + grid - 1) % grid;
+    else if (a == 2)
+        y = (y + 1) % grid;
+    else if (a == 3)
+        x = (x + grid - 1) % grid;
+    else if (a == 4)
+        x = (x + 1) % grid;
+    return (uint32_t)(y * grid + x);
+}
+
+// One thread per env.  Simultaneous moves; capture if the two land on the
+// same cell or swap cells: pursuer +1, evader -1, env done.  Counts live
+// agent-frames (two per live env) with one atomic per workgroup.
+__global__ __launch_bounds__(256) void step_pursuit_kernel(
+    int grid, int64_t n, const uint8_t* __restrict__ act, uint8_t* __restrict__ pos,
+    uint8_t* __restrict__ done, float* __restrict__ ret, unsigned long long* frames)
+{
+    __shared__ int live_s;
+    if (threadIdx.x == 0)
+        live_s = 0;
+    __syncthreads();
+    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int live = 0;
+    if (e < n && !done[e]) {
+        live = 1;
+        uint32_t p0 = pos[e], e0 = pos[n + e];
+        uint32_t p1 = torus_move(p0, act[2 * e], grid);
+        uint32_t e1 = torus_move(e0, act[2 * e + 1], grid);
+        pos[e] = (uint8_t)p1;
+        pos[n + e] = (uint8_t)e1;
+        if (p1 == e1 || (p1 == e0 && e1 == p0)) {
+            done[e] = 1;
+            ret[e] = ret[e] + 1.0f;
+            ret[n + e] = ret[n + e] + (-1.0f);
+        }
+    }
+    unsigned long long b = __ballot(live);
+    if ((threadIdx.x & 63) == 0 && b)
+        atomicAdd(&live_s, __popcll(b));
+    __syncthreads();
+    if (threadIdx.x == 0 && live_s)
+        atomicAdd(frames, (unsigned long long)live_s * 2ull);
+}
+
+// ------------------------------------------------------------ feature dynamics
+
+// One workgroup of 256 threads owns 32 envs and all D outputs of each:
+//   s'[e][k] = tanh_ref( fma-chain_{c=0..D-1}(W[k][c], s[e][c]) + emb[0][a_0][k]
+//                        + emb[1][a_1][k] + ... )
+// Thread (tx = tid%64, ty = tid/64) keeps the accumulators of envs ty*8..ty*8+7
+// and outputs tx + 64j; the input index c runs in ascending order through
+// LDS-staged chunks of WT (c-major) and of the state (so every accumulator
+// sees exactly the sequential fused chain, no split of the sum).  The reward
+// r = u . s' is then a sequential fused chain per env over the staged s'.
+constexpr int kFeatEnvs = 32;
+constexpr int kFeatKC = 32;
+
+template <int D>
+__global__ __launch_bounds__(256) void step_feature_kernel(
+    const float* __restrict__ WT, const float* __restrict__ emb, const float* __restrict__ u,
+    EnvArgs ea, int64_t n, const uint8_t* __restrict__ act, const float* __restrict__ s_in,
+    float* __restrict__ s_out, float* __restrict__ ret)
+{
+    constexpr int NJ = D / 64;
+    constexpr int SSTR = kFeatEnvs + 4;
+    constexpr int WS_FLOATS = kFeatKC * D > kFeatEnvs * (D + 1) ? kFeatKC * D : kFeatEnvs * (D + 1);
+    __shared__ __attribute__((aligned(16))) float Ws[WS_FLOATS];
+    __shared__ __attribute__((aligned(16))) float Ss[kFeatKC * SSTR];
+    const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
+    const int64_t e0 = (int64_t)blockIdx.x * kFeatEnvs;
+
+    float acc[8][NJ];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+            acc[i][j] = 0.0f;
+
+    for (int c0 = 0; c0 < D; c0 += kFeatKC) {
+        // WT rows c0..c0+KC-1 (each D floats) -> Ws[c][k]
+        const float4* src = reinterpret_cast<const float4*>(WT + (int64_t)c0 * D);
+        float4* dst = reinterpret_cast<float4*>(Ws);
+        for (int q = tid; q < kFeatKC * D / 4; q += 256)
+            dst[q] = src[q];
+        // state chunk: env el, columns c0 + 4*cq .. +3 -> Ss[c][el]
+        {
+            int el = tid >> 3, cq = tid & 7;
+            int64_t e = e0 + el;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (e < n)
+                v = *reinterpret_cast<const float4*>(s_in + e * D + c0 + cq * 4);
+            Ss[(cq * 4 + 0) * SSTR + el] = v.x;
+            Ss[(cq * 4 + 1) * SSTR + el] = v.y;
+            Ss[(cq * 4 + 2) * SSTR + el] = v.z;
+            Ss[(cq * 4 + 3) * SSTR + el] = v.w;
+        }
+        __syncthreads();
+#pragma unroll 4
+        for (int c = 0; c < kFeatKC; ++c) {
+            float w[NJ];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                w[j] = Ws[c * D + tx + 64 * j];
+            const float4* sp = reinterpret_cast<const float4*>(&Ss[c * SSTR + ty * 8]);
+            float4 sa = sp[0], sb = sp[1];
+            float sv[8] = {sa.x, sa.y, sa.z, sa.w, sb.x, sb.y, sb.z, sb.w};
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    acc[i][j] = __builtin_fmaf(w[j], sv[i], acc[i][j]);
+        }
+        __syncthreads();
+    }
+
+    // epilogue: embeddings in seat order, tanh_ref, store s' (global + LDS)
+    float* Sl = Ws;   // [32][D+1]
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        int el = ty * 8 + i;
+        int64_t e = e0 + el;
+        if (e < n) {
+            const uint8_t* ae = act + e * ea.n_agents;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                int k = tx + 64 * j;
+                float pre = acc[i][j];
+                for (int q = 0; q < ea.n_agents; ++q)
+                    pre = pre + emb[((int64_t)q * ea.A + ae[q]) * D + k];
+                float sn = tanh_ref(pre);
+                s_out[e * D + k] = sn;
+                Sl[el * (D + 1) + k] = sn;
+            }
+        }
+    }
+    __syncthreads();
+    if (tid < kFeatEnvs) {
+        int64_t e = e0 + tid;
+        if (e < n) {
+            float r = 0.0f;
+            const float* row = Sl + tid * (D + 1);
+            for (int k = 0; k < D; ++k)
+                r = __builtin_fmaf(u[k], row[k], r);
+            for (int q = 0; q < ea.n_agents; ++q) {
+                float v = ((ea.team_row >> q) & 1u) ? r : -r;
+                ret[(int64_t)q * n + e] = ret[(int64_t)q * n + e] + v;
+            }
+        }
+    }
+}
+
+hipError_t launch_env_step(const EnvArgs& e, int64_t n_envs, const uint8_t* actions,
+                           const void* state_in, void* state_out, uint8_t* done, float* ret,
+                           unsigned long long* frames, hipStream_t s)
+{
+    int blocks = (int)((n_envs + 255) / 256);
+    switch (e.kind) {
+    case MALIB_ENV_MATRIX:
+        step_matrix_kernel<<<blocks, 256, 0, s>>>(e.Amat, e.A, 0, n_envs, actions, nullptr, ret);
+        break;
+    case MALIB_ENV_ITER_MATRIX:
+        step_matrix_kernel<<<blocks, 256, 0, s>>>(e.Amat, e.A, 1, n_envs, actions,
+                                                  (uint16_t*)state_out, ret);
+        break;
+    case MALIB_ENV_PURSUIT:
+        step_pursuit_kernel<<<blocks, 256, 0, s>>>(e.grid, n_envs, actions, (uint8_t*)state_out,
+                                                   done, ret, frames);
+        break;
+    case MALIB_ENV_FEATURE: {
+        int fb = (int)((n_envs + kFeatEnvs - 1) / kFeatEnvs);
+        const float* si = (const float*)state_in;
+        float* so = (float*)state_out;
+        if (e.d == 64)
+            step_feature_kernel<64><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+        else if (e.d == 128)
+            step_feature_kernel<128><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+        else if (e.d == 256)
+            step_feature_kernel<256><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+        else if (e.d == 512)
+            step_feature_kernel<512><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+        else
+            return hipErrorInvalidValue;
+        break;
+    }
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// PURSUIT snapshot in the trace format [n_envs][3] = (pursuer, evader, done).
+__global__ void snapshot_pursuit_kernel(const uint8_t* __restrict__ pos,
+                                        const uint8_t* __restrict__ done, int64_t n,
+                                        uint8_t* __restrict__ out)
+{
+    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n)
+        return;
+    out[3 * e] = pos[e];
+    out[3 * e + 1] = pos[n + e];
+    out[3 * e + 2] = done[e];
+}
+
+hipError_t launch_snapshot_pursuit(const void* state, const uint8_t* done, int64_t n_envs,
+                                   uint8_t* out, hipStream_t s)
+{
+    snapshot_pursuit_kernel<<<(int)((n_envs + 255) / 256), 256, 0, s>>>(
+        (const uint8_t*)state, done, n_envs, out);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ payoff reduction
+
+// One thread per env.  Every (row-side seat a, column-side seat b) pair adds
+// the fixed-point return of seat a (2^-32 units; squares in 2^-20 units) and a
+// count to cell (pid[a], pid[b]).  When a whole wavefront targets one cell
+// (blocked assignments), it reduces with shuffles and issues one set of
+// atomics; otherwise each lane adds its own.
+__device__ __forceinline__ long long wave_sum_i64(long long v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+__global__ __launch_bounds__(256) void payoff_kernel(
+    const float* __restrict__ ret, const int32_t* __restrict__ pids, int64_t n, int n_agents,
+    EnvArgs ea, int P, unsigned long long* __restrict__ sum,
+    unsigned long long* __restrict__ sumsq, unsigned long long* __restrict__ cnt)
+{
+    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool valid = e < n;
+    for (int a = 0; a < n_agents; ++a) {
+        if (!((ea.team_row >> a) & 1u))
+            continue;
+        long long fx = 0, fsq = 0;
+        if (valid) {
+            double g = (double)ret[(int64_t)a * n + e];
+            fx = __double2ll_rn(g * 4294967296.0);
+            fsq = __double2ll_rn(g * g * 1048576.0);
+        }
+        for (int b = 0; b < n_agents; ++b) {
+            if (!((ea.team_col >> b) & 1u))
+                continue;
+            int cell = -1;
+            if (valid) {
+                int pa = pids[e * n_agents + a], pb = pids[e * n_agents + b];
+                if (pa >= 0 && pa < P && pb >= 0 && pb < P)
+                    cell = pa * P + pb;
+            }
+            int c0 = __shfl(cell, 0, 64);
+            bool uniform = __ballot(cell != c0) == 0ull;
+            if (uniform) {
+                if (c0 >= 0) {
+                    long long s1 = wave_sum_i64(fx), s2 = wave_sum_i64(fsq);
+                    long long c = wave_sum_i64(cell >= 0 ? 1 : 0);
+                    if ((threadIdx.x & 63) == 0) {
+                        atomicAdd(&sum[c0], (unsigned long long)s1);
+                        atomicAdd(&sumsq[c0], (unsigned long long)s2);
+                        atomicAdd(&cnt[c0], (unsigned long long)c);
+                    }
+                }
+            } else if (cell >= 0) {
+                atomicAdd(&sum[cell], (unsigned long long)fx);
+                atomicAdd(&sumsq[cell], (unsigned long long)fsq);
+                atomicAdd(&cnt[cell], 1ull);
+            }
+        }
+    }
+}
+
+hipError_t launch_payoff(const float* ret, const int32_t* pids, int64_t n_envs, int n_agents,
+                         const int8_t* team, int P, unsigned long long* sum,
+                         unsigned long long* sumsq, unsigned long long* cnt, hipStream_t s)
+{
+    EnvArgs ea{};
+    for (int k = 0; k < n_agents; ++k) {
+        if (team[k] > 0)
+            ea.team_row |= 1u << k;
+        else if (team[k] < 0)
+            ea.team_col |= 1u << k;
+    }
+    payoff_kernel<<<(int)((n_envs + 255) / 256), 256, 0, s>>>(ret, pids, n_envs, n_agents, ea,
+                                                              P, sum, sumsq, cnt);
+    return hipGetLastError();
+}
+
+}  // namespace malib

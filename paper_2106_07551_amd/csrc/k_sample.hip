@@ -1,0 +1,142 @@
+// Sampling kernels: meta-strategy draws (policy id per env seat) and
+// Gumbel-max action sampling, both on the Philox4x64-10 stream.
+#include "device.hpp"
+#include "internal.hpp"
+
+namespace malib {
+
+// One thread per (env, seat).  pid = min{m : x < T[m]} for the first lane x
+// of block (g, 0, kPurposeMeta<<32 | seat, 0); T is non-decreasing with
+// T[P-1] = 2^32, so the binary search always lands inside [0, P).
+__global__ void meta_sample_kernel(const unsigned long long* __restrict__ thr, int n_sigma,
+                                   int P, int64_t n_envs, int n_agents, uint64_t seed,
+                                   int64_t env_offset, int32_t* __restrict__ out)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t total = n_envs * n_agents;
+    if (i >= total)
+        return;
+    int64_t e = i / n_agents;
+    int seat = (int)(i - e * n_agents);
+    u64x4 blk = stream_block(seed, (uint64_t)(env_offset + e), 0, kPurposeMeta, seat, 0);
+    unsigned long long x = (uint32_t)blk.x;
+    const unsigned long long* T = thr + (n_sigma == 1 ? 0 : seat) * P;
+    int lo = 0, hi = P - 1;
+    while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (x < T[mid])
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    out[i] = lo;
+}
+
+hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
+                              int64_t n_envs, int n_agents, uint64_t seed, int64_t env_offset,
+                              int32_t* out, hipStream_t s)
+{
+    int64_t total = n_envs * n_agents;
+    int blocks = (int)((total + 255) / 256);
+    meta_sample_kernel<<<blocks, 256, 0, s>>>(thr, n_sigma, P, n_envs, n_agents, seed,
+                                              env_offset, out);
+    return hipGetLastError();
+}
+
+// One thread per slot (env * n_agents + seat).  z_a = l_a + g_a with
+// g_a = -log(-log u_a) in fp32, u_a from lane a%8 of block a/8 of (g, t,
+// kPurposeAction<<32 | seat); the first index of the maximum wins.  Finished
+// envs (done != 0) take no action (255).
+__global__ void gumbel_kernel(const float* __restrict__ logits, int64_t n_envs, int n_agents,
+                              int A, uint64_t seed, int64_t env_offset, int t,
+                              const uint8_t* __restrict__ done, uint8_t* __restrict__ actions,
+                              uint8_t* __restrict__ log, int* flags)
+{
+    int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (slot >= n_envs * n_agents)
+        return;
+    int64_t e = slot / n_agents;
+    int seat = (int)(slot - e * n_agents);
+    uint8_t best = 255;
+    if (!(done && done[e])) {
+        const float* l = logits + slot * A;
+        float zbest = 0.0f;
+        bool nan = false;
+        u64x4 blk{0, 0, 0, 0};
+        for (int a = 0; a < A; ++a) {
+            if ((a & 7) == 0)
+                blk = stream_block(seed, (uint64_t)(env_offset + e), (uint64_t)t,
+                                   kPurposeAction, seat, (uint64_t)(a >> 3));
+            float u = uniform01(block_lane(blk, a & 7));
+            float g = -logf(-logf(u));
+            float la = l[a];
+            nan |= __builtin_isnan(la);
+            float z = la + g;
+            if (a == 0 || z > zbest) {
+                zbest = z;
+                best = (uint8_t)a;
+            }
+        }
+        if (nan) {
+            atomicOr(flags, kErrNaN);
+            best = 0;
+        }
+    }
+    actions[slot] = best;
+    if (log)
+        log[slot] = best;
+}
+
+hipError_t launch_gumbel(const float* logits, int64_t n_envs, int n_agents, int A,
+                         uint64_t seed, int64_t env_offset, int t, const uint8_t* done,
+                         uint8_t* actions, uint8_t* log, int* flags, hipStream_t s)
+{
+    int64_t total = n_envs * n_agents;
+    int blocks = (int)((total + 255) / 256);
+    gumbel_kernel<<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset, t,
+                                         done, actions, log, flags);
+    return hipGetLastError();
+}
+
+__global__ void debug_tanh_kernel(const float* __restrict__ x, float* __restrict__ y, int64_t n)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (; i < n; i += stride)
+        y[i] = tanh_ref(x[i]);
+}
+
+hipError_t launch_debug_tanh(const float* x, float* y, int64_t n, hipStream_t s)
+{
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 65536)
+        blocks = 65536;
+    if (blocks < 1)
+        blocks = 1;
+    debug_tanh_kernel<<<(int)blocks, 256, 0, s>>>(x, y, n);
+    return hipGetLastError();
+}
+
+__global__ void debug_philox_kernel(const uint64_t* __restrict__ ctr, uint64_t k0, uint64_t k1,
+                                    uint64_t* __restrict__ out, int64_t n)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n)
+        return;
+    u64x4 c{ctr[4 * i], ctr[4 * i + 1], ctr[4 * i + 2], ctr[4 * i + 3]};
+    u64x4 r = philox4x64_10(c, k0, k1);
+    out[4 * i] = r.x;
+    out[4 * i + 1] = r.y;
+    out[4 * i + 2] = r.z;
+    out[4 * i + 3] = r.w;
+}
+
+hipError_t launch_debug_philox(const uint64_t* ctr, uint64_t k0, uint64_t k1, uint64_t* out,
+                               int64_t n, hipStream_t s)
+{
+    int blocks = (int)((n + 255) / 256);
+    debug_philox_kernel<<<blocks, 256, 0, s>>>(ctr, k0, k1, out, n);
+    return hipGetLastError();
+}
+
+}  // namespace malib

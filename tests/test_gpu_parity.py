@@ -1,0 +1,233 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Reduced sizes that the oracle finishes in seconds but that still span several
+policy tiles and a ragged tail; full-size sampled checks live in
+test_gpu_fullsize.py.  Bars: integer/byte/index results and the environment
+state bit for bit (given the same actions); logits within 1e-5 (fp32) /
+1e-2 (bf16) relative to max(1, max|l|); actions equal except counted near
+ties; payoff entries within 1e-3; counts exact.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from gpu_helpers import check_parity, run_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2106_07551_amd as M
+    M.lib()
+
+
+# ------------------------------------------------------------ kernel pieces
+
+def test_philox_device_matches_oracle():
+    import paper_2106_07551_amd as M
+    rng = np.random.default_rng(1)
+    ctr = rng.integers(0, 2**64 - 1, size=(4096, 4), dtype=np.uint64)
+    ctr[:3] = [[0, 0, 0, 0], [2**64 - 1] * 4, [5, 6, (2 << 32) | 3, 1]]
+    key = (0x452821E638D01377, 0xBE5466CF34E90C6C)
+    out = M.debug_philox(torch.from_numpy(ctr.view(np.int64)).cuda(), *key).cpu().numpy()
+    out = out.view(np.uint64)
+    for i in range(0, 4096, 37):
+        assert np.array_equal(out[i], oracle.philox(ctr[i], key)), i
+
+
+def test_tanh_ref_device_bitwise_sampled():
+    """tanh_ref on the device equals the oracle's bit for bit on a strided
+    sample of all 2^32 patterns plus every pattern of [0.25, 16) (both signs)."""
+    import paper_2106_07551_amd as M
+    chunks = [np.arange(0, 2**32, 251, dtype=np.uint64).astype(np.uint32)]
+    lo = np.array([0.25], np.float32).view(np.uint32)[0]
+    hi = np.array([16.0], np.float32).view(np.uint32)[0]
+    dense = np.arange(lo, hi, dtype=np.uint32)
+    chunks += [dense, dense | np.uint32(0x80000000)]
+    for bits in chunks:
+        x = bits.view(np.float32)
+        y = M.debug_tanh_ref(torch.from_numpy(x.copy()).cuda()).cpu().numpy()
+        ref = oracle.tanh_many(x)
+        same = (y.view(np.uint32) == ref.view(np.uint32)) | (np.isnan(y) & np.isnan(ref))
+        assert same.all(), hex(int(bits[np.argmin(same)]))
+
+
+@pytest.mark.parametrize("c", [3, 5])
+def test_meta_sample_device_matches_oracle(c):
+    import paper_2106_07551_amd as M
+    wl = W.make(c)
+    n = 3001
+    for off in (0, 12345):
+        g = M.meta_sample(wl.sigma, wl.P, n, wl.n_agents, wl.seed, env_offset=off)
+        ref = oracle.meta_sample(wl.sigma, wl.P, n, wl.n_agents, wl.seed, off)
+        assert np.array_equal(g.cpu().numpy(), ref)
+
+
+def test_meta_sample_per_seat_rows_and_errors():
+    import paper_2106_07551_amd as M
+    P = 9
+    s = np.random.default_rng(2).random((3, P)).astype(np.float32)
+    s[1, :4] = 0
+    g = M.meta_sample(s, P, 500, 3, 77).cpu().numpy()
+    assert np.array_equal(g, oracle.meta_sample(s, P, 500, 3, 77))
+    assert g[:, 1].min() >= 4
+    for bad in (np.array([1, -1], np.float32), np.array([0, 0], np.float32),
+                np.array([np.nan, 1], np.float32)):
+        with pytest.raises(M.MalibError):
+            M.meta_sample(bad, 2, 10, 1, 1)
+
+
+# ------------------------------------------------------------ parity by workload
+
+def test_parity_matrix_full():
+    """One-step matrix game at its full size (16 pairs x 1024 envs)."""
+    wl = W.make(1)
+    g = run_gpu(wl, snaps=[0])
+    check_parity(wl, g)
+
+
+def test_parity_iter_ragged():
+    """Iterated game, fp32 MLP: 4 policies x 50 envs per pair (400 rows per
+    policy = 6 full 64-row tiles + a ragged one), horizon 32."""
+    wl = W.make(2, P=4, per_pair=50)
+    g = run_gpu(wl, snaps=[0, 1, 5, 31])
+    check_parity(wl, g)
+
+
+def test_parity_pursuit_ragged():
+    """Pursuit, bf16 MLP 75-256-256-5, full population of 32, 300 envs with
+    uniformly sampled pairs (ragged 128-row tiles), horizon 100 with captures."""
+    wl = W.make(3, n_envs=300)
+    g = run_gpu(wl, snaps=[0, 3, 50, 99])
+    rep = check_parity(wl, g)
+    assert (g["actions"] == 255).any(), "expected some captures"
+
+
+def test_parity_feature_ragged():
+    """Feature dynamics d=512, bf16 MLP 512-512-512-18: 4 policies x 5 envs per
+    pair, horizon 8."""
+    wl = W.make(4, P=4, per_pair=5, horizon=8)
+    g = run_gpu(wl, snaps=[0, 4, 7])
+    check_parity(wl, g)
+
+
+def test_parity_team_reduced():
+    """4v4 team game d=256, bf16 MLP 256-512-512-18, 16 policies from a
+    Dirichlet meta-strategy, 100 envs, horizon 6."""
+    wl = W.make(5, P=16, n_envs=100, horizon=6)
+    g = run_gpu(wl, snaps=[0, 3, 5])
+    check_parity(wl, g)
+
+
+@pytest.mark.parametrize("hid", [64, 128, 256])
+def test_parity_team_2v2_hidden_widths(hid):
+    """2v2 feature game with narrower hidden layers (other MFMA wave splits)."""
+    wl = W.team_variant(4, P=6, n_envs=150, horizon=3, dims=[256, hid, hid, 18])
+    g = run_gpu(wl, snaps=[0, 2])
+    check_parity(wl, g)
+
+
+def test_parity_feature_shared_init_d64():
+    wl = W.team_variant(2, d=64, P=3, n_envs=70, horizon=5, dims=[64, 64, 64, 18])
+    wl.init_mode = W.INIT_SHARED
+    g = run_gpu(wl, snaps=[0, 4])
+    check_parity(wl, g)
+    assert np.all(g["states"][0] == g["states"][0][0])
+
+
+# ------------------------------------------------------------ invariants
+
+def test_determinism_and_shard_merge():
+    """Same seed twice gives identical tables; two half batches with
+    env_offset give the same returns and table as one batch."""
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(3, n_envs=2000, horizon=30)
+    pop = IO.make_population(wl)
+    env = IO.make_env(wl)
+    full = IO.make_pairs(wl)
+    r1 = torch.empty((2, 2000), device="cuda")
+    pop.rollout(env, 2000, full, wl.seed, 30, returns=r1)
+    t1 = pop.payoff(reset=True)
+    pop.rollout(env, 2000, full, wl.seed, 30)
+    t2 = pop.payoff(reset=True)
+    assert np.array_equal(t1["counts"], t2["counts"])
+    assert np.array_equal(np.nan_to_num(t1["mean"]), np.nan_to_num(t2["mean"]))
+    ra = torch.empty((2, 1200), device="cuda")
+    rb = torch.empty((2, 800), device="cuda")
+    pa = IO.make_pairs(wl, n_envs=1200, env_offset=0)
+    pb = IO.make_pairs(wl, n_envs=800, env_offset=1200)
+    assert torch.equal(torch.cat([pa, pb]), full)
+    pop.rollout(env, 1200, pa, wl.seed, 30, returns=ra)
+    pop.rollout(env, 800, pb, wl.seed, 30, env_offset=1200, returns=rb)
+    t3 = pop.payoff(reset=True)
+    assert torch.equal(torch.cat([ra, rb], dim=1), r1)
+    assert np.array_equal(t3["counts"], t1["counts"])
+    assert np.array_equal(np.nan_to_num(t3["mean"]), np.nan_to_num(t1["mean"]))
+    assert t3["live_frames"] == t1["live_frames"]
+    pop.close()
+
+
+def test_single_env_and_horizon_one():
+    wl = W.make(5, P=4, n_envs=1, horizon=1)
+    g = run_gpu(wl, snaps=[0])
+    check_parity(wl, g)
+
+
+def test_bad_policy_id_is_flagged():
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(2, P=2, per_pair=64, horizon=2)
+    pop = IO.make_population(wl)
+    env = IO.make_env(wl)
+    pairs = wl.pairs.copy()
+    pairs[5, 1] = 7
+    pop.rollout(env, wl.n_envs, torch.from_numpy(pairs).cuda(), wl.seed, 2)
+    t = pop.payoff(check=False)
+    assert t["status"] == M.binding.E_DEVICE and t["device_flags"] & 1
+    assert t["counts"].sum() == wl.n_envs - 1
+    # flags are cleared once reported
+    pop.rollout(env, wl.n_envs, torch.from_numpy(wl.pairs).cuda(), wl.seed, 2)
+    assert pop.payoff(reset=True)["status"] == 0
+    pop.close()
+
+
+def test_nan_logits_are_flagged():
+    import paper_2106_07551_amd as M
+    wl = W.make(1, per_pair=8)
+    tab = wl.tab_logits.copy()
+    tab[2, 1] = np.nan
+    pop = M.Population(M.POLICY_TABULAR, 4, 3, tab_logits=torch.from_numpy(tab).cuda())
+    from paper_2106_07551_amd import workload_io as IO
+    env = IO.make_env(wl)
+    pop.rollout(env, wl.n_envs, IO.make_pairs(wl), wl.seed, 1)
+    t = pop.payoff(check=False)
+    assert t["status"] == M.binding.E_DEVICE and t["device_flags"] & 2
+    pop.close()
+
+
+def test_host_validation_errors():
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(4, P=2, per_pair=1, horizon=2)
+    pop = IO.make_population(wl)
+    env = IO.make_env(wl)
+    pairs = IO.make_pairs(wl)
+    with pytest.raises(M.MalibError) as e:
+        pop.rollout(env, wl.n_envs, pairs, wl.seed, 0)
+    assert e.value.status == M.binding.E_INVAL
+    with pytest.raises(M.MalibError):
+        pop.rollout(env, 0, pairs, wl.seed, 2)
+    bad = M.Env(M.ENV_FEATURE, 2, 18, team=[1, -1], d=96, W=None, emb=None, u=None)
+    with pytest.raises(M.MalibError):
+        pop.rollout(bad, wl.n_envs, pairs, wl.seed, 2)
+    with pytest.raises(M.MalibError):
+        M.Population(M.POLICY_MLP_BF16, 2, 18, dims=[512, 500, 500, 18],
+                     weights=[torch.zeros(1, device="cuda")] * 3)
+    pop.close()
