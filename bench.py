@@ -1,0 +1,178 @@
+#!/usr/bin/env python3
+"""Benchmark: payoff-table fill throughput on one MI355X.
+
+One step = one full pass of the rollout path over one batch: draw every seat's
+policy from the meta-strategy, bucket slots by policy, reset, H x (grouped
+policy forward -> Gumbel-max sampling -> environment step with return
+accumulation), reduce returns into the payoff table and read it back on the
+host.  Inputs (weights, environment parameters, meta-strategy) are resident in
+HBM before timing starts.
+
+Default workload: the 4v4 team game on R^256 feature dynamics, 16384 envs x 8
+seats, population of 128 bf16 MLPs 256-512-512-18, horizon 200 (the largest
+configuration).  Other workloads: --workload matrix|iter|pursuit|feature|team.
+
+Prints one JSON line with the throughput (live agent-frames/s), the fill time
+(ms per step), the roofline of the grouped policy forward (HIP events on the
+kernel's stream, over the timed region) and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+NAME_TO_C = {"matrix": 1, "iter": 2, "pursuit": 3, "feature": 4, "team": 5}
+
+
+def policy_flops_per_frame(dims):
+    """Algorithmic flops of one policy forward (2 per multiply-add)."""
+    return 2 * sum(dims[i] * dims[i + 1] for i in range(len(dims) - 1))
+
+
+def describe(wl):
+    d = {"workload": wl.name, "n_envs": wl.n_envs, "agents": wl.n_agents,
+         "policies": wl.P, "horizon": wl.horizon, "actions": wl.n_actions}
+    if wl.dims:
+        d["policy"] = ("bf16" if wl.pol_kind == 2 else "fp32") + " MLP " + \
+            "-".join(str(x) for x in wl.dims)
+    else:
+        d["policy"] = "tabular"
+    if wl.d:
+        d["state_dim"] = wl.d
+    d["pairing"] = "blocked all pairs" if wl.pairs is not None else "meta-strategy sample"
+    return d
+
+
+def cpu_baseline(wl, budget_s=12.0, max_s=30.0):
+    """The oracle (single-threaded C) on whole episodes of the same workload,
+    env by env until ~budget_s of CPU time."""
+    import numpy as np
+    import oracle
+    pids_all = wl.pairs if wl.pairs is not None else oracle.meta_sample(
+        wl.sigma, wl.P, wl.n_envs, wl.n_agents, wl.seed)
+    frames = 0
+    envs = 0
+    t0 = time.perf_counter()
+    while True:
+        e = envs * 997 % wl.n_envs
+        r = oracle.rollout(wl, np.array([e]), pids_all[e:e + 1])
+        frames += r["live_frames"]
+        envs += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or el >= max_s or envs >= wl.n_envs:
+            break
+    return {"value": frames / el, "unit": "agent-frames/s", "cores": 1, "kind": "oracle",
+            "sample": f"{envs} full episodes (H={wl.horizon}) of {wl.name}, "
+                      f"{frames} agent-frames in {el:.1f} s, single thread",
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="team", choices=sorted(NAME_TO_C))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the rollout path "
+              "shards by env across GPUs with one all-reduce of the table, which is not "
+              "built here", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    import workloads as W
+
+    torch.cuda.set_device(0)
+    wl = W.make(NAME_TO_C[args.workload])
+    stream = torch.cuda.current_stream()
+    pop = IO.make_population(wl)
+    env = IO.make_env(wl)
+    n, na = wl.n_envs, wl.n_agents
+    pairs = None
+    if wl.pairs is not None:
+        pairs = IO.make_pairs(wl)
+    else:
+        pairs = torch.empty((n, na), dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+
+    def one_step():
+        if wl.pairs is None:
+            M.meta_sample(wl.sigma, wl.P, n, na, wl.seed, out=pairs)
+        pop.rollout(env, n, pairs, wl.seed, wl.horizon)
+        return pop.payoff(reset=True)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+
+    pop.profile_enable(True)
+    frames = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        tab = one_step()
+        frames += tab["live_frames"]
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    kern = {}
+    for name, k in (("policy", M.K_POLICY), ("sample", M.K_SAMPLE), ("env", M.K_ENV),
+                    ("setup", M.K_SETUP), ("payoff", M.K_PAYOFF)):
+        ms, cnt = pop.profile_read(k)
+        kern[name] = {"total_ms": round(ms, 3), "launches": cnt,
+                      "avg_us": round(1000.0 * ms / max(cnt, 1), 3)}
+    pop.profile_enable(False)
+
+    ms_step = 1000.0 * el / args.steps
+    value = frames / el
+    roof = None
+    if wl.pol_kind == W.MLP_BF16:
+        flops = policy_flops_per_frame(wl.dims) * n * na        # per launch
+        avg_s = kern["policy"]["total_ms"] / max(kern["policy"]["launches"], 1) / 1000.0
+        ach = flops / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                "traffic": None, "kernel": "grouped policy forward (mlp_bf16_kernel)",
+                "flops_per_launch": flops}
+    out = {
+        "metric": "agent-frames/s on 1 MI355X (payoff-table fill)",
+        "value": round(value, 1),
+        "unit": "agent-frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "fill_time_ms": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.pol_kind == W.MLP_BF16 else "fp32",
+        "data": "synthetic (seeded generator; random-init policies)",
+        "config": describe(wl),
+        "roofline": roof,
+        "kernels": kern,
+        "frames_per_step": frames // max(args.steps, 1),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+        out["cpu_baseline"]["value"] = round(out["cpu_baseline"]["value"], 1)
+    pop.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
