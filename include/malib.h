@@ -270,6 +270,11 @@ malib_status malib_profile_read(malib_pop_t pop, int32_t kernel, double* total_m
  * dynamics, exposed so it can be compared bit for bit.  x, y: device fp32 [n]. */
 malib_status malib_debug_tanh_ref(const float* x, float* y, int64_t n, void* stream);
 
+/* y[i] = bf16 bits of x[i] (round to nearest even) on the device, with the
+ * conversion the policy kernels use for observations, weights and hidden
+ * activations.  x: device fp32 [n], y: device uint16 [n], n even. */
+malib_status malib_debug_bf16(const float* x, uint16_t* y, int64_t n, void* stream);
+
 /* Philox4x64-10 blocks on the device: out[i] = philox(ctr[i], (key0, key1)).
  * ctr, out: device uint64 [n][4]. */
 malib_status malib_debug_philox(const uint64_t* ctr, uint64_t key0, uint64_t key1,

@@ -24,7 +24,7 @@ K_POLICY, K_SAMPLE, K_ENV, K_SETUP, K_PAYOFF = 0, 1, 2, 3, 4
 EXPORTS = [
     "malib_pop_create", "malib_pop_destroy", "malib_rollout_batch", "malib_payoff_eval",
     "malib_meta_sample", "malib_last_error", "malib_profile_enable", "malib_profile_read",
-    "malib_debug_tanh_ref", "malib_debug_philox",
+    "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
 ]
 
 
@@ -89,6 +89,8 @@ def lib():
         L.malib_profile_read.restype = i32
         L.malib_debug_tanh_ref.argtypes = [vp, vp, i64, vp]
         L.malib_debug_tanh_ref.restype = i32
+        L.malib_debug_bf16.argtypes = [vp, vp, i64, vp]
+        L.malib_debug_bf16.restype = i32
         L.malib_debug_philox.argtypes = [vp, u64, u64, vp, i64, vp]
         L.malib_debug_philox.restype = i32
         _lib = L
@@ -237,6 +239,14 @@ def debug_tanh_ref(x, y=None, stream=None):
     if y is None:
         y = torch.empty_like(x)
     _check(lib().malib_debug_tanh_ref(_dptr(x), _dptr(y), x.numel(), _stream(stream)))
+    return y
+
+
+def debug_bf16(x, stream=None):
+    """bf16 bit patterns (as int16) of an even-length fp32 device tensor."""
+    import torch
+    y = torch.empty(x.shape, dtype=torch.int16, device=x.device)
+    _check(lib().malib_debug_bf16(_dptr(x), _dptr(y), x.numel(), _stream(stream)))
     return y
 
 

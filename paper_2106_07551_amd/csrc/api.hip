@@ -643,6 +643,16 @@ malib_status malib_debug_tanh_ref(const float* x, float* y, int64_t n, void* str
     return MALIB_OK;
 }
 
+malib_status malib_debug_bf16(const float* x, uint16_t* y, int64_t n, void* stream)
+{
+    if (!x || !y || n < 0 || (n & 1))
+        return fail(MALIB_E_INVAL, "bad arguments (n must be even)");
+    if (n == 0)
+        return MALIB_OK;
+    HIP_TRY(launch_debug_bf16(x, y, n, (hipStream_t)stream));
+    return MALIB_OK;
+}
+
 malib_status malib_debug_philox(const uint64_t* ctr, uint64_t key0, uint64_t key1,
                                 uint64_t* out, int64_t n, void* stream)
 {

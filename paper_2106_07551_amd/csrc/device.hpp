@@ -72,9 +72,15 @@ __device__ __forceinline__ uint16_t bf16_bits(float x)
     return (uint16_t)(b >> 16);
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> bf16 (round to nearest even) packed low/high; an IEEE fptrunc,
+// which gfx950 executes as one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
 {
-    return (uint32_t)bf16_bits(lo) | ((uint32_t)bf16_bits(hi) << 16);
+    f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 // exp_ref: Cody-Waite reduction x = n ln2 + r with ln2 split into a high part

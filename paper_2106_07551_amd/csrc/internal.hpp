@@ -15,7 +15,7 @@ namespace malib {
 constexpr int kMaxP = 256;
 constexpr int kMaxActions = 32;
 constexpr int kMaxAgents = 8;
-constexpr int kTileRows = 128;     // rows per bf16 MFMA policy tile
+constexpr int kTileRows = 64;      // rows per bf16 MFMA policy tile
 constexpr int kF32TileRows = 64;   // rows per fp32 policy tile (one wavefront)
 constexpr int kBucketChunk = 2048; // slots per bucketing workgroup
 
@@ -115,6 +115,7 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
                            const uint8_t* done, float* logits, hipStream_t s);
 
 // Diagnostics.
+hipError_t launch_debug_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);
 hipError_t launch_debug_tanh(const float* x, float* y, int64_t n, hipStream_t s);
 hipError_t launch_debug_philox(const uint64_t* ctr, uint64_t k0, uint64_t k1, uint64_t* out,
                                int64_t n, hipStream_t s);

@@ -181,15 +181,16 @@ __global__ __launch_bounds__(256) void step_pursuit_kernel(
 // LDS-staged chunks of WT (c-major) and of the state (so every accumulator
 // sees exactly the sequential fused chain, no split of the sum).  The reward
 // r = u . s' is then a sequential fused chain per env over the staged s'.
-constexpr int kFeatEnvs = 32;
 constexpr int kFeatKC = 32;
 
-template <int D>
+// EPT envs per thread: the workgroup owns 4*EPT envs.
+template <int D, int EPT>
 __global__ __launch_bounds__(256) void step_feature_kernel(
     const float* __restrict__ WT, const float* __restrict__ emb, const float* __restrict__ u,
     EnvArgs ea, int64_t n, const uint8_t* __restrict__ act, const float* __restrict__ s_in,
     float* __restrict__ s_out, float* __restrict__ ret)
 {
+    constexpr int kFeatEnvs = 4 * EPT;
     constexpr int NJ = D / 64;
     constexpr int SSTR = kFeatEnvs + 4;
     constexpr int WS_FLOATS = kFeatKC * D > kFeatEnvs * (D + 1) ? kFeatKC * D : kFeatEnvs * (D + 1);
@@ -198,43 +199,72 @@ __global__ __launch_bounds__(256) void step_feature_kernel(
     const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
     const int64_t e0 = (int64_t)blockIdx.x * kFeatEnvs;
 
-    float acc[8][NJ];
+    float acc[EPT][NJ];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < EPT; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
             acc[i][j] = 0.0f;
 
+    // Staging: chunk c0 of WT (KC x D floats, c-major) and of the state (32 envs
+    // x KC) goes global -> registers -> LDS; the loads of chunk c0+KC are issued
+    // before the FMAs of chunk c0 so their latency overlaps the arithmetic.
+    constexpr int WQ = kFeatKC * D / 4 / 256;     // float4 of WT per thread per chunk
+    // state chunk: kFeatEnvs envs x KC columns = kFeatEnvs*8 float4; threads
+    // beyond that re-load env 0's chunk and skip the LDS store
+    const int el_ld = (tid >> 3) % kFeatEnvs, cq_ld = tid & 7;
+    const bool s_owner = (tid >> 3) < kFeatEnvs;
+    const int64_t e_ld = e0 + el_ld;
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    const v4f* wsrc = reinterpret_cast<const v4f*>(WT) + tid;
+    const float* ssrc = s_in + (e_ld < n ? e_ld : 0) * D + cq_ld * 4;
+    v4f wreg[WQ];
+    v4f sreg;
+#pragma unroll
+    for (int q = 0; q < WQ; ++q)
+        wreg[q] = wsrc[q * 256];
+    sreg = *reinterpret_cast<const v4f*>(ssrc);
     for (int c0 = 0; c0 < D; c0 += kFeatKC) {
-        // WT rows c0..c0+KC-1 (each D floats) -> Ws[c][k]
-        const float4* src = reinterpret_cast<const float4*>(WT + (int64_t)c0 * D);
-        float4* dst = reinterpret_cast<float4*>(Ws);
-        for (int q = tid; q < kFeatKC * D / 4; q += 256)
-            dst[q] = src[q];
-        // state chunk: env el, columns c0 + 4*cq .. +3 -> Ss[c][el]
-        {
-            int el = tid >> 3, cq = tid & 7;
-            int64_t e = e0 + el;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (e < n)
-                v = *reinterpret_cast<const float4*>(s_in + e * D + c0 + cq * 4);
-            Ss[(cq * 4 + 0) * SSTR + el] = v.x;
-            Ss[(cq * 4 + 1) * SSTR + el] = v.y;
-            Ss[(cq * 4 + 2) * SSTR + el] = v.z;
-            Ss[(cq * 4 + 3) * SSTR + el] = v.w;
+        v4f* dst = reinterpret_cast<v4f*>(Ws);
+#pragma unroll
+        for (int q = 0; q < WQ; ++q)
+            dst[q * 256 + tid] = wreg[q];
+        if (e_ld >= n)
+            sreg = v4f{0.f, 0.f, 0.f, 0.f};
+        if (s_owner) {
+            Ss[(cq_ld * 4 + 0) * SSTR + el_ld] = sreg.x;
+            Ss[(cq_ld * 4 + 1) * SSTR + el_ld] = sreg.y;
+            Ss[(cq_ld * 4 + 2) * SSTR + el_ld] = sreg.z;
+            Ss[(cq_ld * 4 + 3) * SSTR + el_ld] = sreg.w;
         }
         __syncthreads();
-#pragma unroll 4
+        {
+            // next chunk (the last iteration re-reads its own chunk, unused)
+            const int cn = c0 + kFeatKC < D ? c0 + kFeatKC : c0;
+            const v4f* wn = wsrc + cn * (D / 4);
+#pragma unroll
+            for (int q = 0; q < WQ; ++q)
+                wreg[q] = wn[q * 256];
+            sreg = *reinterpret_cast<const v4f*>(ssrc + cn);
+        }
+#pragma unroll
         for (int c = 0; c < kFeatKC; ++c) {
             float w[NJ];
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
                 w[j] = Ws[c * D + tx + 64 * j];
-            const float4* sp = reinterpret_cast<const float4*>(&Ss[c * SSTR + ty * 8]);
-            float4 sa = sp[0], sb = sp[1];
-            float sv[8] = {sa.x, sa.y, sa.z, sa.w, sb.x, sb.y, sb.z, sb.w};
+            float sv[EPT];
+            const v4f* sp = reinterpret_cast<const v4f*>(&Ss[c * SSTR + ty * EPT]);
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int q = 0; q < EPT / 4; ++q) {
+                v4f t4 = sp[q];
+                sv[4 * q + 0] = t4.x;
+                sv[4 * q + 1] = t4.y;
+                sv[4 * q + 2] = t4.z;
+                sv[4 * q + 3] = t4.w;
+            }
+#pragma unroll
+            for (int i = 0; i < EPT; ++i)
 #pragma unroll
                 for (int j = 0; j < NJ; ++j)
                     acc[i][j] = __builtin_fmaf(w[j], sv[i], acc[i][j]);
@@ -245,8 +275,8 @@ __global__ __launch_bounds__(256) void step_feature_kernel(
     // epilogue: embeddings in seat order, tanh_ref, store s' (global + LDS)
     float* Sl = Ws;   // [32][D+1]
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        int el = ty * 8 + i;
+    for (int i = 0; i < EPT; ++i) {
+        int el = ty * EPT + i;
         int64_t e = e0 + el;
         if (e < n) {
             const uint8_t* ae = act + e * ea.n_agents;
@@ -296,17 +326,19 @@ hipError_t launch_env_step(const EnvArgs& e, int64_t n_envs, const uint8_t* acti
                                                    done, ret, frames);
         break;
     case MALIB_ENV_FEATURE: {
-        int fb = (int)((n_envs + kFeatEnvs - 1) / kFeatEnvs);
         const float* si = (const float*)state_in;
         float* so = (float*)state_out;
+        // 8 envs per thread (32-env workgroups) for d = 512; 4 (16-env) below,
+        // which doubles the resident wavefronts for the smaller state
+        const int fb8 = (int)((n_envs + 31) / 32), fb4 = (int)((n_envs + 15) / 16);
         if (e.d == 64)
-            step_feature_kernel<64><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<64, 4><<<fb4, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else if (e.d == 128)
-            step_feature_kernel<128><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<128, 4><<<fb4, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else if (e.d == 256)
-            step_feature_kernel<256><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<256, 4><<<fb4, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else if (e.d == 512)
-            step_feature_kernel<512><<<fb, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<512, 8><<<fb8, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else
             return hipErrorInvalidValue;
         break;

@@ -227,7 +227,7 @@ hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int32_t* of
 enum { kObsFeature = 0, kObsPursuit = 1, kObsIter = 2 };
 
 constexpr int kLdw = 520;           // LDS row stride (bf16): 512 + 8 to spread banks
-constexpr int kMlpThreads = 512;    // 8 wavefronts
+constexpr int kMlpThreads = 256;    // 4 wavefronts; two workgroups share a CU
 
 struct MlpBf16Args {
     const uint4* w1; const uint4* w2; const uint4* w3;
@@ -235,78 +235,155 @@ struct MlpBf16Args {
     const int32_t* perm; const int32_t* offsets; const int32_t* tile_off;
     const void* state;
     float* logits;
-    int P, A, in_dim, in_pad, n_agents, grid, d;
+    int P, A, in_dim, n_agents, grid, d;
     int64_t n_envs;
     int n_blocks;                   // launched workgroups (a multiple of 8)
 };
 
-// One MFMA layer of a wavefront: output tiles (n-tiles nt0.., row-tiles rt0..)
-// = W[nt] (32 x 16 per k-step, from the packed fragments) x X^T[rt] (16 x 32,
-// from LDS rows).  acc[nt][rt] register r, lane i holds output unit
-// nt*32 + (r/4)*8 + (i/32)*4 + r%4 of tile row rt*32 + i%32.
-template <int NT, int RT>
-__device__ __forceinline__ void mfma_layer(const uint4* __restrict__ frag, int ksteps, int nt0,
-                                           int rt0, const uint16_t* buf, int lane,
-                                           f32x16 (&acc)[NT][RT])
+// Ring of weight fragments of one layer: k-steps s, s+1, ... in flight, so a
+// wavefront's weight loads are issued DEPTH-1 steps ahead of their MFMAs (and
+// the first DEPTH steps of a layer before the preceding phase's LDS work).
+template <int NT, int DEPTH>
+struct WRing {
+    uint4 a[DEPTH][NT];
+};
+
+template <int NT, int DEPTH>
+__device__ __forceinline__ void ring_fill(WRing<NT, DEPTH>& ring, const uint4* __restrict__ frag,
+                                          int ksteps, int nt0, int lane)
 {
 #pragma unroll
-    for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int r = 0; r < RT; ++r)
-            acc[n][r] = f32x16{};
-    const int brow = lane & 31, bcol = (lane >> 5) * 8;
-    uint4 a_cur[NT];
-#pragma unroll
-    for (int n = 0; n < NT; ++n)
-        a_cur[n] = frag[((int64_t)(nt0 + n) * ksteps + 0) * 64 + lane];
-    for (int ks = 0; ks < ksteps; ++ks) {
-        uint4 a_nxt[NT];
-        if (ks + 1 < ksteps) {
+    for (int s = 0; s < DEPTH; ++s)
+        if (s < ksteps)
 #pragma unroll
             for (int n = 0; n < NT; ++n)
-                a_nxt[n] = frag[((int64_t)(nt0 + n) * ksteps + ks + 1) * 64 + lane];
+                ring.a[s][n] = frag[((int64_t)(nt0 + n) * ksteps + s) * 64 + lane];
+}
+
+// One MFMA layer of a wavefront: output tiles (n-tiles nt0.., row-tiles rt0..)
+// = bias + W[nt] (32 x 16 per k-step, packed fragments) x X^T[rt] (16 x 32, LDS
+// rows).  acc[nt][rt] register r, lane i holds output unit nt*32 + (r/4)*8 +
+// (i/32)*4 + r%4 of tile row rt*32 + i%32.  The ring must hold k-steps
+// 0..DEPTH-1.  (The fp32 sum order of a unit is the bias, then the k-steps.)
+template <int NT, int RT, int DEPTH>
+__device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring,
+                                           const uint4* __restrict__ frag, int ksteps, int nt0,
+                                           int rt0, const uint16_t* buf, int lane,
+                                           const float* __restrict__ bias, f32x16 (&acc)[NT][RT])
+{
+    // accumulators start from the bias of their output units
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+        f32x16 b0;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float4 bb = *reinterpret_cast<const float4*>(
+                bias + (nt0 + n) * 32 + g * 8 + (lane >> 5) * 4);
+            b0[g * 4 + 0] = bb.x;
+            b0[g * 4 + 1] = bb.y;
+            b0[g * 4 + 2] = bb.z;
+            b0[g * 4 + 3] = bb.w;
         }
-        uint4 b[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r)
-            b[r] = *reinterpret_cast<const uint4*>(buf + ((rt0 + r) * 32 + brow) * kLdw + ks * 16 + bcol);
+            acc[n][r] = b0;
+    }
+    const int brow = lane & 31, bcol = (lane >> 5) * 8;
+    const uint16_t* bp[RT];
 #pragma unroll
-        for (int n = 0; n < NT; ++n)
+    for (int r = 0; r < RT; ++r)
+        bp[r] = buf + ((rt0 + r) * 32 + brow) * kLdw + bcol;
+    uint4 b[2][RT];
 #pragma unroll
-            for (int r = 0; r < RT; ++r)
-                acc[n][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8, a_cur[n]), __builtin_bit_cast(bf16x8, b[r]),
-                    acc[n][r], 0, 0, 0);
-        if (ks + 1 < ksteps) {
+    for (int r = 0; r < RT; ++r)
+        b[0][r] = *reinterpret_cast<const uint4*>(bp[r]);
+
+    for (int k0 = 0; k0 < ksteps; k0 += DEPTH) {
 #pragma unroll
-            for (int n = 0; n < NT; ++n)
-                a_cur[n] = a_nxt[n];
+        for (int s = 0; s < DEPTH; ++s) {
+            const int ks = k0 + s;
+            if (ks < ksteps) {
+                if (ks + 1 < ksteps) {
+#pragma unroll
+                    for (int r = 0; r < RT; ++r)
+                        b[(ks + 1) & 1][r] = *reinterpret_cast<const uint4*>(bp[r] + (ks + 1) * 16);
+                }
+#pragma unroll
+                for (int n = 0; n < NT; ++n)
+#pragma unroll
+                    for (int r = 0; r < RT; ++r)
+                        acc[n][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            __builtin_bit_cast(bf16x8, ring.a[s][n]),
+                            __builtin_bit_cast(bf16x8, b[ks & 1][r]), acc[n][r], 0, 0, 0);
+                if (ks + DEPTH < ksteps) {
+#pragma unroll
+                    for (int n = 0; n < NT; ++n)
+                        ring.a[s][n] = frag[((int64_t)(nt0 + n) * ksteps + ks + DEPTH) * 64 + lane];
+                }
+            }
         }
     }
 }
 
-// bias + ReLU + bf16, written back as the next layer's input rows.
+// Output layer (one 32-wide n-tile): wave w takes row-tile w%2 and half h =
+// w/2 of the k-steps.  Its weight fragments are loaded into registers before
+// the preceding epilogue (out_fill), the MFMAs alternate between two
+// accumulators, and the k-halves are summed through LDS by the caller.
+template <int KH>
+struct OutFrags {
+    uint4 a[KH];
+};
+
+template <int KH>
+__device__ __forceinline__ void out_fill(OutFrags<KH>& f, const uint4* __restrict__ frag, int h,
+                                         int lane)
+{
+#pragma unroll
+    for (int k = 0; k < KH; ++k)
+        f.a[k] = frag[(int64_t)(h * KH + k) * 64 + lane];
+}
+
+template <int KH>
+__device__ __forceinline__ f32x16 mfma_out_half(const OutFrags<KH>& f, int h, int rt,
+                                                const uint16_t* buf, int lane)
+{
+    f32x16 acc0 = f32x16{}, acc1 = f32x16{};
+    const uint16_t* bp = buf + (rt * 32 + (lane & 31)) * kLdw + (lane >> 5) * 8 + h * KH * 16;
+    uint4 b[2];
+    b[0] = *reinterpret_cast<const uint4*>(bp);
+#pragma unroll
+    for (int k = 0; k < KH; ++k) {
+        if (k + 1 < KH)
+            b[(k + 1) & 1] = *reinterpret_cast<const uint4*>(bp + (k + 1) * 16);
+        if (k & 1)
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.a[k]),
+                                                           __builtin_bit_cast(bf16x8, b[k & 1]),
+                                                           acc1, 0, 0, 0);
+        else
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.a[k]),
+                                                           __builtin_bit_cast(bf16x8, b[k & 1]),
+                                                           acc0, 0, 0, 0);
+    }
+    return acc0 + acc1;
+}
+
+// ReLU + bf16, written back as the next layer's input rows.
 template <int NT, int RT>
-__device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], const float* bias,
-                                                int nt0, int rt0, uint16_t* buf, int lane)
+__device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], int nt0, int rt0,
+                                                uint16_t* buf, int lane)
 {
 #pragma unroll
     for (int n = 0; n < NT; ++n) {
 #pragma unroll
-        for (int r = 0; r < RT; ++r) {
-            int row = (rt0 + r) * 32 + (lane & 31);
+        for (int g = 0; g < 4; ++g) {
+            const int u0 = (nt0 + n) * 32 + g * 8 + (lane >> 5) * 4;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                int u0 = (nt0 + n) * 32 + g * 8 + (lane >> 5) * 4;
-                float4 bb = *reinterpret_cast<const float4*>(bias + u0);
-                float v0 = acc[n][r][g * 4 + 0] + bb.x;
-                float v1 = acc[n][r][g * 4 + 1] + bb.y;
-                float v2 = acc[n][r][g * 4 + 2] + bb.z;
-                float v3 = acc[n][r][g * 4 + 3] + bb.w;
-                v0 = v0 > 0.0f ? v0 : 0.0f;
-                v1 = v1 > 0.0f ? v1 : 0.0f;
-                v2 = v2 > 0.0f ? v2 : 0.0f;
-                v3 = v3 > 0.0f ? v3 : 0.0f;
+            for (int r = 0; r < RT; ++r) {
+                const int row = (rt0 + r) * 32 + (lane & 31);
+                float v0 = fmaxf(acc[n][r][g * 4 + 0], 0.0f);
+                float v1 = fmaxf(acc[n][r][g * 4 + 1], 0.0f);
+                float v2 = fmaxf(acc[n][r][g * 4 + 2], 0.0f);
+                float v3 = fmaxf(acc[n][r][g * 4 + 3], 0.0f);
                 uint2 pk = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
                 *reinterpret_cast<uint2*>(buf + row * kLdw + u0) = pk;
             }
@@ -316,17 +393,87 @@ __device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], con
 
 template <int HID>
 struct HidSplit {
-    // wavefront grid for a HID-wide layer over the 4 row-tiles
-    static constexpr int NT = HID >= 512 ? 2 : 1;
-    static constexpr int RT = HID >= 256 ? 4 : (HID == 128 ? 2 : 1);
+    // four wavefronts over (HID/32 n-tiles) x (2 row-tiles of 32)
+    static constexpr int NT = HID >= 256 ? HID / 128 : 1;
+    static constexpr int RT = HID >= 128 ? 2 : 1;
     static constexpr int NGROUPS = (HID / 32) / NT;
+    static constexpr int DEPTH = NT >= 4 ? 3 : 4;
 };
 
-template <int HID, int OBS>
-__global__ __launch_bounds__(kMlpThreads) void mlp_bf16_kernel(MlpBf16Args a)
+// Observation rows of the tile -> LDS (bf16).  KIN is the padded input width.
+template <int OBS, int KIN>
+__device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_slot,
+                                          const int* row_env, uint16_t* buf, int tid)
+{
+    if (OBS == kObsFeature) {
+        // KIN == d: rows of d floats, as float4; thread t keeps column t % (KIN/4)
+        constexpr int Q4 = KIN / 4;
+        constexpr int ROWS_PER_PASS = kMlpThreads / Q4;
+        constexpr int PASSES = kTileRows / ROWS_PER_PASS;
+        const int c = (tid % Q4) * 4, r0 = tid / Q4;
+        constexpr int BATCH = PASSES < 4 ? PASSES : 4;
+        typedef float v4f __attribute__((ext_vector_type(4)));
+        const float* S = (const float*)a.state + c;
+#pragma unroll
+        for (int u0 = 0; u0 < PASSES; u0 += BATCH) {
+            v4f v[BATCH];
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u) {
+                const int env = row_env[r0 + (u0 + u) * ROWS_PER_PASS];
+                v[u] = v4f{0.f, 0.f, 0.f, 0.f};
+                if (env >= 0)
+                    v[u] = *reinterpret_cast<const v4f*>(S + (uint32_t)env * (uint32_t)KIN);
+            }
+#pragma unroll
+            for (int u = 0; u < BATCH; ++u) {
+                uint2 pk = make_uint2(pack_bf16x2(v[u].x, v[u].y), pack_bf16x2(v[u].z, v[u].w));
+                *reinterpret_cast<uint2*>(buf + (r0 + (u0 + u) * ROWS_PER_PASS) * kLdw + c) = pk;
+            }
+        }
+    } else if (OBS == kObsPursuit) {
+        const uint8_t* pos = (const uint8_t*)a.state;
+        for (int i = tid; i < kTileRows * KIN; i += kMlpThreads) {
+            const int r = i / KIN, c = i - r * KIN;
+            const int slot = row_slot[r];
+            float v = 0.0f;
+            if (slot >= 0 && c < 75) {
+                const int64_t env = slot / a.n_agents;
+                const int seat = slot - (int)env * a.n_agents;
+                const int pc = pos[env], ec = pos[a.n_envs + env];
+                const int self = seat == 0 ? pc : ec;
+                const int o = c / 3, ch = c - o * 3;
+                const int dy = o / 5 - 2, dx = o % 5 - 2;
+                const int G = a.grid;
+                const int x = ((self % G) + dx + G) % G, y = ((self / G) + dy + G) % G;
+                const int cell = y * G + x;
+                const bool on = ch == 0 ? cell == pc : (ch == 1 ? cell == ec : (dx == 0 && dy == 0));
+                v = on ? 1.0f : 0.0f;
+            }
+            buf[r * kLdw + c] = bf16_bits(v);
+        }
+    } else {
+        const uint16_t* hist = (const uint16_t*)a.state;
+        for (int i = tid; i < kTileRows * KIN; i += kMlpThreads) {
+            const int r = i / KIN, c = i - r * KIN;
+            const int slot = row_slot[r];
+            float v = 0.0f;
+            if (slot >= 0 && c < a.in_dim) {
+                const int64_t env = slot / a.n_agents;
+                const int seat = slot - (int)env * a.n_agents;
+                v = iter_obs(hist[env], seat, a.A, c);
+            }
+            buf[r * kLdw + c] = bf16_bits(v);
+        }
+    }
+}
+
+template <int HID, int OBS, int KIN>
+__global__ __launch_bounds__(kMlpThreads, 2) void mlp_bf16_kernel(MlpBf16Args a)
 {
     __shared__ __attribute__((aligned(16))) uint16_t buf[kTileRows * kLdw];
     __shared__ int row_slot[kTileRows];
+    __shared__ int row_env[kTileRows];
+    __shared__ float red[2 * 16 * 64];   // output-layer partial sums of the second k-half
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
     // workgroups are dispatched round-robin over the 8 XCDs: give each XCD a
@@ -340,83 +487,55 @@ __global__ __launch_bounds__(kMlpThreads) void mlp_bf16_kernel(MlpBf16Args a)
     const int r0 = a.offsets[p] + (t - a.tile_off[p]) * kTileRows;
     const int nrows = min(kTileRows, a.offsets[p + 1] - r0);
 
-    if (tid < kTileRows)
-        row_slot[tid] = tid < nrows ? a.perm[r0 + tid] : -1;
-    __syncthreads();
-
-    // ---- observations -> LDS rows (bf16)
-    if (OBS == kObsFeature) {
-        const int q4 = a.in_pad / 4;
-        const float* S = (const float*)a.state;
-        for (int i = tid; i < kTileRows * q4; i += kMlpThreads) {
-            int r = i / q4, c = (i - r * q4) * 4;
-            int slot = row_slot[r];
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (slot >= 0 && c < a.in_dim)
-                v = *reinterpret_cast<const float4*>(S + (int64_t)(slot / a.n_agents) * a.d + c);
-            uint2 pk = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
-            *reinterpret_cast<uint2*>(buf + r * kLdw + c) = pk;
-        }
-    } else if (OBS == kObsPursuit) {
-        const uint8_t* pos = (const uint8_t*)a.state;
-        for (int i = tid; i < kTileRows * a.in_pad; i += kMlpThreads) {
-            int r = i / a.in_pad, c = i - r * a.in_pad;
-            int slot = row_slot[r];
-            float v = 0.0f;
-            if (slot >= 0 && c < 75) {
-                int64_t env = slot / a.n_agents;
-                int seat = slot - (int)env * a.n_agents;
-                int pc = pos[env], ec = pos[a.n_envs + env];
-                int self = seat == 0 ? pc : ec;
-                int o = c / 3, ch = c - o * 3;
-                int dy = o / 5 - 2, dx = o % 5 - 2;
-                int G = a.grid;
-                int x = ((self % G) + dx + G) % G, y = ((self / G) + dy + G) % G;
-                int cell = y * G + x;
-                bool on = ch == 0 ? cell == pc : (ch == 1 ? cell == ec : (dx == 0 && dy == 0));
-                v = on ? 1.0f : 0.0f;
-            }
-            buf[r * kLdw + c] = bf16_bits(v);
-        }
-    } else {
-        const uint16_t* hist = (const uint16_t*)a.state;
-        for (int i = tid; i < kTileRows * a.in_pad; i += kMlpThreads) {
-            int r = i / a.in_pad, c = i - r * a.in_pad;
-            int slot = row_slot[r];
-            float v = 0.0f;
-            if (slot >= 0 && c < a.in_dim) {
-                int64_t env = slot / a.n_agents;
-                int seat = slot - (int)env * a.n_agents;
-                v = iter_obs(hist[env], seat, a.A, c);
-            }
-            buf[r * kLdw + c] = bf16_bits(v);
-        }
-    }
-    __syncthreads();
-
     using S = HidSplit<HID>;
     const int nt0 = (wave % S::NGROUPS) * S::NT;
     const int rt0 = (wave / S::NGROUPS) * S::RT;
-    f32x16 acc[S::NT][S::RT];
+    const uint4* W1 = a.w1 + (int64_t)p * (HID / 32) * (KIN / 16) * 64;
+    const uint4* W2 = a.w2 + (int64_t)p * (HID / 32) * (HID / 16) * 64;
+    WRing<S::NT, S::DEPTH> ring;
+    ring_fill(ring, W1, KIN / 16, nt0, lane);     // overlaps the observation gather
 
-    // ---- layer 1: in_pad -> HID
-    mfma_layer<S::NT, S::RT>(a.w1 + (int64_t)p * (HID / 32) * (a.in_pad / 16) * 64,
-                             a.in_pad / 16, nt0, rt0, buf, lane, acc);
+    if (tid < kTileRows) {
+        const int slot = tid < nrows ? a.perm[r0 + tid] : -1;
+        row_slot[tid] = slot;
+        row_env[tid] = slot >= 0 ? slot / a.n_agents : -1;
+    }
     __syncthreads();
-    hidden_epilogue<S::NT, S::RT>(acc, a.b1 + p * HID, nt0, rt0, buf, lane);
+    build_obs<OBS, KIN>(a, row_slot, row_env, buf, tid);
+    __syncthreads();
+
+    f32x16 acc[S::NT][S::RT];
+    // ---- layer 1: KIN -> HID
+    mfma_layer<S::NT, S::RT, S::DEPTH>(ring, W1, KIN / 16, nt0, rt0, buf, lane,
+                                       a.b1 + p * HID, acc);
+    ring_fill(ring, W2, HID / 16, nt0, lane);      // overlaps the epilogue
+    __syncthreads();
+    hidden_epilogue<S::NT, S::RT>(acc, nt0, rt0, buf, lane);
     __syncthreads();
     // ---- layer 2: HID -> HID
-    mfma_layer<S::NT, S::RT>(a.w2 + (int64_t)p * (HID / 32) * (HID / 16) * 64, HID / 16, nt0,
-                             rt0, buf, lane, acc);
+    mfma_layer<S::NT, S::RT, S::DEPTH>(ring, W2, HID / 16, nt0, rt0, buf, lane,
+                                       a.b2 + p * HID, acc);
+    constexpr int KH = HID / 32;                    // k-steps per half of the output layer
+    const int h = wave >> 1, rt = wave & 1;
+    OutFrags<KH> of;
+    out_fill<KH>(of, a.w3 + (int64_t)p * (HID / 16) * 64, h, lane);   // overlaps the epilogue
     __syncthreads();
-    hidden_epilogue<S::NT, S::RT>(acc, a.b2 + p * HID, nt0, rt0, buf, lane);
+    hidden_epilogue<S::NT, S::RT>(acc, nt0, rt0, buf, lane);
     __syncthreads();
-    // ---- layer 3: HID -> A (one 32-wide output tile; one row-tile per wave)
-    if (wave < 4) {
-        f32x16 o[1][1];
-        mfma_layer<1, 1>(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16, 0, wave, buf, lane, o);
-        int row = wave * 32 + (lane & 31);
-        int slot = row < nrows ? row_slot[row] : -1;
+    // ---- layer 3: HID -> A (one 32-wide output tile), k-halves summed in LDS
+    f32x16 o = mfma_out_half<KH>(of, h, rt, buf, lane);
+    if (h == 1) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            red[(rt * 16 + j) * 64 + lane] = o[j];
+    }
+    __syncthreads();
+    if (h == 0) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            o[j] += red[(rt * 16 + j) * 64 + lane];
+        const int row = rt * 32 + (lane & 31);
+        const int slot = row < nrows ? row_slot[row] : -1;
         if (slot >= 0) {
             float* out = a.logits + (int64_t)slot * a.A;
             const float* b3 = a.b3 + p * a.A;
@@ -424,12 +543,38 @@ __global__ __launch_bounds__(kMlpThreads) void mlp_bf16_kernel(MlpBf16Args a)
             for (int g = 0; g < 4; ++g)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    int u = g * 8 + (lane >> 5) * 4 + q;
+                    const int u = g * 8 + (lane >> 5) * 4 + q;
                     if (u < a.A)
-                        out[u] = o[0][0][g * 4 + q] + b3[u];
+                        out[u] = o[g * 4 + q] + b3[u];
                 }
         }
     }
+}
+
+template <int HID, int OBS, int KIN>
+static void launch_one(const MlpBf16Args& a, int blocks, hipStream_t s)
+{
+    mlp_bf16_kernel<HID, OBS, KIN><<<blocks, kMlpThreads, 0, s>>>(a);
+}
+
+template <int HID>
+static hipError_t launch_hid(const MlpBf16Args& a, int obs, int in_pad, int blocks, hipStream_t s)
+{
+    if (obs == kObsPursuit && in_pad == 80)
+        launch_one<HID, kObsPursuit, 80>(a, blocks, s);
+    else if (obs == kObsIter && in_pad == 32)
+        launch_one<HID, kObsIter, 32>(a, blocks, s);
+    else if (obs == kObsFeature && in_pad == 64)
+        launch_one<HID, kObsFeature, 64>(a, blocks, s);
+    else if (obs == kObsFeature && in_pad == 128)
+        launch_one<HID, kObsFeature, 128>(a, blocks, s);
+    else if (obs == kObsFeature && in_pad == 256)
+        launch_one<HID, kObsFeature, 256>(a, blocks, s);
+    else if (obs == kObsFeature && in_pad == 512)
+        launch_one<HID, kObsFeature, 512>(a, blocks, s);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
 }
 
 hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid, int d,
@@ -453,7 +598,6 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
     a.P = pop.P;
     a.A = pop.A;
     a.in_dim = pop.in_dim;
-    a.in_pad = pop.in_pad;
     a.n_agents = n_agents;
     a.grid = grid;
     a.d = d;
@@ -463,22 +607,13 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
     a.n_blocks = blocks;
     int obs = env_kind == MALIB_ENV_FEATURE ? kObsFeature
               : env_kind == MALIB_ENV_PURSUIT ? kObsPursuit : kObsIter;
-#define MALIB_MLP_CASE(H)                                                                   \
-    if (pop.hid == H) {                                                                     \
-        if (obs == kObsFeature)                                                             \
-            mlp_bf16_kernel<H, kObsFeature><<<blocks, kMlpThreads, 0, s>>>(a);              \
-        else if (obs == kObsPursuit)                                                        \
-            mlp_bf16_kernel<H, kObsPursuit><<<blocks, kMlpThreads, 0, s>>>(a);              \
-        else                                                                                \
-            mlp_bf16_kernel<H, kObsIter><<<blocks, kMlpThreads, 0, s>>>(a);                 \
-        return hipGetLastError();                                                           \
+    switch (pop.hid) {
+    case 64: return launch_hid<64>(a, obs, pop.in_pad, blocks, s);
+    case 128: return launch_hid<128>(a, obs, pop.in_pad, blocks, s);
+    case 256: return launch_hid<256>(a, obs, pop.in_pad, blocks, s);
+    case 512: return launch_hid<512>(a, obs, pop.in_pad, blocks, s);
+    default: return hipErrorInvalidValue;
     }
-    MALIB_MLP_CASE(64)
-    MALIB_MLP_CASE(128)
-    MALIB_MLP_CASE(256)
-    MALIB_MLP_CASE(512)
-#undef MALIB_MLP_CASE
-    return hipErrorInvalidValue;
 }
 
 }  // namespace malib

@@ -117,6 +117,24 @@ hipError_t launch_debug_tanh(const float* x, float* y, int64_t n, hipStream_t s)
     return hipGetLastError();
 }
 
+__global__ void debug_bf16_kernel(const float* __restrict__ x, uint32_t* __restrict__ y,
+                                  int64_t n_pairs)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (; i < n_pairs; i += stride)
+        y[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
+}
+
+hipError_t launch_debug_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s)
+{
+    int64_t pairs = n / 2;
+    int64_t blocks = (pairs + 255) / 256;
+    blocks = blocks > 65536 ? 65536 : (blocks < 1 ? 1 : blocks);
+    debug_bf16_kernel<<<(int)blocks, 256, 0, s>>>(x, (uint32_t*)y, pairs);
+    return hipGetLastError();
+}
+
 __global__ void debug_philox_kernel(const uint64_t* __restrict__ ctr, uint64_t k0, uint64_t k1,
                                     uint64_t* __restrict__ out, int64_t n)
 {

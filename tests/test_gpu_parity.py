@@ -58,6 +58,36 @@ def test_tanh_ref_device_bitwise_sampled():
         assert same.all(), hex(int(bits[np.argmin(same)]))
 
 
+def test_bf16_device_matches_oracle():
+    """The device bf16 conversion (observations, weights, hidden activations)
+    equals the oracle's round-to-nearest-even bit for bit: every low half-word
+    under a set of high half-words (zeros, subnormals, normals, the largest
+    finite values, infinities, NaNs; both signs) plus a strided sample of all
+    patterns (NaNs compared as NaN)."""
+    import paper_2106_07551_amd as M
+    highs = sorted({(e << 7) | m for e in list(range(0, 6)) + list(range(118, 138)) +
+                    list(range(250, 256)) for m in (0, 1, 0x3F, 0x40, 0x7E, 0x7F)})
+    bits, ref = [], []
+    for sign in (0, 0x8000):
+        for h in highs:
+            first = (sign | h) << 16
+            bits.append(np.arange(1 << 16, dtype=np.uint32) + np.uint32(first))
+            ref.append(oracle.bf16_range(first, 1 << 16))
+    stride = np.arange(0, 2**32, 65521, dtype=np.uint64).astype(np.uint32)
+    bits.append(stride)
+    ref.append(np.array([oracle.bf16_bits(float(v)) for v in stride.view(np.float32)],
+                        np.uint16))
+    bits = np.concatenate(bits)
+    ref = np.concatenate(ref)
+    if bits.size % 2:
+        bits, ref = bits[:-1], ref[:-1]
+    x = bits.view(np.float32)
+    y = M.debug_bf16(torch.from_numpy(x.copy()).cuda()).cpu().numpy().view(np.uint16)
+    nan = np.isnan(x)
+    ok = (y == ref) | (nan & ((y & 0x7F80) == 0x7F80) & ((y & 0x7F) != 0))
+    assert ok.all(), hex(int(bits[np.argmin(ok)]))
+
+
 @pytest.mark.parametrize("c", [3, 5])
 def test_meta_sample_device_matches_oracle(c):
     import paper_2106_07551_amd as M
