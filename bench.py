@@ -53,6 +53,30 @@ def describe(wl):
     return d
 
 
+def profiled_traffic(workload):
+    """HBM bytes per launch of the grouped policy forward from the committed
+    rocprofv3 summary of this workload (FETCH_SIZE and WRITE_SIZE scaled by the
+    plain-copy calibration), or None when there is none or the kernel sources
+    changed since it was taken."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("k_policy.hip", "device.hpp", "internal.hpp"):
+        with open(os.path.join(ROOT, "paper_2106_07551_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    cur = h.hexdigest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        kv = {}
+        for line in open(path):
+            if "=" in line and not line.startswith(("#", "|", "-")):
+                k, _, v = line.strip().partition("=")
+                kv[k] = v
+        if kv.get("workload") == workload and kv.get("kernel_source_sha256") == cur \
+                and "traffic_bytes_per_launch" in kv:
+            return int(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
+    return None, None
+
+
 def cpu_baseline(wl, budget_s=12.0, max_s=30.0):
     """The oracle (single-threaded C) on whole episodes of the same workload,
     env by env until ~budget_s of CPU time."""
@@ -157,10 +181,15 @@ def main():
         flops = policy_flops_per_frame(wl.dims) * n * na        # per launch
         avg_s = kern["policy"]["total_ms"] / max(kern["policy"]["launches"], 1) / 1000.0
         ach = flops / avg_s / 1e12
+        traffic, src = profiled_traffic(wl.name)
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                "traffic": None, "kernel": "grouped policy forward (mlp_bf16_kernel)",
+                "traffic": traffic, "kernel": "grouped policy forward (mlp_bf16_kernel)",
                 "flops_per_launch": flops}
+        if traffic is not None:
+            roof["traffic_unit"] = "bytes per launch (HBM, rocprofv3 FETCH_SIZE+WRITE_SIZE)"
+            roof["traffic_source"] = src
+            roof["traffic_GBps"] = round(traffic / avg_s / 1e9, 1)
     out = {
         "metric": "agent-frames/s on 1 MI355X (payoff-table fill)",
         "value": round(value, 1),

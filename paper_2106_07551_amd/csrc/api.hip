@@ -255,7 +255,7 @@ void malib_pop_destroy(malib_pop_t p)
                     (void*)p->dev_frames})
         if (q)
             (void)hipFree(q);
-    for (DevBuf* b : {&p->perm, &p->hist, &p->base, &p->offsets, &p->tile_off, &p->logits,
+    for (DevBuf* b : {&p->perm, &p->perm_env, &p->tile_info, &p->hist, &p->base, &p->offsets, &p->tile_off, &p->logits,
                       &p->actions, &p->ret, &p->state0, &p->state1, &p->wt, &p->done,
                       &p->thresholds})
         release(*b);
@@ -381,7 +381,8 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
     // ---- buffers
     const int64_t ns = n_envs * n_agents;
     const bool mlp = pop->kind != MALIB_POLICY_TABULAR;
-    const int tile_rows = pop->kind == MALIB_POLICY_MLP_F32 ? kF32TileRows : kTileRows;
+    const int tile_rows = pop->kind == MALIB_POLICY_MLP_BF16 ? kBf16TileRows : kF32TileRows;
+    const int max_tiles = max_tiles_for(ns, pop->P, tile_rows);
     const int n_chunks = (int)((ns + kBucketChunk - 1) / kBucketChunk);
     HIP_TRY(ensure(pop->logits, sizeof(float) * ns * pop->A));
     HIP_TRY(ensure(pop->actions, ns));
@@ -398,6 +399,8 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
         HIP_TRY(ensure(pop->wt, sizeof(float) * env->d * env->d));
     if (mlp) {
         HIP_TRY(ensure(pop->perm, sizeof(int32_t) * ns));
+        HIP_TRY(ensure(pop->perm_env, sizeof(int32_t) * ns));
+        HIP_TRY(ensure(pop->tile_info, sizeof(int4) * (size_t)max_tiles));
         HIP_TRY(ensure(pop->hist, sizeof(int32_t) * (size_t)pop->P * n_chunks));
         HIP_TRY(ensure(pop->base, sizeof(int32_t) * (size_t)pop->P * n_chunks));
         HIP_TRY(ensure(pop->offsets, sizeof(int32_t) * (pop->P + 1)));
@@ -418,9 +421,10 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
     int pi = prof_begin(*pop, MALIB_K_SETUP, s);
     HIP_TRY(hipMemsetAsync(ret, 0, sizeof(float) * ns, s));
     if (mlp)
-        HIP_TRY(launch_bucket(pair_assign, ns, pop->P, tile_rows, (int32_t*)pop->hist.ptr,
-                              (int32_t*)pop->base.ptr, perm, offsets, tile_off, pop->dev_flags,
-                              s));
+        HIP_TRY(launch_bucket(pair_assign, ns, n_agents, pop->P, tile_rows, max_tiles,
+                              (int32_t*)pop->hist.ptr, (int32_t*)pop->base.ptr, perm,
+                              (int32_t*)pop->perm_env.ptr, offsets, tile_off,
+                              (int4*)pop->tile_info.ptr, pop->dev_flags, s));
     HIP_TRY(launch_reset(ea, n_envs, seed, env_offset, cur, done, s));
     if (env->kind == MALIB_ENV_FEATURE)
         HIP_TRY(launch_transpose(env->W, (float*)pop->wt.ptr, env->d, s));
@@ -450,10 +454,12 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
             HIP_TRY(launch_tabular(pop->tab, pair_assign, ns, pop->A, pop->P, pop->dev_flags,
                                    logits, s));
         else if (pop->kind == MALIB_POLICY_MLP_F32)
-            HIP_TRY(launch_mlp_f32(*pop, perm, offsets, tile_off, ns, n_agents, cur, logits, s));
+            HIP_TRY(launch_mlp_f32(*pop, perm, (const int4*)pop->tile_info.ptr, ns, n_agents,
+                                   cur, logits, s));
         else
-            HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d, perm, offsets,
-                                    tile_off, ns, cur, done, logits, s));
+            HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d, tile_rows,
+                                    perm, (const int32_t*)pop->perm_env.ptr,
+                                    (const int4*)pop->tile_info.ptr, ns, cur, logits, s));
         prof_end(*pop, pi, s);
         if (si >= 0 && trace->logits)
             HIP_TRY(hipMemcpyAsync(trace->logits + (int64_t)si * ns * pop->A, logits,

@@ -101,8 +101,8 @@ __global__ __launch_bounds__(1024) void bucket_scan_kernel(
 }
 
 __global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
-    const int32_t* __restrict__ pids, int64_t n_slots, int P, int n_chunks,
-    const int32_t* __restrict__ base, int32_t* __restrict__ perm)
+    const int32_t* __restrict__ pids, int64_t n_slots, int n_agents, int P, int n_chunks,
+    const int32_t* __restrict__ base, int32_t* __restrict__ perm, int32_t* __restrict__ perm_env)
 {
     __shared__ int wcnt[kWaves][kMaxP];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -150,6 +150,7 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
             if (mine) {
                 int rank = __popcll(m & lt_mask);
                 perm[dst0 + rank] = (int32_t)i;
+                perm_env[dst0 + rank] = (int32_t)(i / n_agents);
             }
             if (lane == leader)
                 run[wave][lp] = dst0 + __popcll(m);
@@ -159,17 +160,46 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
     }
 }
 
-hipError_t launch_bucket(const int32_t* pids, int64_t n_slots, int P, int tile_rows,
-                         int32_t* hist, int32_t* base, int32_t* perm, int32_t* offsets,
-                         int32_t* tile_off, int* flags, hipStream_t s)
+// One thread per tile slot: the policy owning tile t (the last policy whose
+// first tile is <= t, which skips empty buckets), its first row and row count.
+__global__ void tile_table_kernel(const int32_t* __restrict__ offsets,
+                                  const int32_t* __restrict__ tile_off, int P, int tile_rows,
+                                  int max_tiles, int4* __restrict__ info)
+{
+    int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= max_tiles)
+        return;
+    if (t >= tile_off[P]) {
+        info[t] = make_int4(-1, 0, 0, 0);
+        return;
+    }
+    int lo = 0, hi = P - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (tile_off[mid] <= t)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    int r0 = offsets[lo] + (t - tile_off[lo]) * tile_rows;
+    int rows = min(tile_rows, offsets[lo + 1] - r0);
+    info[t] = make_int4(lo, r0, rows, 0);
+}
+
+hipError_t launch_bucket(const int32_t* pids, int64_t n_slots, int n_agents, int P,
+                         int tile_rows, int max_tiles, int32_t* hist, int32_t* base,
+                         int32_t* perm, int32_t* perm_env, int32_t* offsets, int32_t* tile_off,
+                         int4* tile_info, int* flags, hipStream_t s)
 {
     int n_chunks = (int)((n_slots + kBucketChunk - 1) / kBucketChunk);
     bucket_hist_kernel<<<n_chunks, kBucketThreads, 0, s>>>(pids, n_slots, P, n_chunks, hist,
                                                            flags);
     bucket_scan_kernel<<<1, 1024, 0, s>>>(hist, P, n_chunks, tile_rows, base, offsets,
                                           tile_off);
-    bucket_scatter_kernel<<<n_chunks, kBucketThreads, 0, s>>>(pids, n_slots, P, n_chunks,
-                                                              base, perm);
+    bucket_scatter_kernel<<<n_chunks, kBucketThreads, 0, s>>>(pids, n_slots, n_agents, P,
+                                                              n_chunks, base, perm, perm_env);
+    tile_table_kernel<<<(max_tiles + 255) / 256, 256, 0, s>>>(offsets, tile_off, P, tile_rows,
+                                                             max_tiles, tile_info);
     return hipGetLastError();
 }
 

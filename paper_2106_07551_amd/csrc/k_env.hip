@@ -199,6 +199,19 @@ __global__ __launch_bounds__(256) void step_feature_kernel(
     const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
     const int64_t e0 = (int64_t)blockIdx.x * kFeatEnvs;
 
+    // the actions of this thread's envs, packed 8 bits per seat (at most 8
+    // seats); envs past the end read as action 0 and are never stored
+    uint64_t act_pk[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int64_t e = e0 + ty * EPT + i;
+        uint64_t v = 0;
+        if (e < n)
+            for (int q = 0; q < ea.n_agents; ++q)
+                v |= (uint64_t)act[e * ea.n_agents + q] << (8 * q);
+        act_pk[i] = v;
+    }
+
     float acc[EPT][NJ];
 #pragma unroll
     for (int i = 0; i < EPT; ++i)
@@ -272,24 +285,42 @@ __global__ __launch_bounds__(256) void step_feature_kernel(
         __syncthreads();
     }
 
-    // epilogue: embeddings in seat order, tanh_ref, store s' (global + LDS)
-    float* Sl = Ws;   // [32][D+1]
+    // epilogue: embeddings in seat order (seat-outer so that each seat's loads
+    // for all of the thread's outputs are independent), tanh_ref, store s'
+    float* Sl = Ws;   // [kFeatEnvs][D+1]
+    float pre[EPT][NJ];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+            pre[i][j] = acc[i][j];
+#pragma unroll
+    for (int q = 0; q < kMaxAgents; ++q) {
+        if (q < ea.n_agents) {
+            int off[EPT];
+#pragma unroll
+            for (int i = 0; i < EPT; ++i) {
+                const int a_q = (int)((act_pk[i] >> (8 * q)) & 0xFFu);
+                off[i] = (q * ea.A + a_q) * D + tx;
+            }
+#pragma unroll
+            for (int i = 0; i < EPT; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    pre[i][j] = pre[i][j] + emb[off[i] + 64 * j];
+        }
+    }
 #pragma unroll
     for (int i = 0; i < EPT; ++i) {
-        int el = ty * EPT + i;
-        int64_t e = e0 + el;
-        if (e < n) {
-            const uint8_t* ae = act + e * ea.n_agents;
+        const int el = ty * EPT + i;
+        const int64_t e = e0 + el;
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                int k = tx + 64 * j;
-                float pre = acc[i][j];
-                for (int q = 0; q < ea.n_agents; ++q)
-                    pre = pre + emb[((int64_t)q * ea.A + ae[q]) * D + k];
-                float sn = tanh_ref(pre);
+        for (int j = 0; j < NJ; ++j) {
+            const int k = tx + 64 * j;
+            const float sn = tanh_ref(pre[i][j]);
+            if (e < n)
                 s_out[e * D + k] = sn;
-                Sl[el * (D + 1) + k] = sn;
-            }
+            Sl[el * (D + 1) + k] = sn;
         }
     }
     __syncthreads();

@@ -87,23 +87,6 @@ hipError_t launch_tabular(const float* tab, const int32_t* pids, int64_t n_slots
     return hipGetLastError();
 }
 
-// ------------------------------------------------------------ tile lookup
-
-// Tile t of the bucketed slots: the policy p with tile_off[p] <= t < tile_off[p+1]
-// and its row range in perm.
-__device__ __forceinline__ int tile_policy(const int32_t* __restrict__ tile_off, int P, int t)
-{
-    int lo = 0, hi = P - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (tile_off[mid] <= t)
-            lo = mid;
-        else
-            hi = mid - 1;
-    }
-    return lo;
-}
-
 // ------------------------------------------------------------------ fp32 MLP
 
 // Iterated matrix game observation element c (0..8A-1) of a seat: lag c/(2A),
@@ -122,10 +105,10 @@ __device__ __forceinline__ float iter_obs(uint32_t hist, int seat, int A, int c)
 struct MlpF32Args {
     const float* w1; const float* w2; const float* w3;
     const float* b1; const float* b2; const float* b3;
-    const int32_t* perm; const int32_t* offsets; const int32_t* tile_off;
+    const int32_t* perm; const int4* tile_info;
     const uint16_t* hist;
     float* logits;
-    int P, A, IN, n_agents;
+    int P, A, IN, n_agents, max_tiles;
 };
 
 template <int HID, int IN, int AMAX>
@@ -133,12 +116,15 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
 {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int t = blockIdx.x * 4 + wave;
-    if (t >= a.tile_off[a.P])
+    if (t >= a.max_tiles)
         return;
-    int p = tile_policy(a.tile_off, a.P, t);
-    p = __builtin_amdgcn_readfirstlane(p);
-    const int r0 = a.offsets[p] + (t - a.tile_off[p]) * kF32TileRows;
-    const int r1 = min(r0 + kF32TileRows, a.offsets[p + 1]);
+    const int4 ti = a.tile_info[t];
+    const int p = __builtin_amdgcn_readfirstlane(ti.x);
+    if (p < 0)
+        return;
+    const int r0 = __builtin_amdgcn_readfirstlane(ti.y);
+    // (tiles of kF32TileRows = 64 rows: one row per lane)
+    const int r1 = r0 + __builtin_amdgcn_readfirstlane(ti.z);
     const int row = r0 + lane;
     const bool valid = row < r1;
     const int slot = a.perm[valid ? row : r0];
@@ -189,9 +175,9 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
     }
 }
 
-hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int32_t* offsets,
-                          const int32_t* tile_off, int64_t n_slots, int n_agents,
-                          const void* state, float* logits, hipStream_t s)
+hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int4* tile_info,
+                          int64_t n_slots, int n_agents, const void* state, float* logits,
+                          hipStream_t s)
 {
     MlpF32Args a;
     a.w1 = (const float*)pop.w[0];
@@ -201,16 +187,19 @@ hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int32_t* of
     a.b2 = pop.b[1];
     a.b3 = pop.b[2];
     a.perm = perm;
-    a.offsets = offsets;
-    a.tile_off = tile_off;
+    a.tile_info = tile_info;
     a.hist = (const uint16_t*)state;
     a.logits = logits;
     a.P = pop.P;
     a.A = pop.A;
     a.IN = pop.in_dim;
     a.n_agents = n_agents;
-    int64_t max_tiles = (n_slots + kF32TileRows - 1) / kF32TileRows + pop.P;
-    int blocks = (int)((max_tiles + 3) / 4);
+    // tile_info holds max_tiles_for() entries; a wave past them would read out
+    // of range, so the grid covers exactly that many wavefronts (rounded down
+    // to whole workgroups plus one guarded workgroup)
+    const int max_tiles = max_tiles_for(n_slots, pop.P, kF32TileRows);
+    a.max_tiles = max_tiles;
+    int blocks = (max_tiles + 3) / 4;
     if (pop.in_dim != 24 || pop.A > 3)
         return hipErrorInvalidValue;
     if (pop.hid == 32)
@@ -227,17 +216,17 @@ hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int32_t* of
 enum { kObsFeature = 0, kObsPursuit = 1, kObsIter = 2 };
 
 constexpr int kLdw = 520;           // LDS row stride (bf16): 512 + 8 to spread banks
-constexpr int kMlpThreads = 256;    // 4 wavefronts; two workgroups share a CU
 
 struct MlpBf16Args {
     const uint4* w1; const uint4* w2; const uint4* w3;
     const float* b1; const float* b2; const float* b3;
-    const int32_t* perm; const int32_t* offsets; const int32_t* tile_off;
+    const int32_t* perm; const int32_t* perm_env; const int4* tile_info;
     const void* state;
     float* logits;
     int P, A, in_dim, n_agents, grid, d;
     int64_t n_envs;
     int n_blocks;                   // launched workgroups (a multiple of 8)
+    int max_tiles;                  // entries of tile_info
 };
 
 // Ring of weight fragments of one layer: k-steps s, s+1, ... in flight, so a
@@ -391,27 +380,32 @@ __device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], int
     }
 }
 
-template <int HID>
+// Wavefront grid of a HID-wide layer: WAVES wavefronts over (HID/32 n-tiles) x
+// (RTILES row-tiles of 32); each wave owns NT n-tiles x RT row-tiles.
+template <int HID, int WAVES, int RTILES>
 struct HidSplit {
-    // four wavefronts over (HID/32 n-tiles) x (2 row-tiles of 32)
-    static constexpr int NT = HID >= 256 ? HID / 128 : 1;
-    static constexpr int RT = HID >= 128 ? 2 : 1;
-    static constexpr int NGROUPS = (HID / 32) / NT;
+    static constexpr int NTT = HID / 32;
+    static constexpr int NGROUPS = NTT >= WAVES ? WAVES : NTT;
+    static constexpr int RGROUPS = WAVES / NGROUPS;
+    static constexpr int NT = NTT / NGROUPS;
+    static constexpr int RT = RTILES / RGROUPS;
     static constexpr int DEPTH = NT >= 4 ? 3 : 4;
+    static_assert(NGROUPS * RGROUPS == WAVES && NT * NGROUPS == NTT && RT * RGROUPS == RTILES,
+                  "wave split");
 };
 
 // Observation rows of the tile -> LDS (bf16).  KIN is the padded input width.
-template <int OBS, int KIN>
+template <int OBS, int KIN, int MR, int THREADS>
 __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_slot,
                                           const int* row_env, uint16_t* buf, int tid)
 {
     if (OBS == kObsFeature) {
         // KIN == d: rows of d floats, as float4; thread t keeps column t % (KIN/4)
         constexpr int Q4 = KIN / 4;
-        constexpr int ROWS_PER_PASS = kMlpThreads / Q4;
-        constexpr int PASSES = kTileRows / ROWS_PER_PASS;
+        constexpr int ROWS_PER_PASS = THREADS / Q4;
+        constexpr int PASSES = MR / ROWS_PER_PASS;
         const int c = (tid % Q4) * 4, r0 = tid / Q4;
-        constexpr int BATCH = PASSES < 4 ? PASSES : 4;
+        constexpr int BATCH = PASSES < 16 ? PASSES : 16;
         typedef float v4f __attribute__((ext_vector_type(4)));
         const float* S = (const float*)a.state + c;
 #pragma unroll
@@ -432,7 +426,7 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
         }
     } else if (OBS == kObsPursuit) {
         const uint8_t* pos = (const uint8_t*)a.state;
-        for (int i = tid; i < kTileRows * KIN; i += kMlpThreads) {
+        for (int i = tid; i < MR * KIN; i += THREADS) {
             const int r = i / KIN, c = i - r * KIN;
             const int slot = row_slot[r];
             float v = 0.0f;
@@ -453,7 +447,7 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
         }
     } else {
         const uint16_t* hist = (const uint16_t*)a.state;
-        for (int i = tid; i < kTileRows * KIN; i += kMlpThreads) {
+        for (int i = tid; i < MR * KIN; i += THREADS) {
             const int r = i / KIN, c = i - r * KIN;
             const int slot = row_slot[r];
             float v = 0.0f;
@@ -467,27 +461,31 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
     }
 }
 
-template <int HID, int OBS, int KIN>
-__global__ __launch_bounds__(kMlpThreads, 2) void mlp_bf16_kernel(MlpBf16Args a)
+// MR rows per tile (the library uses 64: four wavefronts, two workgroups per CU).
+template <int HID, int OBS, int KIN, int MR>
+__global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpBf16Args a)
 {
-    __shared__ __attribute__((aligned(16))) uint16_t buf[kTileRows * kLdw];
-    __shared__ int row_slot[kTileRows];
-    __shared__ int row_env[kTileRows];
-    __shared__ float red[2 * 16 * 64];   // output-layer partial sums of the second k-half
+    constexpr int THREADS = MR * 4, WAVES = MR / 16, RTILES = MR / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t buf[MR * kLdw];
+    __shared__ int row_slot[MR];
+    __shared__ int row_env[MR];
+    __shared__ float red[RTILES * 16 * 64];   // output-layer partial sums of the second k-half
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
     // workgroups are dispatched round-robin over the 8 XCDs: give each XCD a
     // contiguous run of tiles so that a policy's tiles share one L2
     const int per = a.n_blocks / 8;
     const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
-    const int total = a.tile_off[a.P];
-    if (t >= total)
+    if (t >= a.max_tiles)
         return;
-    const int p = tile_policy(a.tile_off, a.P, t);
-    const int r0 = a.offsets[p] + (t - a.tile_off[p]) * kTileRows;
-    const int nrows = min(kTileRows, a.offsets[p + 1] - r0);
+    const int4 ti = a.tile_info[t];
+    const int p = ti.x;
+    if (p < 0)
+        return;
+    const int r0 = ti.y;
+    const int nrows = ti.z;
 
-    using S = HidSplit<HID>;
+    using S = HidSplit<HID, WAVES, RTILES>;
     const int nt0 = (wave % S::NGROUPS) * S::NT;
     const int rt0 = (wave / S::NGROUPS) * S::RT;
     const uint4* W1 = a.w1 + (int64_t)p * (HID / 32) * (KIN / 16) * 64;
@@ -495,13 +493,12 @@ __global__ __launch_bounds__(kMlpThreads, 2) void mlp_bf16_kernel(MlpBf16Args a)
     WRing<S::NT, S::DEPTH> ring;
     ring_fill(ring, W1, KIN / 16, nt0, lane);     // overlaps the observation gather
 
-    if (tid < kTileRows) {
-        const int slot = tid < nrows ? a.perm[r0 + tid] : -1;
-        row_slot[tid] = slot;
-        row_env[tid] = slot >= 0 ? slot / a.n_agents : -1;
+    if (tid < MR) {
+        row_slot[tid] = tid < nrows ? a.perm[r0 + tid] : -1;
+        row_env[tid] = tid < nrows ? a.perm_env[r0 + tid] : -1;
     }
     __syncthreads();
-    build_obs<OBS, KIN>(a, row_slot, row_env, buf, tid);
+    build_obs<OBS, KIN, MR, THREADS>(a, row_slot, row_env, buf, tid);
     __syncthreads();
 
     f32x16 acc[S::NT][S::RT];
@@ -516,7 +513,7 @@ __global__ __launch_bounds__(kMlpThreads, 2) void mlp_bf16_kernel(MlpBf16Args a)
     mfma_layer<S::NT, S::RT, S::DEPTH>(ring, W2, HID / 16, nt0, rt0, buf, lane,
                                        a.b2 + p * HID, acc);
     constexpr int KH = HID / 32;                    // k-steps per half of the output layer
-    const int h = wave >> 1, rt = wave & 1;
+    const int h = wave / RTILES, rt = wave % RTILES;
     OutFrags<KH> of;
     out_fill<KH>(of, a.w3 + (int64_t)p * (HID / 16) * 64, h, lane);   // overlaps the epilogue
     __syncthreads();
@@ -552,37 +549,40 @@ __global__ __launch_bounds__(kMlpThreads, 2) void mlp_bf16_kernel(MlpBf16Args a)
 }
 
 template <int HID, int OBS, int KIN>
-static void launch_one(const MlpBf16Args& a, int blocks, hipStream_t s)
+static void launch_one(const MlpBf16Args& a, int rows, int blocks, hipStream_t s)
 {
-    mlp_bf16_kernel<HID, OBS, KIN><<<blocks, kMlpThreads, 0, s>>>(a);
+    (void)rows;   // kBf16TileRows
+    mlp_bf16_kernel<HID, OBS, KIN, kBf16TileRows><<<blocks, kBf16TileRows * 4, 0, s>>>(a);
 }
 
 template <int HID>
-static hipError_t launch_hid(const MlpBf16Args& a, int obs, int in_pad, int blocks, hipStream_t s)
+static hipError_t launch_hid(const MlpBf16Args& a, int obs, int in_pad, int rows, int blocks,
+                             hipStream_t s)
 {
     if (obs == kObsPursuit && in_pad == 80)
-        launch_one<HID, kObsPursuit, 80>(a, blocks, s);
+        launch_one<HID, kObsPursuit, 80>(a, rows, blocks, s);
     else if (obs == kObsIter && in_pad == 32)
-        launch_one<HID, kObsIter, 32>(a, blocks, s);
+        launch_one<HID, kObsIter, 32>(a, rows, blocks, s);
     else if (obs == kObsFeature && in_pad == 64)
-        launch_one<HID, kObsFeature, 64>(a, blocks, s);
+        launch_one<HID, kObsFeature, 64>(a, rows, blocks, s);
     else if (obs == kObsFeature && in_pad == 128)
-        launch_one<HID, kObsFeature, 128>(a, blocks, s);
+        launch_one<HID, kObsFeature, 128>(a, rows, blocks, s);
     else if (obs == kObsFeature && in_pad == 256)
-        launch_one<HID, kObsFeature, 256>(a, blocks, s);
+        launch_one<HID, kObsFeature, 256>(a, rows, blocks, s);
     else if (obs == kObsFeature && in_pad == 512)
-        launch_one<HID, kObsFeature, 512>(a, blocks, s);
+        launch_one<HID, kObsFeature, 512>(a, rows, blocks, s);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
 hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid, int d,
-                           const int32_t* perm, const int32_t* offsets, const int32_t* tile_off,
-                           int64_t n_slots, const void* state, const uint8_t* done,
+                           int tile_rows, const int32_t* perm, const int32_t* perm_env,
+                           const int4* tile_info, int64_t n_slots, const void* state,
                            float* logits, hipStream_t s)
 {
-    (void)done;
+    if (tile_rows != kBf16TileRows)
+        return hipErrorInvalidValue;
     MlpBf16Args a;
     a.w1 = (const uint4*)pop.w[0];
     a.w2 = (const uint4*)pop.w[1];
@@ -591,8 +591,8 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
     a.b2 = pop.b[1];
     a.b3 = pop.b[2];
     a.perm = perm;
-    a.offsets = offsets;
-    a.tile_off = tile_off;
+    a.perm_env = perm_env;
+    a.tile_info = tile_info;
     a.state = state;
     a.logits = logits;
     a.P = pop.P;
@@ -602,16 +602,17 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
     a.grid = grid;
     a.d = d;
     a.n_envs = n_slots / n_agents;
-    int64_t max_tiles = (n_slots + kTileRows - 1) / kTileRows + pop.P;
-    int blocks = (int)((max_tiles + 7) / 8 * 8);
+    const int max_tiles = max_tiles_for(n_slots, pop.P, tile_rows);
+    int blocks = (max_tiles + 7) / 8 * 8;
     a.n_blocks = blocks;
+    a.max_tiles = max_tiles;
     int obs = env_kind == MALIB_ENV_FEATURE ? kObsFeature
               : env_kind == MALIB_ENV_PURSUIT ? kObsPursuit : kObsIter;
     switch (pop.hid) {
-    case 64: return launch_hid<64>(a, obs, pop.in_pad, blocks, s);
-    case 128: return launch_hid<128>(a, obs, pop.in_pad, blocks, s);
-    case 256: return launch_hid<256>(a, obs, pop.in_pad, blocks, s);
-    case 512: return launch_hid<512>(a, obs, pop.in_pad, blocks, s);
+    case 64: return launch_hid<64>(a, obs, pop.in_pad, tile_rows, blocks, s);
+    case 128: return launch_hid<128>(a, obs, pop.in_pad, tile_rows, blocks, s);
+    case 256: return launch_hid<256>(a, obs, pop.in_pad, tile_rows, blocks, s);
+    case 512: return launch_hid<512>(a, obs, pop.in_pad, tile_rows, blocks, s);
     default: return hipErrorInvalidValue;
     }
 }

@@ -132,7 +132,7 @@ def test_parity_iter_ragged():
 
 def test_parity_pursuit_ragged():
     """Pursuit, bf16 MLP 75-256-256-5, full population of 32, 300 envs with
-    uniformly sampled pairs (ragged 128-row tiles), horizon 100 with captures."""
+    uniformly sampled pairs (ragged 64-row tiles), horizon 100 with captures."""
     wl = W.make(3, n_envs=300)
     g = run_gpu(wl, snaps=[0, 3, 50, 99])
     rep = check_parity(wl, g)
