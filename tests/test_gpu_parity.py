@@ -58,6 +58,22 @@ def test_tanh_ref_device_bitwise_sampled():
         assert same.all(), hex(int(bits[np.argmin(same)]))
 
 
+def test_tanh_ref_device_bitwise_exhaustive():
+    """tanh_ref on the device equals the oracle's bit for bit over all 2^32 fp32
+    bit patterns (NaNs compared as NaN), in chunks of 2^27."""
+    import paper_2106_07551_amd as M
+    chunk = 1 << 27
+    x = torch.empty(chunk, dtype=torch.int32, device="cuda")
+    base = torch.arange(chunk, dtype=torch.int32, device="cuda")
+    for c in range(1 << 5):
+        first = c * chunk
+        x.copy_(base + (first - (1 << 32) if first >= (1 << 31) else first))
+        y = M.debug_tanh_ref(x.view(torch.float32)).cpu().numpy()
+        ref = oracle.tanh_range(first, chunk)
+        same = (y.view(np.uint32) == ref.view(np.uint32)) | (np.isnan(y) & np.isnan(ref))
+        assert same.all(), hex(first + int(np.argmin(same)))
+
+
 def test_bf16_device_matches_oracle():
     """The device bf16 conversion (observations, weights, hidden activations)
     equals the oracle's round-to-nearest-even bit for bit: every low half-word
