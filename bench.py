@@ -157,7 +157,9 @@ def main():
         one_step()
     torch.cuda.synchronize()
 
-    pop.profile_enable(True)
+    # timed region: HIP events around one grouped-forward launch in four (the
+    # events' own cost would otherwise show up in the fill time)
+    pop.profile_enable(True, kernels=[M.K_POLICY], every=4)
     frames = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -167,6 +169,12 @@ def main():
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     kern = {}
+    ms, cnt = pop.profile_read(M.K_POLICY)
+    policy_avg_us = 1000.0 * ms / max(cnt, 1)
+    policy_timed = cnt
+    # per-kernel breakdown from one more (untimed) fill with every launch timed
+    pop.profile_enable(True)
+    one_step()
     for name, k in (("policy", M.K_POLICY), ("sample", M.K_SAMPLE), ("env", M.K_ENV),
                     ("setup", M.K_SETUP), ("payoff", M.K_PAYOFF)):
         ms, cnt = pop.profile_read(k)
@@ -179,13 +187,14 @@ def main():
     roof = None
     if wl.pol_kind == W.MLP_BF16:
         flops = policy_flops_per_frame(wl.dims) * n * na        # per launch
-        avg_s = kern["policy"]["total_ms"] / max(kern["policy"]["launches"], 1) / 1000.0
+        avg_s = policy_avg_us * 1e-6
         ach = flops / avg_s / 1e12
         traffic, src = profiled_traffic(wl.name)
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                 "traffic": traffic, "kernel": "grouped policy forward (mlp_bf16_kernel)",
-                "flops_per_launch": flops}
+                "flops_per_launch": flops, "avg_launch_us": round(policy_avg_us, 3),
+                "timed_launches": policy_timed}
         if traffic is not None:
             roof["traffic_unit"] = "bytes per launch (HBM, rocprofv3 FETCH_SIZE+WRITE_SIZE)"
             roof["traffic_source"] = src

@@ -255,12 +255,14 @@ enum {
     MALIB_K_COUNT = 5
 };
 
-/* Enable (1) or disable (0) HIP-event timing of every kernel launch of the
- * handle, on the stream the kernel runs on.  Enabling clears the totals. */
-malib_status malib_profile_enable(malib_pop_t pop, int32_t enable);
+/* HIP-event timing of the handle's kernel launches, on the stream each kernel
+ * runs on.  mask: bit (1 << MALIB_K_x) enables class x (0 disables timing);
+ * every: time one launch in `every` of each enabled class (>= 1), so that the
+ * events' own cost stays small in long runs.  Each call clears the totals. */
+malib_status malib_profile_enable(malib_pop_t pop, int32_t mask, int32_t every);
 
-/* Total elapsed milliseconds and launch count of one kernel class since the
- * profile was enabled; synchronizes the recorded events. */
+/* Total elapsed milliseconds and number of timed launches of one kernel class
+ * since the profile was enabled; synchronizes the recorded events. */
 malib_status malib_profile_read(malib_pop_t pop, int32_t kernel, double* total_ms,
                                 int64_t* launches);
 

@@ -83,7 +83,7 @@ def lib():
         L.malib_meta_sample.restype = i32
         L.malib_last_error.argtypes = []
         L.malib_last_error.restype = C.c_char_p
-        L.malib_profile_enable.argtypes = [vp, i32]
+        L.malib_profile_enable.argtypes = [vp, i32, i32]
         L.malib_profile_enable.restype = i32
         L.malib_profile_read.argtypes = [vp, i32, C.POINTER(C.c_double), C.POINTER(i64)]
         L.malib_profile_read.restype = i32
@@ -176,8 +176,15 @@ class Population:
                "envs": st.envs, "device_flags": st.device_flags, "status": rc}
         return out
 
-    def profile_enable(self, on: bool = True):
-        _check(lib().malib_profile_enable(self.handle, int(on)))
+    def profile_enable(self, on: bool = True, *, kernels=None, every: int = 1):
+        """Time launches of the kernel classes in ``kernels`` (default: all when
+        ``on``), one in ``every``."""
+        mask = 0
+        if on:
+            ks = range(5) if kernels is None else kernels
+            for k in ks:
+                mask |= 1 << k
+        _check(lib().malib_profile_enable(self.handle, mask, every))
 
     def profile_read(self, kernel: int):
         ms = C.c_double()

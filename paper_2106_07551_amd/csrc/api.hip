@@ -74,7 +74,9 @@ int round_up(int x, int m) { return (x + m - 1) / m * m; }
 // ---- profiling: one event pair per launch of a kernel class
 int prof_begin(Pop& p, int kind, hipStream_t s)
 {
-    if (!p.prof.on)
+    if (!((p.prof.mask >> kind) & 1))
+        return -1;
+    if (p.prof.seen[kind]++ % p.prof.every != 0)
         return -1;
     if (p.prof.used == p.prof.pool.size()) {
         EventPair ev;
@@ -602,11 +604,16 @@ malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, i
 
 // ---------------------------------------------------------------- profiling
 
-malib_status malib_profile_enable(malib_pop_t pop, int32_t enable)
+malib_status malib_profile_enable(malib_pop_t pop, int32_t mask, int32_t every)
 {
     if (!pop)
         return fail(MALIB_E_INVAL, "pop is NULL");
-    pop->prof.on = enable != 0;
+    if (every < 1 || mask < 0 || mask >= (1 << MALIB_K_COUNT))
+        return fail(MALIB_E_INVAL, "bad profile mask %d / every %d", mask, every);
+    pop->prof.mask = mask;
+    pop->prof.every = every;
+    for (int k = 0; k < MALIB_K_COUNT; ++k)
+        pop->prof.seen[k] = 0;
     pop->prof.used = 0;
     pop->prof.kind.clear();
     return MALIB_OK;

@@ -29,7 +29,9 @@ struct EventPair {
 };
 
 struct Profile {
-    bool on = false;
+    int mask = 0;                 // bit k: time kernel class k
+    int every = 1;                // time one launch in `every` per class
+    int64_t seen[MALIB_K_COUNT] = {0, 0, 0, 0, 0};
     std::vector<EventPair> pool;
     size_t used = 0;
     std::vector<int> kind;        // kernel class of each used pair

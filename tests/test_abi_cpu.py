@@ -61,7 +61,7 @@ def test_validation_before_device_work():
     sig = np.array([1.0, 1.0], np.float32)
     assert L.malib_meta_sample(sig.ctypes.data, 3, 2, 10, 2, 1, 0, out, None) == B.E_INVAL
     assert L.malib_meta_sample(sig.ctypes.data, 1, 2, 10, 9, 1, 0, out, None) == B.E_INVAL
-    assert L.malib_profile_enable(None, 1) == B.E_INVAL
+    assert L.malib_profile_enable(None, 1, 1) == B.E_INVAL
     assert L.malib_debug_tanh_ref(None, None, 4, None) == B.E_INVAL
 
 

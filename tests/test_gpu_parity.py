@@ -226,6 +226,27 @@ def test_single_env_and_horizon_one():
     check_parity(wl, g)
 
 
+def test_profile_mask_and_stride():
+    """Only the enabled kernel classes are timed, one launch in `every`."""
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(5, P=8, n_envs=64, horizon=10)
+    pop = IO.make_population(wl)
+    env = IO.make_env(wl)
+    pairs = IO.make_pairs(wl)
+    pop.profile_enable(True, kernels=[M.K_POLICY], every=4)
+    pop.rollout(env, wl.n_envs, pairs, wl.seed, 10)
+    ms, n = pop.profile_read(M.K_POLICY)
+    assert n == 3 and ms > 0          # launches 0, 4, 8
+    assert pop.profile_read(M.K_ENV) == (0.0, 0)
+    pop.profile_enable(True)
+    pop.rollout(env, wl.n_envs, pairs, wl.seed, 10)
+    assert pop.profile_read(M.K_ENV)[1] == 10 and pop.profile_read(M.K_SETUP)[1] == 1
+    pop.profile_enable(False)
+    pop.payoff(reset=True)
+    pop.close()
+
+
 def test_bad_policy_id_is_flagged():
     import paper_2106_07551_amd as M
     from paper_2106_07551_amd import workload_io as IO
