@@ -53,6 +53,16 @@ def describe(wl):
     return d
 
 
+def policy_kernel(wl):
+    """Which bf16 policy kernel the library runs for this workload: the
+    persistent 128-row kernel for d=512 feature observations with >= 256 slots
+    per policy, the 64-row kernel otherwise."""
+    import workloads as W
+    if wl.env_kind == W.FEATURE and wl.d == 512 and wl.n_envs * wl.n_agents >= 256 * wl.P:
+        return "mlp_bf16_persist_kernel"
+    return "mlp_bf16_kernel"
+
+
 def profiled_traffic(workload):
     """HBM bytes per launch of the grouped policy forward from the committed
     rocprofv3 summary of this workload (FETCH_SIZE and WRITE_SIZE scaled by the
@@ -192,7 +202,7 @@ def main():
         traffic, src = profiled_traffic(wl.name)
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic, "kernel": "grouped policy forward (mlp_bf16_kernel)",
+                "traffic": traffic, "kernel": "grouped policy forward (" + policy_kernel(wl) + ")",
                 "flops_per_launch": flops, "avg_launch_us": round(policy_avg_us, 3),
                 "timed_launches": policy_timed}
         if traffic is not None:

@@ -74,6 +74,8 @@ def lib():
         L.ora_bf16_bits.argtypes = [C.c_float]
         L.ora_bf16_round.restype = C.c_float
         L.ora_bf16_round.argtypes = [C.c_float]
+        L.ora_bf16_relu.restype = C.c_float
+        L.ora_bf16_relu.argtypes = [C.c_float]
         L.ora_exp_ref.restype = C.c_float
         L.ora_exp_ref.argtypes = [C.c_float]
         L.ora_tanh_ref.restype = C.c_float
@@ -140,6 +142,11 @@ def bf16_bits(x):
 
 def bf16_round(x):
     return lib().ora_bf16_round(float(x))
+
+
+def bf16_relu(x):
+    """Hidden-unit ReLU of the bf16 policies (on the rounded value)."""
+    return lib().ora_bf16_relu(float(x))
 
 
 def exp_ref(x):

@@ -129,6 +129,19 @@ float ora_bf16_round(float x)
     return y;
 }
 
+/* Hidden-unit ReLU of the bf16 policies, applied to the rounded value: a bf16
+ * with its sign bit set (negative, -0, -inf, negative NaN) becomes +0, any
+ * other value is kept.  For every non-NaN x this is bf16(max(x, 0)). */
+float ora_bf16_relu(float x)
+{
+    uint32_t b = (uint32_t)ora_bf16_bits(x) << 16;
+    if (b & 0x80000000u)
+        b = 0;
+    float y;
+    memcpy(&y, &b, 4);
+    return y;
+}
+
 /* ------------------------------------------------------------------------ */
 /* exp_ref / tanh_ref: the fixed fp32 definitions used by the feature         */
 /* dynamics (the environment's tanh must be reproducible bit for bit).        */
@@ -414,7 +427,7 @@ static void mlp_f32(const ora_config* c, int p, const double* obs, float* logits
 /* bf16 MLP: the input and every hidden activation are rounded to bf16 (round to
  * nearest even); products of bf16 values are exact, the layer sum is formed in
  * fp64 and rounded to the fp32 accumulator, the fp32 bias is added in fp32;
- * hidden = bf16(max(acc, 0)); logits stay fp32. */
+ * hidden = ReLU of bf16(acc) (ora_bf16_relu); logits stay fp32. */
 static void mlp_bf16(const ora_config* c, int p, const double* obs, float* logits)
 {
     int L = c->n_layers;
@@ -435,7 +448,7 @@ static void mlp_bf16(const ora_config* c, int p, const double* obs, float* logit
                 acc += (double)ora_bf16_round(Wp[(size_t)j * in + k]) * (double)x[k];
             float a32 = (float)acc + bias_of(c, l, p, j);
             if (l + 1 < L)
-                y[j] = ora_bf16_round(a32 > 0.0f ? a32 : 0.0f);
+                y[j] = ora_bf16_relu(a32);
             else
                 y[j] = a32;
         }

@@ -190,6 +190,7 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
                                 "%s failed: %s", #expr, hipGetErrorString(e_)));          \
     } while (0)
     TRY(hipGetDevice(&p->device));
+    TRY(hipDeviceGetAttribute(&p->n_cus, hipDeviceAttributeMultiprocessorCount, p->device));
     p->kind = desc->kind;
     p->P = P;
     p->A = A;
@@ -219,7 +220,11 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
                 int op = round_up(fo, 32);
                 size_t wb = (size_t)P * (op / 32) * (ip / 16) * 64 * 16;
                 TRY(hipMalloc(&p->w[l], wb));
-                TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, p->w[l], s));
+                TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, 0, p->w[l], s));
+                if (l == 2) {
+                    TRY(hipMalloc(&p->w3k, wb));
+                    TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, 1, p->w3k, s));
+                }
             }
         }
     }
@@ -245,6 +250,8 @@ void malib_pop_destroy(malib_pop_t p)
     if (!p)
         return;
     (void)hipDeviceSynchronize();
+    if (p->w3k)
+        (void)hipFree(p->w3k);
     for (int l = 0; l < 3; ++l) {
         if (p->w[l])
             (void)hipFree(p->w[l]);
@@ -383,7 +390,11 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
     // ---- buffers
     const int64_t ns = n_envs * n_agents;
     const bool mlp = pop->kind != MALIB_POLICY_TABULAR;
-    const int tile_rows = pop->kind == MALIB_POLICY_MLP_BF16 ? kBf16TileRows : kF32TileRows;
+    const bool persist = pop->kind == MALIB_POLICY_MLP_BF16 &&
+                         use_persist_kernel(env->kind, pop->in_pad, ns, pop->P);
+    const int tile_rows = pop->kind == MALIB_POLICY_MLP_BF16
+                              ? (persist ? kPersistRows : kBf16TileRows)
+                              : kF32TileRows;
     const int max_tiles = max_tiles_for(ns, pop->P, tile_rows);
     const int n_chunks = (int)((ns + kBucketChunk - 1) / kBucketChunk);
     HIP_TRY(ensure(pop->logits, sizeof(float) * ns * pop->A));
@@ -458,6 +469,10 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
         else if (pop->kind == MALIB_POLICY_MLP_F32)
             HIP_TRY(launch_mlp_f32(*pop, perm, (const int4*)pop->tile_info.ptr, ns, n_agents,
                                    cur, logits, s));
+        else if (persist)
+            HIP_TRY(launch_mlp_bf16_persist(*pop, perm, (const int32_t*)pop->perm_env.ptr,
+                                            (const int4*)pop->tile_info.ptr, tile_off, ns,
+                                            n_agents, cur, logits, s));
         else
             HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d, tile_rows,
                                     perm, (const int32_t*)pop->perm_env.ptr,

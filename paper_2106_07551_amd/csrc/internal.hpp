@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -44,8 +45,10 @@ struct Pop {
     int in_dim = 0, hid = 0;
     int in_pad = 0;               // bf16: input padded to a multiple of 16
     int device = 0;
+    int n_cus = 0;                // compute units of the device
     // packed weights
     void* w[3] = {nullptr, nullptr, nullptr};   // bf16 fragment layout or fp32 [P][out][in]
+    void* w3k = nullptr;          // bf16 output layer in the accumulator k order
     float* b[3] = {nullptr, nullptr, nullptr};  // fp32 [P][out] (zero-filled when absent)
     float* tab = nullptr;                       // fp32 [P][A]
     // payoff accumulators: [P*P] each
@@ -112,7 +115,7 @@ hipError_t launch_payoff(const float* ret, const int32_t* pids, int64_t n_envs, 
 
 // Policy forwards.
 hipError_t launch_pack_bf16(const float* w, int P, int out, int in, int out_pad, int in_pad,
-                            void* dst, hipStream_t s);
+                            int kperm, void* dst, hipStream_t s);
 hipError_t launch_tabular(const float* tab, const int32_t* pids, int64_t n_slots, int A, int P,
                           int* flags, float* logits, hipStream_t s);
 hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int4* tile_info,
@@ -127,6 +130,19 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
                            int tile_rows, const int32_t* perm, const int32_t* perm_env,
                            const int4* tile_info, int64_t n_slots, const void* state,
                            float* logits, hipStream_t s);
+// Feature observations of d = 512 with >= 256 slots per policy on average:
+// persistent kernel over 128-row tiles (one eight-wave workgroup per CU, output
+// layer fed from the layer-2 accumulators).  For narrower observations the
+// 64-row kernel (two workgroups per CU, whose phases overlap) measured faster.
+constexpr int kPersistRows = 128;
+inline bool use_persist_kernel(int env_kind, int in_pad, int64_t n_slots, int P)
+{
+    return env_kind == MALIB_ENV_FEATURE && in_pad == 512 && n_slots >= 256 * (int64_t)P;
+}
+hipError_t launch_mlp_bf16_persist(const Pop& pop, const int32_t* perm, const int32_t* perm_env,
+                                   const int4* tile_info, const int32_t* tile_off,
+                                   int64_t n_slots, int n_agents, const void* state,
+                                   float* logits, hipStream_t s);
 
 // Diagnostics.
 hipError_t launch_debug_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);

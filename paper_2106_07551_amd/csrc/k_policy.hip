@@ -23,8 +23,16 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 //   frag[p][nt][ks][lane] = 8 bf16: W[p][nt*32 + lane%32][ks*16 + (lane/32)*8 + j]
 // which is the A operand of v_mfma_f32_32x32x16_bf16 for output tile nt and
 // k-step ks, so a wavefront loads it as 1 KiB contiguous.
+//
+// With kperm set, the k order inside each 32-wide block of inputs follows the
+// accumulator layout of the previous layer's MFMA (register g*4+q of lane i
+// holds unit (g*8 + (i/32)*4 + q) of its 32-unit tile): k-step ks takes
+// registers of groups g = 2(ks%2), 2(ks%2)+1 of tile ks/2, so that a
+// wavefront can feed its own accumulators, converted to bf16, as the B operand
+// without a trip through LDS.  Element j of lane i of k-step ks is input
+//   (ks/2)*32 + (2(ks%2) + j/4)*8 + (i/32)*4 + j%4.
 __global__ void pack_bf16_kernel(const float* __restrict__ w, int P, int out, int in,
-                                 int out_pad, int in_pad, uint4* __restrict__ dst)
+                                 int out_pad, int in_pad, int kperm, uint4* __restrict__ dst)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     int nts = out_pad / 32, kss = in_pad / 16;
@@ -43,6 +51,8 @@ __global__ void pack_bf16_kernel(const float* __restrict__ w, int P, int out, in
     for (int q = 0; q < 4; ++q) {
         float lo = 0.0f, hi = 0.0f;
         int c = col0 + 2 * q;
+        if (kperm)
+            c = (ks >> 1) * 32 + (2 * (ks & 1) + (q >> 1)) * 8 + (lane >> 5) * 4 + (2 * q & 3);
         if (row < out && c < in)
             lo = w[((int64_t)p * out + row) * in + c];
         if (row < out && c + 1 < in)
@@ -53,11 +63,13 @@ __global__ void pack_bf16_kernel(const float* __restrict__ w, int P, int out, in
 }
 
 hipError_t launch_pack_bf16(const float* w, int P, int out, int in, int out_pad, int in_pad,
-                            void* dst, hipStream_t s)
+                            int kperm, void* dst, hipStream_t s)
 {
+    if (kperm && in_pad % 32 != 0)
+        return hipErrorInvalidValue;
     int64_t total = (int64_t)P * (out_pad / 32) * (in_pad / 16) * 64;
     pack_bf16_kernel<<<(int)((total + 255) / 256), 256, 0, s>>>(w, P, out, in, out_pad, in_pad,
-                                                               (uint4*)dst);
+                                                               kperm, (uint4*)dst);
     return hipGetLastError();
 }
 
@@ -227,7 +239,29 @@ struct MlpBf16Args {
     int64_t n_envs;
     int n_blocks;                   // launched workgroups (a multiple of 8)
     int max_tiles;                  // entries of tile_info
+    // persistent kernel
+    const uint4* w3k;               // output layer packed with the accumulator k order
+    const int32_t* tile_off;        // tile_off[P] = number of tiles
 };
+
+// Weight fragments of one layer of one policy, read through a buffer resource:
+// the base address and size sit in scalar registers, each load takes the
+// lane's byte offset (lane * 16, one VGPR for all loads) and the fragment's
+// wave-uniform byte offset in a scalar register, so no 64-bit per-lane
+// addresses are kept.  Loads beyond n_frags fragments return zero.
+using Frags = __amdgpu_buffer_rsrc_t;
+
+__device__ __forceinline__ Frags frag_src(const uint4* base, int n_frags)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(base), (short)0, n_frags * 1024,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ uint4 load_frag(Frags src, int idx, uint32_t loff)
+{
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(src, (int)loff, idx * 1024, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
 
 // Ring of weight fragments of one layer: k-steps s, s+1, ... in flight, so a
 // wavefront's weight loads are issued DEPTH-1 steps ahead of their MFMAs (and
@@ -238,7 +272,7 @@ struct WRing {
 };
 
 template <int NT, int DEPTH>
-__device__ __forceinline__ void ring_fill(WRing<NT, DEPTH>& ring, const uint4* __restrict__ frag,
+__device__ __forceinline__ void ring_fill(WRing<NT, DEPTH>& ring, Frags frag,
                                           int ksteps, int nt0, int lane)
 {
 #pragma unroll
@@ -246,7 +280,7 @@ __device__ __forceinline__ void ring_fill(WRing<NT, DEPTH>& ring, const uint4* _
         if (s < ksteps)
 #pragma unroll
             for (int n = 0; n < NT; ++n)
-                ring.a[s][n] = frag[((int64_t)(nt0 + n) * ksteps + s) * 64 + lane];
+                ring.a[s][n] = load_frag(frag, (nt0 + n) * ksteps + s, lane * 16u);
 }
 
 // One MFMA layer of a wavefront: output tiles (n-tiles nt0.., row-tiles rt0..)
@@ -255,8 +289,8 @@ __device__ __forceinline__ void ring_fill(WRing<NT, DEPTH>& ring, const uint4* _
 // (i/32)*4 + r%4 of tile row rt*32 + i%32.  The ring must hold k-steps
 // 0..DEPTH-1.  (The fp32 sum order of a unit is the bias, then the k-steps.)
 template <int NT, int RT, int DEPTH>
-__device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring,
-                                           const uint4* __restrict__ frag, int ksteps, int nt0,
+__device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring, Frags frag, int ksteps,
+                                           int nt0,
                                            int rt0, const uint16_t* buf, int lane,
                                            const float* __restrict__ bias, f32x16 (&acc)[NT][RT])
 {
@@ -307,8 +341,67 @@ __device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring,
                 if (ks + DEPTH < ksteps) {
 #pragma unroll
                     for (int n = 0; n < NT; ++n)
-                        ring.a[s][n] = frag[((int64_t)(nt0 + n) * ksteps + ks + DEPTH) * 64 + lane];
+                        ring.a[s][n] = load_frag(frag, (nt0 + n) * ksteps + ks + DEPTH, lane * 16u);
                 }
+                // keep each refill in its own k-step: left alone, the scheduler
+                // may sink the loads next to their use and serialize the ring
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+}
+
+// The same layer with one B buffer: row tile r of the next k-step is read
+// from LDS as soon as this k-step's MFMAs on it are issued (row-tile-outer
+// order), which saves RT x 4 VGPRs for the wider wave tiles.
+template <int NT, int RT, int DEPTH>
+__device__ __forceinline__ void mfma_layer_1b(WRing<NT, DEPTH>& ring, Frags frag, int ksteps,
+                                              int nt0, int rt0, const uint16_t* buf, int lane,
+                                              const float* __restrict__ bias,
+                                              f32x16 (&acc)[NT][RT])
+{
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+        f32x16 b0;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float4 bb = *reinterpret_cast<const float4*>(
+                bias + (nt0 + n) * 32 + g * 8 + (lane >> 5) * 4);
+            b0[g * 4 + 0] = bb.x;
+            b0[g * 4 + 1] = bb.y;
+            b0[g * 4 + 2] = bb.z;
+            b0[g * 4 + 3] = bb.w;
+        }
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+            acc[n][r] = b0;
+    }
+    const uint16_t* bp = buf + (rt0 * 32 + (lane & 31)) * kLdw + (lane >> 5) * 8;
+    uint4 b[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+        b[r] = *reinterpret_cast<const uint4*>(bp + r * 32 * kLdw);
+    for (int k0 = 0; k0 < ksteps; k0 += DEPTH) {
+#pragma unroll
+        for (int s = 0; s < DEPTH; ++s) {
+            const int ks = k0 + s;
+            if (ks < ksteps) {
+#pragma unroll
+                for (int r = 0; r < RT; ++r) {
+#pragma unroll
+                    for (int n = 0; n < NT; ++n)
+                        acc[n][r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            __builtin_bit_cast(bf16x8, ring.a[s][n]),
+                            __builtin_bit_cast(bf16x8, b[r]), acc[n][r], 0, 0, 0);
+                    if (ks + 1 < ksteps)
+                        b[r] = *reinterpret_cast<const uint4*>(bp + r * 32 * kLdw + (ks + 1) * 16);
+                }
+                if (ks + DEPTH < ksteps) {
+#pragma unroll
+                    for (int n = 0; n < NT; ++n)
+                        ring.a[s][n] = load_frag(frag, (nt0 + n) * ksteps + ks + DEPTH, lane * 16u);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
     }
@@ -324,12 +417,12 @@ struct OutFrags {
 };
 
 template <int KH>
-__device__ __forceinline__ void out_fill(OutFrags<KH>& f, const uint4* __restrict__ frag, int h,
+__device__ __forceinline__ void out_fill(OutFrags<KH>& f, Frags frag, int h,
                                          int lane)
 {
 #pragma unroll
     for (int k = 0; k < KH; ++k)
-        f.a[k] = frag[(int64_t)(h * KH + k) * 64 + lane];
+        f.a[k] = load_frag(frag, h * KH + k, lane * 16u);
 }
 
 template <int KH>
@@ -356,6 +449,18 @@ __device__ __forceinline__ f32x16 mfma_out_half(const OutFrags<KH>& f, int h, in
     return acc0 + acc1;
 }
 
+// Hidden-unit ReLU on two accumulators: round both to bf16 (one
+// v_cvt_pk_bf16_f32), then clear every half whose sign bit is set with one
+// signed 16-bit max against 0.  For non-NaN inputs this is bf16(max(x, 0));
+// a negative NaN becomes +0 and a positive NaN stays NaN.
+typedef short short2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t relu_pack(float lo, float hi)
+{
+    short2_t v = __builtin_bit_cast(short2_t, pack_bf16x2(lo, hi));
+    v = __builtin_elementwise_max(v, short2_t{0, 0});
+    return __builtin_bit_cast(uint32_t, v);
+}
+
 // ReLU + bf16, written back as the next layer's input rows.
 template <int NT, int RT>
 __device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], int nt0, int rt0,
@@ -369,11 +474,8 @@ __device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], int
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
                 const int row = (rt0 + r) * 32 + (lane & 31);
-                float v0 = fmaxf(acc[n][r][g * 4 + 0], 0.0f);
-                float v1 = fmaxf(acc[n][r][g * 4 + 1], 0.0f);
-                float v2 = fmaxf(acc[n][r][g * 4 + 2], 0.0f);
-                float v3 = fmaxf(acc[n][r][g * 4 + 3], 0.0f);
-                uint2 pk = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+                uint2 pk = make_uint2(relu_pack(acc[n][r][g * 4 + 0], acc[n][r][g * 4 + 1]),
+                                      relu_pack(acc[n][r][g * 4 + 2], acc[n][r][g * 4 + 3]));
                 *reinterpret_cast<uint2*>(buf + row * kLdw + u0) = pk;
             }
         }
@@ -470,7 +572,8 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
     __shared__ int row_slot[MR];
     __shared__ int row_env[MR];
     __shared__ float red[RTILES * 16 * 64];   // output-layer partial sums of the second k-half
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
     // workgroups are dispatched round-robin over the 8 XCDs: give each XCD a
     // contiguous run of tiles so that a policy's tiles share one L2
@@ -479,7 +582,7 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
     if (t >= a.max_tiles)
         return;
     const int4 ti = a.tile_info[t];
-    const int p = ti.x;
+    const int p = __builtin_amdgcn_readfirstlane(ti.x);
     if (p < 0)
         return;
     const int r0 = ti.y;
@@ -488,8 +591,10 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
     using S = HidSplit<HID, WAVES, RTILES>;
     const int nt0 = (wave % S::NGROUPS) * S::NT;
     const int rt0 = (wave / S::NGROUPS) * S::RT;
-    const uint4* W1 = a.w1 + (int64_t)p * (HID / 32) * (KIN / 16) * 64;
-    const uint4* W2 = a.w2 + (int64_t)p * (HID / 32) * (HID / 16) * 64;
+    const Frags W1 = frag_src(a.w1 + (int64_t)p * (HID / 32) * (KIN / 16) * 64,
+                              (HID / 32) * (KIN / 16));
+    const Frags W2 = frag_src(a.w2 + (int64_t)p * (HID / 32) * (HID / 16) * 64,
+                              (HID / 32) * (HID / 16));
     WRing<S::NT, S::DEPTH> ring;
     ring_fill(ring, W1, KIN / 16, nt0, lane);     // overlaps the observation gather
 
@@ -515,7 +620,8 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
     constexpr int KH = HID / 32;                    // k-steps per half of the output layer
     const int h = wave / RTILES, rt = wave % RTILES;
     OutFrags<KH> of;
-    out_fill<KH>(of, a.w3 + (int64_t)p * (HID / 16) * 64, h, lane);   // overlaps the epilogue
+    out_fill<KH>(of, frag_src(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16), h,
+                 lane);                                          // overlaps the epilogue
     __syncthreads();
     hidden_epilogue<S::NT, S::RT>(acc, nt0, rt0, buf, lane);
     __syncthreads();
@@ -545,6 +651,281 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
                         out[u] = o[g * 4 + q] + b3[u];
                 }
         }
+    }
+}
+
+// ------------------------------------------------------------ persistent bf16 MLP
+
+// Feature observations, large batches: one persistent workgroup of eight
+// wavefronts per CU walks a contiguous run of tiles of up to 128 rows (the
+// tile table is built with 128-row tiles), so every weight fragment it streams
+// serves 128 rows.  Runs are equal in tiles; run i of G goes to XCD i / (G/8)
+// so that neighbouring runs (the same policies) share an L2.
+//
+// Per tile: observations (bf16, LDS) -> layer 1 -> ReLU/bf16 into LDS ->
+// layer 2 -> output layer straight from the layer-2 accumulators (the output
+// weights are packed in their k order, see pack_bf16_kernel) -> per-wave
+// partial logits summed through LDS in wave order.  The next tile's table
+// entry, row indices and output bias are fetched before layer 2, its first
+// weight fragments and observation rows while the partial logits are summed.
+template <int HID, int KIN>
+__global__ __launch_bounds__(512, 1) void mlp_bf16_persist_kernel(MlpBf16Args a)
+{
+    constexpr int MR = kPersistRows, THREADS = 512, WAVES = 8, RTILES = 4;
+    using S = HidSplit<HID, WAVES, RTILES>;
+    constexpr int NT = S::NT, RT = S::RT, NG = S::NGROUPS;
+    static_assert(NG * RTILES * 16 * 64 * 4 <= MR * kLdw * 2, "partials fit in the row buffer");
+    __shared__ __attribute__((aligned(16))) uint16_t buf[MR * kLdw];
+    __shared__ int row_slot[2][MR];
+    __shared__ int row_env[2][MR];
+    __shared__ float b3s[2][kMaxActions];
+    float* red = reinterpret_cast<float*>(buf);   // [NG][RTILES][16][64] partial logits
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int nt0 = (wave % NG) * NT, rt0 = (wave / NG) * RT, ng = wave % NG;
+
+    const int T = a.tile_off[a.P];
+    const int G = gridDim.x, ri = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+    const int t0 = (int)((int64_t)ri * T / G), t1 = (int)((int64_t)(ri + 1) * T / G);
+    if (t0 >= t1)
+        return;
+
+    constexpr int F1 = (HID / 32) * (KIN / 16), F2 = (HID / 32) * (HID / 16), F3 = HID / 16;
+    constexpr int Q4 = KIN / 4, RPP = THREADS / Q4, PASSES = MR / RPP;
+    // observation float4s per thread fetched ahead (more would spill)
+    constexpr int PRE = PASSES < 8 ? PASSES : 8;
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    const int G3 = (a.A + 7) >> 3;   // accumulator groups holding real actions
+
+    int t = t0, cur = 0;
+    int4 ti = a.tile_info[t];
+    int p = __builtin_amdgcn_readfirstlane(ti.x), nrows = __builtin_amdgcn_readfirstlane(ti.z);
+    {
+        const int r0 = __builtin_amdgcn_readfirstlane(ti.y);
+        if (tid < MR) {
+            row_slot[0][tid] = tid < nrows ? a.perm[r0 + tid] : -1;
+            row_env[0][tid] = tid < nrows ? a.perm_env[r0 + tid] : -1;
+        }
+        if (tid < a.A)
+            b3s[0][tid] = a.b3[p * a.A + tid];
+        __syncthreads();
+        const int oc = (tid % Q4) * 4, orow = tid / Q4;
+        const float* S0 = (const float*)a.state + oc;
+        v4f ob[PASSES];
+#pragma unroll
+        for (int u = 0; u < PASSES; ++u) {
+            const int env = row_env[0][orow + u * RPP];
+            ob[u] = v4f{0.f, 0.f, 0.f, 0.f};
+            if (env >= 0)
+                ob[u] = *reinterpret_cast<const v4f*>(S0 + (uint32_t)env * (uint32_t)KIN);
+        }
+#pragma unroll
+        for (int u = 0; u < PASSES; ++u)
+            *reinterpret_cast<uint2*>(buf + (orow + u * RPP) * kLdw + oc) =
+                make_uint2(pack_bf16x2(ob[u].x, ob[u].y), pack_bf16x2(ob[u].z, ob[u].w));
+    }
+    WRing<NT, S::DEPTH> ring;
+    ring_fill(ring, frag_src(a.w1 + (int64_t)p * F1 * 64, F1), KIN / 16, nt0, tid & 63);
+    __syncthreads();
+
+    for (;;) {
+        // per-lane values are recomputed every tile from an opaque copy of
+        // the thread index: hoisted out of the loop they would stay live
+        // across the MFMA layers and push the allocator into spills
+        int tq = tid;
+        asm volatile("" : "+v"(tq));
+        const int ln = tq & 63;
+        f32x16 acc[NT][RT];
+        // ---- layer 1 (first fragments already in the ring)
+        mfma_layer_1b<NT, RT, S::DEPTH>(ring, frag_src(a.w1 + (int64_t)p * F1 * 64, F1),
+                                        KIN / 16, nt0, rt0, buf, ln, a.b1 + p * HID, acc);
+        const Frags W2 = frag_src(a.w2 + (int64_t)p * F2 * 64, F2);
+        ring_fill(ring, W2, HID / 16, nt0, ln);
+        __syncthreads();
+        hidden_epilogue<NT, RT>(acc, nt0, rt0, buf, ln);
+        // next tile: table entry, row indices and output bias (into registers)
+        const bool has_next = t + 1 < t1;
+        int4 tin = make_int4(0, 0, 0, 0);
+        if (has_next)
+            tin = a.tile_info[t + 1];
+        const int pn = __builtin_amdgcn_readfirstlane(tin.x);
+        const int nn = __builtin_amdgcn_readfirstlane(tin.z);
+        const int rn = __builtin_amdgcn_readfirstlane(tin.y);
+        int slot_n = -1, env_n = -1;
+        float b3_n = 0.0f;
+        if (has_next) {
+            if (tq < nn) {
+                slot_n = a.perm[rn + tq];
+                env_n = a.perm_env[rn + tq];
+            }
+            if (tq < a.A)
+                b3_n = a.b3[pn * a.A + tq];
+        }
+        __syncthreads();
+        // ---- layer 2
+        mfma_layer_1b<NT, RT, S::DEPTH>(ring, W2, HID / 16, nt0, rt0, buf, ln, a.b2 + p * HID,
+                                        acc);
+        // output-layer fragments of this wave's hidden units (k-steps 2n, 2n+1)
+        uint4 w3[NT][2];
+        {
+            const Frags W3 = frag_src(a.w3k + (int64_t)p * F3 * 64, F3);
+#pragma unroll
+            for (int n = 0; n < NT; ++n)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    w3[n][j] = load_frag(W3, (nt0 + n) * 2 + j, ln * 16u);
+        }
+        if (tq < MR) {
+            row_slot[cur ^ 1][tq] = slot_n;
+            row_env[cur ^ 1][tq] = env_n;
+        }
+        if (tq < kMaxActions)
+            b3s[cur ^ 1][tq] = b3_n;
+
+        // ---- layer 3 from the accumulators: partial logits over this wave's units
+        f32x16 o[RT];
+#pragma unroll
+        for (int rr = 0; rr < RT; ++rr) {
+            o[rr] = f32x16{};
+#pragma unroll
+            for (int n = 0; n < NT; ++n)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    const f32x16& c = acc[n][rr];
+                    const int g0 = 8 * j, g1 = 8 * j + 4;
+                    uint4 bq;
+                    bq.x = relu_pack(c[g0 + 0], c[g0 + 1]);
+                    bq.y = relu_pack(c[g0 + 2], c[g0 + 3]);
+                    bq.z = relu_pack(c[g1 + 0], c[g1 + 1]);
+                    bq.w = relu_pack(c[g1 + 2], c[g1 + 3]);
+                    o[rr] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        __builtin_bit_cast(bf16x8, w3[n][j]), __builtin_bit_cast(bf16x8, bq),
+                        o[rr], 0, 0, 0);
+                }
+        }
+        __syncthreads();   // every wave is done reading the hidden rows
+#pragma unroll
+        for (int rr = 0; rr < RT; ++rr)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                if (g < G3)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        red[((ng * RTILES + rt0 + rr) * 16 + g * 4 + q) * 64 + ln] =
+                            o[rr][g * 4 + q];
+        __builtin_amdgcn_sched_barrier(0);
+        // next tile: first layer-1 fragments, observation rows -> registers
+        // (issued now, consumed after the partial sums: nothing in between
+        // waits on the vector memory counter)
+        const int oc = (tq % Q4) * 4, orow = tq / Q4;
+        v4f ob[PRE];
+        const float* S0 = (const float*)a.state + oc;
+        if (has_next) {
+            ring_fill(ring, frag_src(a.w1 + (int64_t)pn * F1 * 64, F1), KIN / 16, nt0, ln);
+#pragma unroll
+            for (int u = 0; u < PRE; ++u) {
+                const int env = row_env[cur ^ 1][orow + u * RPP];
+                ob[u] = v4f{0.f, 0.f, 0.f, 0.f};
+                if (env >= 0)
+                    ob[u] = *reinterpret_cast<const v4f*>(S0 + (uint32_t)env * (uint32_t)KIN);
+            }
+        }
+        __syncthreads();
+        // logits: partials summed in wave order, then the bias; thread
+        // (row, u0) writes actions u0, u0+4, ...
+        {
+            const int row = tq >> 2;
+            if (row < nrows) {
+                const int slot = row_slot[cur][row];
+                float* out = a.logits + (int64_t)slot * a.A;
+                for (int u = tq & 3; u < a.A; u += 4) {
+                    const int lr = (row & 31) + 32 * ((u >> 2) & 1);
+                    const int reg = (u >> 3) * 4 + (u & 3);
+                    float v = 0.0f;
+#pragma unroll
+                    for (int gq = 0; gq < NG; ++gq)
+                        v += red[((gq * RTILES + (row >> 5)) * 16 + reg) * 64 + lr];
+                    out[u] = v + b3s[cur][u];
+                }
+            }
+        }
+        if (!has_next)
+            break;
+        __syncthreads();   // partials consumed: the row buffer takes the next observations
+#pragma unroll
+        for (int u = 0; u < PRE; ++u)
+            *reinterpret_cast<uint2*>(buf + (orow + u * RPP) * kLdw + oc) =
+                make_uint2(pack_bf16x2(ob[u].x, ob[u].y), pack_bf16x2(ob[u].z, ob[u].w));
+        // the remaining rows
+#pragma unroll
+        for (int u0 = PRE; u0 < PASSES; u0 += PRE) {
+            v4f o2[PRE];
+#pragma unroll
+            for (int u = 0; u < PRE; ++u) {
+                const int env = row_env[cur ^ 1][orow + (u0 + u) * RPP];
+                o2[u] = v4f{0.f, 0.f, 0.f, 0.f};
+                if (env >= 0)
+                    o2[u] = *reinterpret_cast<const v4f*>(S0 + (uint32_t)env * (uint32_t)KIN);
+            }
+#pragma unroll
+            for (int u = 0; u < PRE; ++u)
+                *reinterpret_cast<uint2*>(buf + (orow + (u0 + u) * RPP) * kLdw + oc) =
+                    make_uint2(pack_bf16x2(o2[u].x, o2[u].y), pack_bf16x2(o2[u].z, o2[u].w));
+        }
+        ++t;
+        p = pn;
+        nrows = nn;
+        cur ^= 1;
+        __syncthreads();
+    }
+}
+
+template <int HID>
+static hipError_t launch_persist_hid(const MlpBf16Args& a, int kin, int blocks, hipStream_t s)
+{
+    if (kin != 512)
+        return hipErrorInvalidValue;
+    mlp_bf16_persist_kernel<HID, 512><<<blocks, 512, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_mlp_bf16_persist(const Pop& pop, const int32_t* perm, const int32_t* perm_env,
+                                   const int4* tile_info, const int32_t* tile_off,
+                                   int64_t n_slots, int n_agents, const void* state,
+                                   float* logits, hipStream_t s)
+{
+    if (pop.A > kMaxActions || !pop.w3k)
+        return hipErrorInvalidValue;
+    MlpBf16Args a = {};
+    a.w1 = (const uint4*)pop.w[0];
+    a.w2 = (const uint4*)pop.w[1];
+    a.w3 = (const uint4*)pop.w[2];
+    a.w3k = (const uint4*)pop.w3k;
+    a.b1 = pop.b[0];
+    a.b2 = pop.b[1];
+    a.b3 = pop.b[2];
+    a.perm = perm;
+    a.perm_env = perm_env;
+    a.tile_info = tile_info;
+    a.tile_off = tile_off;
+    a.state = state;
+    a.logits = logits;
+    a.P = pop.P;
+    a.A = pop.A;
+    a.in_dim = pop.in_dim;
+    a.n_agents = n_agents;
+    // one workgroup per CU (fewer for small batches: tiles are spread evenly
+    // over the workgroups, a multiple of the 8 XCDs)
+    const int64_t tiles = (n_slots + kPersistRows - 1) / kPersistRows + pop.P;
+    int blocks = (int)std::min<int64_t>(tiles, pop.n_cus);
+    blocks = std::max(8, (blocks + 7) / 8 * 8);
+    switch (pop.hid) {
+    case 64: return launch_persist_hid<64>(a, pop.in_pad, blocks, s);
+    case 128: return launch_persist_hid<128>(a, pop.in_pad, blocks, s);
+    case 256: return launch_persist_hid<256>(a, pop.in_pad, blocks, s);
+    case 512: return launch_persist_hid<512>(a, pop.in_pad, blocks, s);
+    default: return hipErrorInvalidValue;
     }
 }
 
@@ -581,8 +962,6 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
                            const int4* tile_info, int64_t n_slots, const void* state,
                            float* logits, hipStream_t s)
 {
-    if (tile_rows != kBf16TileRows)
-        return hipErrorInvalidValue;
     MlpBf16Args a;
     a.w1 = (const uint4*)pop.w[0];
     a.w2 = (const uint4*)pop.w[1];
@@ -602,6 +981,8 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
     a.grid = grid;
     a.d = d;
     a.n_envs = n_slots / n_agents;
+    if (tile_rows != kBf16TileRows)
+        return hipErrorInvalidValue;
     const int max_tiles = max_tiles_for(n_slots, pop.P, tile_rows);
     int blocks = (max_tiles + 7) / 8 * 8;
     a.n_blocks = blocks;

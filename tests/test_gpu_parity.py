@@ -187,6 +187,55 @@ def test_parity_feature_shared_init_d64():
     assert np.all(g["states"][0] == g["states"][0][0])
 
 
+# Larger buckets: several full tiles per policy plus ragged tails.  With d=512
+# observations and >= 256 slots per policy the persistent 128-row kernel runs
+# (output layer fed from the accumulators, next tile prefetched); below that,
+# and for narrower observations, the 64-row kernel.
+
+def test_parity_team_large_buckets():
+    """4v4 team game, 4 policies, 150 envs x 8 seats = 1200 slots (uneven
+    Dirichlet buckets)."""
+    wl = W.make(5, P=4, n_envs=150, horizon=4)
+    g = run_gpu(wl, snaps=[0, 3])
+    check_parity(wl, g)
+
+
+def test_parity_feature_d512_large_buckets():
+    """d=512, 2 policies x 70 envs per pair = 560 slots (persistent kernel)."""
+    wl = W.make(4, P=2, per_pair=70, horizon=4)
+    g = run_gpu(wl, snaps=[0, 3])
+    check_parity(wl, g)
+
+
+@pytest.mark.parametrize("hid", [64, 128, 256, 512])
+def test_parity_persistent_hidden_widths(hid):
+    """d=512 2v2 game, 2 policies x 320 slots: every wave split of the
+    persistent kernel."""
+    wl = W.team_variant(4, d=512, P=2, n_envs=160, horizon=3, dims=[512, hid, hid, 18])
+    g = run_gpu(wl, snaps=[0, 2])
+    check_parity(wl, g)
+
+
+@pytest.mark.parametrize("hid", [64, 128, 256])
+def test_parity_team_2v2_large_buckets_hidden_widths(hid):
+    wl = W.team_variant(4, P=2, n_envs=200, horizon=3, dims=[256, hid, hid, 18])
+    g = run_gpu(wl, snaps=[0, 2])
+    check_parity(wl, g)
+
+
+@pytest.mark.parametrize("d", [256, 512])
+def test_parity_many_tiles_sampled(d):
+    """80000 slots (more tiles than workgroups: 64-row tiles for d=256, several
+    128-row tiles per persistent workgroup for d=512); the oracle replays a
+    sample of envs including both ends of the batch."""
+    wl = W.team_variant(4, d=d, P=2, n_envs=20000, horizon=3, dims=[d, 64, 64, 18])
+    g = run_gpu(wl, snaps=[0, 2])
+    rng = np.random.default_rng(7)
+    sel = np.sort(np.concatenate([[0, 1, wl.n_envs - 1],
+                                  rng.choice(np.arange(2, wl.n_envs - 1), 197, replace=False)]))
+    check_parity(wl, g, sel)
+
+
 # ------------------------------------------------------------ invariants
 
 def test_determinism_and_shard_merge():

@@ -255,6 +255,26 @@ def test_mlp_f32_matches_torch():
         assert np.allclose(got, ref, rtol=1e-6, atol=1e-6)
 
 
+def test_bf16_relu_is_relu_of_the_rounded_value():
+    """ReLU of a hidden unit: bf16(max(x, 0)) (torch) for every non-NaN x,
+    including -0 (-> +0), tiny negatives, values that round up to a power of
+    two and infinities; a NaN keeps its sign rule (negative NaN -> +0,
+    positive NaN stays NaN)."""
+    xs = [0.0, -0.0, 1e-40, -1e-40, 1.0, -1.0, 3.0e38, -3.0e38, np.inf, -np.inf,
+          1.00390625, 1.0039062500001, -2.9e-39, 65504.0, -7.5]
+    rng = np.random.default_rng(3)
+    xs += list(rng.standard_normal(2000).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 2000))
+    t = torch.tensor(np.array(xs, np.float32))
+    ref = torch.relu(t).to(torch.bfloat16).float().numpy()
+    ref = np.where(ref == 0, np.float32(0), ref)     # max(-0, 0) is taken as +0
+    got = np.array([oracle.bf16_relu(x) for x in xs], np.float32)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    pos_nan = np.frombuffer(np.uint32(0x7FC01234).tobytes(), np.float32)[0]
+    neg_nan = np.frombuffer(np.uint32(0xFFC01234).tobytes(), np.float32)[0]
+    assert np.isnan(oracle.bf16_relu(pos_nan))
+    assert np.float32(oracle.bf16_relu(neg_nan)).view(np.uint32) == 0
+
+
 def test_mlp_bf16_matches_torch_emulation():
     """bf16 policy: bf16 input and hidden activations, exact products, fp32
     accumulator; emulated with torch's bf16 conversion and fp64 linear."""
