@@ -220,11 +220,8 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
                 int op = round_up(fo, 32);
                 size_t wb = (size_t)P * (op / 32) * (ip / 16) * 64 * 16;
                 TRY(hipMalloc(&p->w[l], wb));
-                TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, 0, p->w[l], s));
-                if (l == 2) {
-                    TRY(hipMalloc(&p->w3k, wb));
-                    TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, 1, p->w3k, s));
-                }
+                // the output layer in the k order of the layer-2 accumulators
+                TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, l == 2, p->w[l], s));
             }
         }
     }
@@ -250,8 +247,6 @@ void malib_pop_destroy(malib_pop_t p)
     if (!p)
         return;
     (void)hipDeviceSynchronize();
-    if (p->w3k)
-        (void)hipFree(p->w3k);
     for (int l = 0; l < 3; ++l) {
         if (p->w[l])
             (void)hipFree(p->w[l]);

@@ -47,8 +47,9 @@ struct Pop {
     int device = 0;
     int n_cus = 0;                // compute units of the device
     // packed weights
-    void* w[3] = {nullptr, nullptr, nullptr};   // bf16 fragment layout or fp32 [P][out][in]
-    void* w3k = nullptr;          // bf16 output layer in the accumulator k order
+    // bf16: fragment layout (the output layer's k order follows the layer-2
+    // accumulators, see pack_bf16_kernel); fp32: [P][out][in]
+    void* w[3] = {nullptr, nullptr, nullptr};
     float* b[3] = {nullptr, nullptr, nullptr};  // fp32 [P][out] (zero-filled when absent)
     float* tab = nullptr;                       // fp32 [P][A]
     // payoff accumulators: [P*P] each

@@ -239,9 +239,7 @@ struct MlpBf16Args {
     int64_t n_envs;
     int n_blocks;                   // launched workgroups (a multiple of 8)
     int max_tiles;                  // entries of tile_info
-    // persistent kernel
-    const uint4* w3k;               // output layer packed with the accumulator k order
-    const int32_t* tile_off;        // tile_off[P] = number of tiles
+    const int32_t* tile_off;        // persistent kernel: tile_off[P] = number of tiles
 };
 
 // Weight fragments of one layer of one policy, read through a buffer resource:
@@ -407,48 +405,6 @@ __device__ __forceinline__ void mfma_layer_1b(WRing<NT, DEPTH>& ring, Frags frag
     }
 }
 
-// Output layer (one 32-wide n-tile): wave w takes row-tile w%2 and half h =
-// w/2 of the k-steps.  Its weight fragments are loaded into registers before
-// the preceding epilogue (out_fill), the MFMAs alternate between two
-// accumulators, and the k-halves are summed through LDS by the caller.
-template <int KH>
-struct OutFrags {
-    uint4 a[KH];
-};
-
-template <int KH>
-__device__ __forceinline__ void out_fill(OutFrags<KH>& f, Frags frag, int h,
-                                         int lane)
-{
-#pragma unroll
-    for (int k = 0; k < KH; ++k)
-        f.a[k] = load_frag(frag, h * KH + k, lane * 16u);
-}
-
-template <int KH>
-__device__ __forceinline__ f32x16 mfma_out_half(const OutFrags<KH>& f, int h, int rt,
-                                                const uint16_t* buf, int lane)
-{
-    f32x16 acc0 = f32x16{}, acc1 = f32x16{};
-    const uint16_t* bp = buf + (rt * 32 + (lane & 31)) * kLdw + (lane >> 5) * 8 + h * KH * 16;
-    uint4 b[2];
-    b[0] = *reinterpret_cast<const uint4*>(bp);
-#pragma unroll
-    for (int k = 0; k < KH; ++k) {
-        if (k + 1 < KH)
-            b[(k + 1) & 1] = *reinterpret_cast<const uint4*>(bp + (k + 1) * 16);
-        if (k & 1)
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.a[k]),
-                                                           __builtin_bit_cast(bf16x8, b[k & 1]),
-                                                           acc1, 0, 0, 0);
-        else
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, f.a[k]),
-                                                           __builtin_bit_cast(bf16x8, b[k & 1]),
-                                                           acc0, 0, 0, 0);
-    }
-    return acc0 + acc1;
-}
-
 // Hidden-unit ReLU on two accumulators: round both to bf16 (one
 // v_cvt_pk_bf16_f32), then clear every half whose sign bit is set with one
 // signed 16-bit max against 0.  For non-NaN inputs this is bf16(max(x, 0));
@@ -479,6 +435,87 @@ __device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], int
                 *reinterpret_cast<uint2*>(buf + row * kLdw + u0) = pk;
             }
         }
+    }
+}
+
+// ---- output layer fed from the layer-2 accumulators
+//
+// A wave holding layer-2 accumulators acc[n][r] (units (nt0+n)*32.., rows of
+// row tile rt0+r) converts them with ReLU to bf16 B operands in place: k-step
+// j of n-tile nt0+n takes registers 8j..8j+7 (see pack_bf16_kernel's kperm
+// layout, in which the output weights are packed), so the output layer
+// needs no trip of the second hidden layer through LDS.  Each wave produces
+// partial logits over its own units; the partials of the NG waves sharing a
+// row tile are summed in wave order by out_reduce.
+
+template <int NT>
+__device__ __forceinline__ void load_w3(uint4 (&w3)[NT][2], Frags W3, int nt0, int lane)
+{
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            w3[n][j] = load_frag(W3, (nt0 + n) * 2 + j, lane * 16u);
+}
+
+template <int NT, int RT>
+__device__ __forceinline__ void out_from_acc(const f32x16 (&acc)[NT][RT],
+                                             const uint4 (&w3)[NT][2], f32x16 (&o)[RT])
+{
+#pragma unroll
+    for (int rr = 0; rr < RT; ++rr) {
+        o[rr] = f32x16{};
+#pragma unroll
+        for (int n = 0; n < NT; ++n)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const f32x16& c = acc[n][rr];
+                const int g0 = 8 * j, g1 = 8 * j + 4;
+                uint4 bq;
+                bq.x = relu_pack(c[g0 + 0], c[g0 + 1]);
+                bq.y = relu_pack(c[g0 + 2], c[g0 + 3]);
+                bq.z = relu_pack(c[g1 + 0], c[g1 + 1]);
+                bq.w = relu_pack(c[g1 + 2], c[g1 + 3]);
+                o[rr] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, w3[n][j]), __builtin_bit_cast(bf16x8, bq), o[rr],
+                    0, 0, 0);
+            }
+    }
+}
+
+// Partials of wave group ng for row tiles rt0.. into red[NG][RTILES][16][64]
+// (registers of output groups g < G3 only: the real actions).
+template <int RT, int RTILES>
+__device__ __forceinline__ void out_partials(float* red, const f32x16 (&o)[RT], int ng, int rt0,
+                                             int G3, int lane)
+{
+#pragma unroll
+    for (int rr = 0; rr < RT; ++rr)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            if (g < G3)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    red[((ng * RTILES + rt0 + rr) * 16 + g * 4 + q) * 64 + lane] = o[rr][g * 4 + q];
+}
+
+// Logit (row, u) = sum over wave groups (in order) + bias; thread (row, u0)
+// writes u0, u0+4, ... of its row.
+template <int NG, int RTILES>
+__device__ __forceinline__ void out_reduce(const float* red, int row, int slot, int u0, int A,
+                                           const float* b3, float* __restrict__ logits)
+{
+    if (slot < 0)
+        return;
+    float* out = logits + (int64_t)slot * A;
+    for (int u = u0; u < A; u += 4) {
+        const int lr = (row & 31) + 32 * ((u >> 2) & 1);
+        const int reg = (u >> 3) * 4 + (u & 3);
+        float v = 0.0f;
+#pragma unroll
+        for (int gq = 0; gq < NG; ++gq)
+            v += red[((gq * RTILES + (row >> 5)) * 16 + reg) * 64 + lr];
+        out[u] = v + b3[u];
     }
 }
 
@@ -564,6 +601,8 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
 }
 
 // MR rows per tile (the library uses 64: four wavefronts, two workgroups per CU).
+// Layers 1 and 2 run from LDS rows; the output layer is fed from the layer-2
+// accumulators (out_from_acc), its partials summed through the row buffer.
 template <int HID, int OBS, int KIN, int MR>
 __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpBf16Args a)
 {
@@ -571,7 +610,8 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
     __shared__ __attribute__((aligned(16))) uint16_t buf[MR * kLdw];
     __shared__ int row_slot[MR];
     __shared__ int row_env[MR];
-    __shared__ float red[RTILES * 16 * 64];   // output-layer partial sums of the second k-half
+    static_assert(HidSplit<HID, WAVES, RTILES>::NGROUPS * RTILES * 16 * 64 * 4 <= MR * kLdw * 2,
+                  "output partials fit in the row buffer");
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -617,40 +657,19 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
     // ---- layer 2: HID -> HID
     mfma_layer<S::NT, S::RT, S::DEPTH>(ring, W2, HID / 16, nt0, rt0, buf, lane,
                                        a.b2 + p * HID, acc);
-    constexpr int KH = HID / 32;                    // k-steps per half of the output layer
-    const int h = wave / RTILES, rt = wave % RTILES;
-    OutFrags<KH> of;
-    out_fill<KH>(of, frag_src(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16), h,
-                 lane);                                          // overlaps the epilogue
+    // ---- layer 3 from the accumulators, partial logits summed through LDS
+    uint4 w3[S::NT][2];
+    load_w3<S::NT>(w3, frag_src(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16), nt0, lane);
+    f32x16 o[S::RT];
+    out_from_acc<S::NT, S::RT>(acc, w3, o);
+    __syncthreads();   // every wave is done reading the hidden rows: buf takes the partials
+    float* red = reinterpret_cast<float*>(buf);
+    out_partials<S::RT, RTILES>(red, o, wave % S::NGROUPS, rt0, (a.A + 7) >> 3, lane);
     __syncthreads();
-    hidden_epilogue<S::NT, S::RT>(acc, nt0, rt0, buf, lane);
-    __syncthreads();
-    // ---- layer 3: HID -> A (one 32-wide output tile), k-halves summed in LDS
-    f32x16 o = mfma_out_half<KH>(of, h, rt, buf, lane);
-    if (h == 1) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-            red[(rt * 16 + j) * 64 + lane] = o[j];
-    }
-    __syncthreads();
-    if (h == 0) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-            o[j] += red[(rt * 16 + j) * 64 + lane];
-        const int row = rt * 32 + (lane & 31);
-        const int slot = row < nrows ? row_slot[row] : -1;
-        if (slot >= 0) {
-            float* out = a.logits + (int64_t)slot * a.A;
-            const float* b3 = a.b3 + p * a.A;
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int u = g * 8 + (lane >> 5) * 4 + q;
-                    if (u < a.A)
-                        out[u] = o[g * 4 + q] + b3[u];
-                }
-        }
+    {
+        const int row = tid >> 2;
+        out_reduce<S::NGROUPS, RTILES>(red, row, row < nrows ? row_slot[row] : -1, tid & 3, a.A,
+                                       a.b3 + p * a.A, a.logits);
     }
 }
 
@@ -664,7 +683,7 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
 //
 // Per tile: observations (bf16, LDS) -> layer 1 -> ReLU/bf16 into LDS ->
 // layer 2 -> output layer straight from the layer-2 accumulators (the output
-// weights are packed in their k order, see pack_bf16_kernel) -> per-wave
+// weights are packed in that k order, see pack_bf16_kernel) -> per-wave
 // partial logits summed through LDS in wave order.  The next tile's table
 // entry, row indices and output bias are fetched before layer 2, its first
 // weight fragments and observation rows while the partial logits are summed.
@@ -766,16 +785,8 @@ __global__ __launch_bounds__(512, 1) void mlp_bf16_persist_kernel(MlpBf16Args a)
         // ---- layer 2
         mfma_layer_1b<NT, RT, S::DEPTH>(ring, W2, HID / 16, nt0, rt0, buf, ln, a.b2 + p * HID,
                                         acc);
-        // output-layer fragments of this wave's hidden units (k-steps 2n, 2n+1)
         uint4 w3[NT][2];
-        {
-            const Frags W3 = frag_src(a.w3k + (int64_t)p * F3 * 64, F3);
-#pragma unroll
-            for (int n = 0; n < NT; ++n)
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    w3[n][j] = load_frag(W3, (nt0 + n) * 2 + j, ln * 16u);
-        }
+        load_w3<NT>(w3, frag_src(a.w3 + (int64_t)p * F3 * 64, F3), nt0, ln);
         if (tq < MR) {
             row_slot[cur ^ 1][tq] = slot_n;
             row_env[cur ^ 1][tq] = env_n;
@@ -785,35 +796,9 @@ __global__ __launch_bounds__(512, 1) void mlp_bf16_persist_kernel(MlpBf16Args a)
 
         // ---- layer 3 from the accumulators: partial logits over this wave's units
         f32x16 o[RT];
-#pragma unroll
-        for (int rr = 0; rr < RT; ++rr) {
-            o[rr] = f32x16{};
-#pragma unroll
-            for (int n = 0; n < NT; ++n)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) {
-                    const f32x16& c = acc[n][rr];
-                    const int g0 = 8 * j, g1 = 8 * j + 4;
-                    uint4 bq;
-                    bq.x = relu_pack(c[g0 + 0], c[g0 + 1]);
-                    bq.y = relu_pack(c[g0 + 2], c[g0 + 3]);
-                    bq.z = relu_pack(c[g1 + 0], c[g1 + 1]);
-                    bq.w = relu_pack(c[g1 + 2], c[g1 + 3]);
-                    o[rr] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, w3[n][j]), __builtin_bit_cast(bf16x8, bq),
-                        o[rr], 0, 0, 0);
-                }
-        }
+        out_from_acc<NT, RT>(acc, w3, o);
         __syncthreads();   // every wave is done reading the hidden rows
-#pragma unroll
-        for (int rr = 0; rr < RT; ++rr)
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-                if (g < G3)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        red[((ng * RTILES + rt0 + rr) * 16 + g * 4 + q) * 64 + ln] =
-                            o[rr][g * 4 + q];
+        out_partials<RT, RTILES>(red, o, ng, rt0, G3, ln);
         __builtin_amdgcn_sched_barrier(0);
         // next tile: first layer-1 fragments, observation rows -> registers
         // (issued now, consumed after the partial sums: nothing in between
@@ -832,24 +817,9 @@ __global__ __launch_bounds__(512, 1) void mlp_bf16_persist_kernel(MlpBf16Args a)
             }
         }
         __syncthreads();
-        // logits: partials summed in wave order, then the bias; thread
-        // (row, u0) writes actions u0, u0+4, ...
-        {
-            const int row = tq >> 2;
-            if (row < nrows) {
-                const int slot = row_slot[cur][row];
-                float* out = a.logits + (int64_t)slot * a.A;
-                for (int u = tq & 3; u < a.A; u += 4) {
-                    const int lr = (row & 31) + 32 * ((u >> 2) & 1);
-                    const int reg = (u >> 3) * 4 + (u & 3);
-                    float v = 0.0f;
-#pragma unroll
-                    for (int gq = 0; gq < NG; ++gq)
-                        v += red[((gq * RTILES + (row >> 5)) * 16 + reg) * 64 + lr];
-                    out[u] = v + b3s[cur][u];
-                }
-            }
-        }
+        // logits: partials summed in wave order, then the bias
+        out_reduce<NG, RTILES>(red, tq >> 2, row_slot[cur][tq >> 2], tq & 3, a.A, b3s[cur],
+                               a.logits);
         if (!has_next)
             break;
         __syncthreads();   // partials consumed: the row buffer takes the next observations
@@ -895,13 +865,12 @@ hipError_t launch_mlp_bf16_persist(const Pop& pop, const int32_t* perm, const in
                                    int64_t n_slots, int n_agents, const void* state,
                                    float* logits, hipStream_t s)
 {
-    if (pop.A > kMaxActions || !pop.w3k)
+    if (pop.A > kMaxActions)
         return hipErrorInvalidValue;
     MlpBf16Args a = {};
     a.w1 = (const uint4*)pop.w[0];
     a.w2 = (const uint4*)pop.w[1];
     a.w3 = (const uint4*)pop.w[2];
-    a.w3k = (const uint4*)pop.w3k;
     a.b1 = pop.b[0];
     a.b2 = pop.b[1];
     a.b3 = pop.b[2];
