@@ -328,6 +328,25 @@ def test_nan_logits_are_flagged():
     pop.close()
 
 
+@pytest.mark.parametrize("c,n_envs", [(3, 96), (5, 40), (4, 0)])
+def test_nan_logits_are_flagged_bf16(c, n_envs):
+    """A NaN output weight of policy 1 makes that policy's logits NaN; the
+    bf16 kernels (64-row, and the persistent one for the d=512 feature game)
+    raise the device flag while sampling."""
+    from paper_2106_07551_amd import workload_io as IO
+    import paper_2106_07551_amd as M
+    wl = W.make(c, P=2, per_pair=80, horizon=2) if c == 4 else W.make(c, P=2, n_envs=n_envs,
+                                                                      horizon=2)
+    wl.weights[2] = wl.weights[2].copy()
+    wl.weights[2][1, 0, 0] = np.nan
+    pop = IO.make_population(wl)
+    env = IO.make_env(wl)
+    pop.rollout(env, wl.n_envs, IO.make_pairs(wl), wl.seed, 2)
+    t = pop.payoff(check=False)
+    assert t["status"] == M.binding.E_DEVICE and t["device_flags"] & 2
+    pop.close()
+
+
 def test_host_validation_errors():
     import paper_2106_07551_amd as M
     from paper_2106_07551_amd import workload_io as IO
