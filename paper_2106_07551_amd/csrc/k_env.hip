@@ -173,24 +173,29 @@ __global__ __launch_bounds__(256) void step_pursuit_kernel(
 
 // ------------------------------------------------------------ feature dynamics
 
-// One workgroup of 256 threads owns 32 envs and all D outputs of each:
+// One workgroup of kFeatWaves wavefronts owns kFeatWaves*EPT envs and all D
+// outputs of each:
 //   s'[e][k] = tanh_ref( fma-chain_{c=0..D-1}(W[k][c], s[e][c]) + emb[0][a_0][k]
 //                        + emb[1][a_1][k] + ... )
-// Thread (tx = tid%64, ty = tid/64) keeps the accumulators of envs ty*8..ty*8+7
-// and outputs tx + 64j; the input index c runs in ascending order through
+// Thread (tx = tid%64, ty = tid/64) keeps the accumulators of envs
+// ty*EPT..ty*EPT+EPT-1 and outputs tx + 64j; the input index c runs in ascending order through
 // LDS-staged chunks of WT (c-major) and of the state (so every accumulator
 // sees exactly the sequential fused chain, no split of the sum).  The reward
 // r = u . s' is then a sequential fused chain per env over the staged s'.
 constexpr int kFeatKC = 32;
+// Eight wavefronts per workgroup: the WT chunks staged through LDS serve twice
+// as many envs as with four, and the grid has half as many workgroups to ramp
+// up and drain (d=256: 50 vs 54 us per step of 16384 envs; d=512: -3%).
+constexpr int kFeatWaves = 8, kFeatThreads = 64 * kFeatWaves;
 
-// EPT envs per thread: the workgroup owns 4*EPT envs.
+// EPT envs per thread.
 template <int D, int EPT>
-__global__ __launch_bounds__(256) void step_feature_kernel(
+__global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     const float* __restrict__ WT, const float* __restrict__ emb, const float* __restrict__ u,
     EnvArgs ea, int64_t n, const uint8_t* __restrict__ act, const float* __restrict__ s_in,
     float* __restrict__ s_out, float* __restrict__ ret)
 {
-    constexpr int kFeatEnvs = 4 * EPT;
+    constexpr int kFeatEnvs = kFeatWaves * EPT;
     constexpr int NJ = D / 64;
     constexpr int SSTR = kFeatEnvs + 4;
     constexpr int WS_FLOATS = kFeatKC * D > kFeatEnvs * (D + 1) ? kFeatKC * D : kFeatEnvs * (D + 1);
@@ -222,7 +227,7 @@ __global__ __launch_bounds__(256) void step_feature_kernel(
     // Staging: chunk c0 of WT (KC x D floats, c-major) and of the state (32 envs
     // x KC) goes global -> registers -> LDS; the loads of chunk c0+KC are issued
     // before the FMAs of chunk c0 so their latency overlaps the arithmetic.
-    constexpr int WQ = kFeatKC * D / 4 / 256;     // float4 of WT per thread per chunk
+    constexpr int WQ = kFeatKC * D / 4 / kFeatThreads;   // float4 of WT per thread per chunk
     // state chunk: kFeatEnvs envs x KC columns = kFeatEnvs*8 float4; threads
     // beyond that re-load env 0's chunk and skip the LDS store
     const int el_ld = (tid >> 3) % kFeatEnvs, cq_ld = tid & 7;
@@ -235,13 +240,13 @@ __global__ __launch_bounds__(256) void step_feature_kernel(
     v4f sreg;
 #pragma unroll
     for (int q = 0; q < WQ; ++q)
-        wreg[q] = wsrc[q * 256];
+        wreg[q] = wsrc[q * kFeatThreads];
     sreg = *reinterpret_cast<const v4f*>(ssrc);
     for (int c0 = 0; c0 < D; c0 += kFeatKC) {
         v4f* dst = reinterpret_cast<v4f*>(Ws);
 #pragma unroll
         for (int q = 0; q < WQ; ++q)
-            dst[q * 256 + tid] = wreg[q];
+            dst[q * kFeatThreads + tid] = wreg[q];
         if (e_ld >= n)
             sreg = v4f{0.f, 0.f, 0.f, 0.f};
         if (s_owner) {
@@ -257,7 +262,7 @@ __global__ __launch_bounds__(256) void step_feature_kernel(
             const v4f* wn = wsrc + cn * (D / 4);
 #pragma unroll
             for (int q = 0; q < WQ; ++q)
-                wreg[q] = wn[q * 256];
+                wreg[q] = wn[q * kFeatThreads];
             sreg = *reinterpret_cast<const v4f*>(ssrc + cn);
         }
 #pragma unroll
@@ -359,17 +364,17 @@ hipError_t launch_env_step(const EnvArgs& e, int64_t n_envs, const uint8_t* acti
     case MALIB_ENV_FEATURE: {
         const float* si = (const float*)state_in;
         float* so = (float*)state_out;
-        // 8 envs per thread (32-env workgroups) for d = 512; 4 (16-env) below,
-        // which doubles the resident wavefronts for the smaller state
-        const int fb8 = (int)((n_envs + 31) / 32), fb4 = (int)((n_envs + 15) / 16);
+        // 8 envs per thread for d = 512 (64-env workgroups), 4 below (32 envs)
+        const int fb8 = (int)((n_envs + 8 * kFeatWaves - 1) / (8 * kFeatWaves));
+        const int fb4 = (int)((n_envs + 4 * kFeatWaves - 1) / (4 * kFeatWaves));
         if (e.d == 64)
-            step_feature_kernel<64, 4><<<fb4, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<64, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else if (e.d == 128)
-            step_feature_kernel<128, 4><<<fb4, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<128, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else if (e.d == 256)
-            step_feature_kernel<256, 4><<<fb4, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<256, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else if (e.d == 512)
-            step_feature_kernel<512, 8><<<fb8, 256, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<512, 8><<<fb8, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
         else
             return hipErrorInvalidValue;
         break;
