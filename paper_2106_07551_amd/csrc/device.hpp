@@ -21,13 +21,27 @@ struct u64x4 {
 // 64x64->128-bit products with the round constants, the high halves xor-ed
 // with the other counter words and the key; the key advances by the Weyl
 // increments between rounds.
+// 64x64 -> 128-bit product from four 32x32 -> 64 multiply-adds: the partial
+// products are chained so that no sum can overflow 64 bits.
+__device__ __forceinline__ void mul_hilo64(uint64_t a, uint64_t b, uint64_t& lo, uint64_t& hi)
+{
+    const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32);
+    const uint32_t b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+    const uint64_t p00 = (uint64_t)a0 * b0;
+    const uint64_t t = (uint64_t)a0 * b1 + (p00 >> 32);
+    const uint64_t u = (uint64_t)a1 * b0 + (uint32_t)t;
+    lo = (u << 32) | (uint32_t)p00;
+    hi = (uint64_t)a1 * b1 + ((t >> 32) + (u >> 32));
+}
+
 __device__ __forceinline__ u64x4 philox4x64_10(u64x4 c, uint64_t k0, uint64_t k1)
 {
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
         const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
-        uint64_t lo0 = m0 * c.x, hi0 = __umul64hi(m0, c.x);
-        uint64_t lo1 = m1 * c.z, hi1 = __umul64hi(m1, c.z);
+        uint64_t lo0, hi0, lo1, hi1;
+        mul_hilo64(m0, c.x, lo0, hi0);
+        mul_hilo64(m1, c.z, lo1, hi1);
         u64x4 n;
         n.x = hi1 ^ c.y ^ k0;
         n.y = lo1;

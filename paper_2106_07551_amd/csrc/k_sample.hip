@@ -43,14 +43,27 @@ hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
     return hipGetLastError();
 }
 
+// Gumbel noise -ln(-ln u) for u in [2^-24, 1 - 2^-24] (uniform01's range):
+// both logarithms see normal fp32 inputs, so each is the hardware log2
+// (v_log_f32, 1 ulp) times ln 2, without the denormal scaling of logf.
+__device__ __forceinline__ float gumbel01(float u)
+{
+    const float ln2 = 0x1.62e430p-1f;
+    const float e = -(__builtin_amdgcn_logf(u) * ln2);
+    return -(__builtin_amdgcn_logf(e) * ln2);
+}
+
 // One thread per slot (env * n_agents + seat).  z_a = l_a + g_a with
-// g_a = -log(-log u_a) in fp32, u_a from lane a%8 of block a/8 of (g, t,
+// g_a = -log(-log u_a) in fp32 (gumbel01), u_a from lane a%8 of block a/8 of (g, t,
 // kPurposeAction<<32 | seat); the first index of the maximum wins.  Finished
-// envs (done != 0) take no action (255).
-__global__ void gumbel_kernel(const float* __restrict__ logits, int64_t n_envs, int n_agents,
-                              int A, uint64_t seed, int64_t env_offset, int t,
-                              const uint8_t* __restrict__ done, uint8_t* __restrict__ actions,
-                              uint8_t* __restrict__ log, int* flags)
+// envs (done != 0) take no action (255).  AMAX >= A (a multiple of 8): the
+// slot's logits are all loaded and its Philox blocks all drawn before the
+// arithmetic, so their latencies overlap instead of one load per action.
+template <int AMAX>
+__global__ __launch_bounds__(256) void gumbel_kernel(
+    const float* __restrict__ logits, int64_t n_envs, int n_agents, int A, uint64_t seed,
+    int64_t env_offset, int t, const uint8_t* __restrict__ done, uint8_t* __restrict__ actions,
+    uint8_t* __restrict__ log, int* flags)
 {
     int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (slot >= n_envs * n_agents)
@@ -60,21 +73,28 @@ __global__ void gumbel_kernel(const float* __restrict__ logits, int64_t n_envs, 
     uint8_t best = 255;
     if (!(done && done[e])) {
         const float* l = logits + slot * A;
+        float lv[AMAX];
+#pragma unroll
+        for (int a = 0; a < AMAX; ++a)
+            lv[a] = a < A ? l[a] : 0.0f;
+        u64x4 blk[AMAX / 8];
+#pragma unroll
+        for (int b = 0; b < AMAX / 8; ++b)
+            if (b * 8 < A)
+                blk[b] = stream_block(seed, (uint64_t)(env_offset + e), (uint64_t)t,
+                                      kPurposeAction, seat, (uint64_t)b);
         float zbest = 0.0f;
         bool nan = false;
-        u64x4 blk{0, 0, 0, 0};
-        for (int a = 0; a < A; ++a) {
-            if ((a & 7) == 0)
-                blk = stream_block(seed, (uint64_t)(env_offset + e), (uint64_t)t,
-                                   kPurposeAction, seat, (uint64_t)(a >> 3));
-            float u = uniform01(block_lane(blk, a & 7));
-            float g = -logf(-logf(u));
-            float la = l[a];
-            nan |= __builtin_isnan(la);
-            float z = la + g;
-            if (a == 0 || z > zbest) {
-                zbest = z;
-                best = (uint8_t)a;
+#pragma unroll
+        for (int a = 0; a < AMAX; ++a) {
+            if (a < A) {
+                float g = gumbel01(uniform01(block_lane(blk[a >> 3], a & 7)));
+                nan |= __builtin_isnan(lv[a]);
+                float z = lv[a] + g;
+                if (a == 0 || z > zbest) {
+                    zbest = z;
+                    best = (uint8_t)a;
+                }
             }
         }
         if (nan) {
@@ -93,8 +113,20 @@ hipError_t launch_gumbel(const float* logits, int64_t n_envs, int n_agents, int 
 {
     int64_t total = n_envs * n_agents;
     int blocks = (int)((total + 255) / 256);
-    gumbel_kernel<<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset, t,
-                                         done, actions, log, flags);
+    if (A <= 8)
+        gumbel_kernel<8><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset, t,
+                                                done, actions, log, flags);
+    else if (A <= 16)
+        gumbel_kernel<16><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset,
+                                                 t, done, actions, log, flags);
+    else if (A <= 24)
+        gumbel_kernel<24><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset,
+                                                 t, done, actions, log, flags);
+    else if (A <= 32)
+        gumbel_kernel<32><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset,
+                                                 t, done, actions, log, flags);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
