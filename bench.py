@@ -53,6 +53,42 @@ def describe(wl):
     return d
 
 
+PEAK_F32_ALU_TFLOPS = 78.6   # fp32 FMA without packed fp32 (256 CU x 4 SIMD x 16 lanes x 2 x 2.4 GHz)
+
+
+def algorithmic_work(wl):
+    """Per-launch algorithmic HBM bytes (and flops where the kernel is ALU- or
+    MFMA-bound) of the per-step kernels: unique data each launch must read or
+    write, counted once."""
+    import workloads as W
+    n, na, A = wl.n_envs, wl.n_agents, wl.n_actions
+    ns = n * na
+    out = {}
+    # sampling: logits in, action byte out
+    out["sample"] = {"bytes": ns * (4 * A + 1)}
+    if wl.env_kind == W.FEATURE:
+        d = wl.d
+        # state in and out, joint actions, returns read-modify-write, W and the
+        # embedding table once
+        b = n * (8 * d + na + 8 * na) + 4 * d * d + 4 * na * A * d + 4 * d
+        out["env"] = {"bytes": b, "flops": 2 * d * d * n}
+    elif wl.env_kind == W.PURSUIT:
+        out["env"] = {"bytes": n * (2 * 2 + 2 + 1 + 8 * na)}
+    elif wl.env_kind == W.ITER_MATRIX:
+        out["env"] = {"bytes": n * (2 * 2 + na + 8 * na)}
+    else:
+        out["env"] = {"bytes": n * (na + 8 * na)}
+    if wl.dims:
+        wbytes = (2 if wl.pol_kind == W.MLP_BF16 else 4) * wl.P * sum(
+            wl.dims[i] * wl.dims[i + 1] for i in range(len(wl.dims) - 1))
+        obs = n * wl.d * 4 if wl.env_kind == W.FEATURE else 0
+        out["policy"] = {"bytes": wbytes + obs + ns * 4 * A,
+                         "flops": policy_flops_per_frame(wl.dims) * ns}
+    else:
+        out["policy"] = {"bytes": wl.P * A * 4 + ns * 4 * A}
+    return out
+
+
 def policy_kernel(wl):
     """Which bf16 policy kernel the library runs for this workload: the
     persistent 128-row kernel for d=512 feature observations with >= 256 slots
@@ -173,8 +209,11 @@ def main():
     frames = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    step_s = []
     for _ in range(args.steps):
-        tab = one_step()
+        ts = time.perf_counter()
+        tab = one_step()          # ends with the table on the host (synchronizes)
+        step_s.append(time.perf_counter() - ts)
         frames += tab["live_frames"]
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
@@ -185,11 +224,21 @@ def main():
     # per-kernel breakdown from one more (untimed) fill with every launch timed
     pop.profile_enable(True)
     one_step()
+    work = algorithmic_work(wl)
     for name, k in (("policy", M.K_POLICY), ("sample", M.K_SAMPLE), ("env", M.K_ENV),
                     ("setup", M.K_SETUP), ("payoff", M.K_PAYOFF)):
         ms, cnt = pop.profile_read(k)
         kern[name] = {"total_ms": round(ms, 3), "launches": cnt,
                       "avg_us": round(1000.0 * ms / max(cnt, 1), 3)}
+        if name in work and cnt:
+            t = ms * 1e-3 / cnt
+            w = work[name]
+            kern[name]["alg_bytes"] = w["bytes"]
+            kern[name]["hbm_GBps"] = round(w["bytes"] / t / 1e9, 1)
+            kern[name]["hbm_frac"] = round(w["bytes"] / t / 1e9 / PEAK_HBM_GBS, 4)
+            if name == "env" and "flops" in w:
+                kern[name]["fp32_TFLOPs"] = round(w["flops"] / t / 1e12, 2)
+                kern[name]["alu_frac"] = round(w["flops"] / t / 1e12 / PEAK_F32_ALU_TFLOPS, 4)
     pop.profile_enable(False)
 
     ms_step = 1000.0 * el / args.steps
@@ -218,6 +267,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 3),
         "fill_time_ms": round(ms_step, 3),
+        "fill_time_ms_median": round(1000.0 * sorted(step_s)[len(step_s) // 2], 3),
+        "fill_time_ms_min": round(1000.0 * min(step_s), 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
