@@ -178,7 +178,8 @@ __global__ __launch_bounds__(256) void step_pursuit_kernel(
 //   s'[e][k] = tanh_ref( fma-chain_{c=0..D-1}(W[k][c], s[e][c]) + emb[0][a_0][k]
 //                        + emb[1][a_1][k] + ... )
 // Thread (tx = tid%64, ty = tid/64) keeps the accumulators of envs
-// ty*EPT..ty*EPT+EPT-1 and outputs tx + 64j; the input index c runs in ascending order through
+// ty*EPT..ty*EPT+EPT-1 and outputs g*64*GW + GW*tx + j (groups of GW <= 4
+// consecutive outputs); the input index c runs in ascending order through
 // LDS-staged chunks of WT (c-major) and of the state (so every accumulator
 // sees exactly the sequential fused chain, no split of the sum).  The reward
 // r = u . s' is then a sequential fused chain per env over the staged s'.
@@ -189,6 +190,52 @@ constexpr int kFeatKC = 32;
 constexpr int kFeatWaves = 8, kFeatThreads = 64 * kFeatWaves;
 
 // EPT envs per thread.
+// GW consecutive floats (GW = 1, 2 or 4) as one load or store: outputs are
+// mapped to threads in groups of GW consecutive indices, so the WT reads from
+// LDS, the embedding loads and the state stores are single wide accesses.
+template <int GW>
+struct FVec;
+template <>
+struct FVec<1> {
+    float v[1];
+    __device__ __forceinline__ void load(const float* p) { v[0] = *p; }
+    __device__ __forceinline__ void store(float* p) const { *p = v[0]; }
+};
+template <>
+struct FVec<2> {
+    float v[2];
+    __device__ __forceinline__ void load(const float* p)
+    {
+        typedef float v2f __attribute__((ext_vector_type(2)));
+        const v2f t = *reinterpret_cast<const v2f*>(p);
+        v[0] = t.x;
+        v[1] = t.y;
+    }
+    __device__ __forceinline__ void store(float* p) const
+    {
+        typedef float v2f __attribute__((ext_vector_type(2)));
+        *reinterpret_cast<v2f*>(p) = v2f{v[0], v[1]};
+    }
+};
+template <>
+struct FVec<4> {
+    float v[4];
+    __device__ __forceinline__ void load(const float* p)
+    {
+        typedef float v4f __attribute__((ext_vector_type(4)));
+        const v4f t = *reinterpret_cast<const v4f*>(p);
+        v[0] = t.x;
+        v[1] = t.y;
+        v[2] = t.z;
+        v[3] = t.w;
+    }
+    __device__ __forceinline__ void store(float* p) const
+    {
+        typedef float v4f __attribute__((ext_vector_type(4)));
+        *reinterpret_cast<v4f*>(p) = v4f{v[0], v[1], v[2], v[3]};
+    }
+};
+
 template <int D, int EPT>
 __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     const float* __restrict__ WT, const float* __restrict__ emb, const float* __restrict__ u,
@@ -196,9 +243,12 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     float* __restrict__ s_out, float* __restrict__ ret)
 {
     constexpr int kFeatEnvs = kFeatWaves * EPT;
-    constexpr int NJ = D / 64;
+    constexpr int NJ = D / 64;                  // outputs per thread
+    constexpr int GW = NJ < 4 ? NJ : 4;         // ... in groups of GW consecutive ones
+    constexpr int NG = NJ / GW;                 // output k of (group g, j) = g*64*GW + GW*tx + j
     constexpr int SSTR = kFeatEnvs + 4;
-    constexpr int WS_FLOATS = kFeatKC * D > kFeatEnvs * (D + 1) ? kFeatKC * D : kFeatEnvs * (D + 1);
+    constexpr int SLD = D + 4;                  // row stride of s' in LDS (16-byte rows)
+    constexpr int WS_FLOATS = kFeatKC * D > kFeatEnvs * SLD ? kFeatKC * D : kFeatEnvs * SLD;
     __shared__ __attribute__((aligned(16))) float Ws[WS_FLOATS];
     __shared__ __attribute__((aligned(16))) float Ss[kFeatKC * SSTR];
     const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
@@ -269,8 +319,13 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
         for (int c = 0; c < kFeatKC; ++c) {
             float w[NJ];
 #pragma unroll
-            for (int j = 0; j < NJ; ++j)
-                w[j] = Ws[c * D + tx + 64 * j];
+            for (int g = 0; g < NG; ++g) {
+                FVec<GW> t;
+                t.load(&Ws[c * D + g * 64 * GW + GW * tx]);
+#pragma unroll
+                for (int j = 0; j < GW; ++j)
+                    w[g * GW + j] = t.v[j];
+            }
             float sv[EPT];
             const v4f* sp = reinterpret_cast<const v4f*>(&Ss[c * SSTR + ty * EPT]);
 #pragma unroll
@@ -292,7 +347,7 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
 
     // epilogue: embeddings in seat order (seat-outer so that each seat's loads
     // for all of the thread's outputs are independent), tanh_ref, store s'
-    float* Sl = Ws;   // [kFeatEnvs][D+1]
+    float* Sl = Ws;   // [kFeatEnvs][SLD]
     float pre[EPT][NJ];
 #pragma unroll
     for (int i = 0; i < EPT; ++i)
@@ -306,13 +361,18 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
 #pragma unroll
             for (int i = 0; i < EPT; ++i) {
                 const int a_q = (int)((act_pk[i] >> (8 * q)) & 0xFFu);
-                off[i] = (q * ea.A + a_q) * D + tx;
+                off[i] = (q * ea.A + a_q) * D + GW * tx;
             }
 #pragma unroll
             for (int i = 0; i < EPT; ++i)
 #pragma unroll
-                for (int j = 0; j < NJ; ++j)
-                    pre[i][j] = pre[i][j] + emb[off[i] + 64 * j];
+                for (int g = 0; g < NG; ++g) {
+                    FVec<GW> t;
+                    t.load(emb + off[i] + g * 64 * GW);
+#pragma unroll
+                    for (int j = 0; j < GW; ++j)
+                        pre[i][g * GW + j] = pre[i][g * GW + j] + t.v[j];
+                }
         }
     }
 #pragma unroll
@@ -320,12 +380,15 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
         const int el = ty * EPT + i;
         const int64_t e = e0 + el;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int k = tx + 64 * j;
-            const float sn = tanh_ref(pre[i][j]);
+        for (int g = 0; g < NG; ++g) {
+            const int k0 = g * 64 * GW + GW * tx;
+            FVec<GW> t;
+#pragma unroll
+            for (int j = 0; j < GW; ++j)
+                t.v[j] = tanh_ref(pre[i][g * GW + j]);
             if (e < n)
-                s_out[e * D + k] = sn;
-            Sl[el * (D + 1) + k] = sn;
+                t.store(s_out + e * D + k0);
+            t.store(Sl + el * SLD + k0);
         }
     }
     __syncthreads();
@@ -333,7 +396,7 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
         int64_t e = e0 + tid;
         if (e < n) {
             float r = 0.0f;
-            const float* row = Sl + tid * (D + 1);
+            const float* row = Sl + tid * SLD;
             for (int k = 0; k < D; ++k)
                 r = __builtin_fmaf(u[k], row[k], r);
             for (int q = 0; q < ea.n_agents; ++q) {
