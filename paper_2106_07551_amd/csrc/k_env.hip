@@ -391,19 +391,28 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
             t.store(Sl + el * SLD + k0);
         }
     }
+    // reward chain of the workgroup's envs (one lane each); the seats' running
+    // returns are fetched before the chain so their latency overlaps it, and
+    // the chain is unrolled so that its LDS and scalar loads run ahead of the
+    // dependent FMAs
+    const int64_t er = e0 + tid;
+    const bool rlane = tid < kFeatEnvs && er < n;
+    float rv[kMaxAgents];
+#pragma unroll
+    for (int q = 0; q < kMaxAgents; ++q)
+        if (rlane && q < ea.n_agents)
+            rv[q] = ret[(int64_t)q * n + er];
     __syncthreads();
-    if (tid < kFeatEnvs) {
-        int64_t e = e0 + tid;
-        if (e < n) {
-            float r = 0.0f;
-            const float* row = Sl + tid * SLD;
-            for (int k = 0; k < D; ++k)
-                r = __builtin_fmaf(u[k], row[k], r);
-            for (int q = 0; q < ea.n_agents; ++q) {
-                float v = ((ea.team_row >> q) & 1u) ? r : -r;
-                ret[(int64_t)q * n + e] = ret[(int64_t)q * n + e] + v;
-            }
-        }
+    if (rlane) {
+        float r = 0.0f;
+        const float* row = Sl + tid * SLD;
+#pragma unroll
+        for (int k = 0; k < D; ++k)
+            r = __builtin_fmaf(u[k], row[k], r);
+#pragma unroll
+        for (int q = 0; q < kMaxAgents; ++q)
+            if (q < ea.n_agents)
+                ret[(int64_t)q * n + er] = rv[q] + (((ea.team_row >> q) & 1u) ? r : -r);
     }
 }
 
