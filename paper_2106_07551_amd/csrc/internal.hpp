@@ -127,6 +127,11 @@ hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int4* tile_
 // tiles halve the weight traffic per row but leave one workgroup per CU; on
 // the 4v4 and d=512 workloads they measured 12% and 3% slower.)
 constexpr int kBf16TileRows = 64;
+// Threads of a 64-row tile's workgroup: eight wavefronts (two workgroups per
+// CU give four per SIMD to hide the weight-fragment latency; pursuit's forward
+// measured 29.5 -> 23.7 us against four) for hidden widths >= 128; four below,
+// where eight would leave a wavefront no whole tile.
+constexpr int bf16_tile_threads(int hid) { return hid >= 128 ? 512 : 256; }
 hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid, int d,
                            int tile_rows, const int32_t* perm, const int32_t* perm_env,
                            const int4* tile_info, int64_t n_slots, const void* state,

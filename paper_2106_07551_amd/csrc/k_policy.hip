@@ -552,10 +552,12 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
             v4f v[BATCH];
 #pragma unroll
             for (int u = 0; u < BATCH; ++u) {
+                // padding rows (env < 0) read env 0's row and drop it: a
+                // conditional load here made the compiler spill
                 const int env = row_env[r0 + (u0 + u) * ROWS_PER_PASS];
-                v[u] = v4f{0.f, 0.f, 0.f, 0.f};
-                if (env >= 0)
-                    v[u] = *reinterpret_cast<const v4f*>(S + (uint32_t)env * (uint32_t)KIN);
+                const v4f t =
+                    *reinterpret_cast<const v4f*>(S + (uint32_t)max(env, 0) * (uint32_t)KIN);
+                v[u] = env >= 0 ? t : v4f{0.f, 0.f, 0.f, 0.f};
             }
 #pragma unroll
             for (int u = 0; u < BATCH; ++u) {
@@ -600,13 +602,16 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
     }
 }
 
-// MR rows per tile (the library uses 64: four wavefronts, two workgroups per CU).
+// MR rows per tile (the library uses 64), two workgroups per CU; eight
+// wavefronts per workgroup for hidden widths >= 128 (four per SIMD in all),
+// four below.
 // Layers 1 and 2 run from LDS rows; the output layer is fed from the layer-2
 // accumulators (out_from_acc), its partials summed through the row buffer.
 template <int HID, int OBS, int KIN, int MR>
-__global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpBf16Args a)
+__global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void mlp_bf16_kernel(
+    MlpBf16Args a)
 {
-    constexpr int THREADS = MR * 4, WAVES = MR / 16, RTILES = MR / 32;
+    constexpr int THREADS = bf16_tile_threads(HID), WAVES = THREADS / 64, RTILES = MR / 32;
     __shared__ __attribute__((aligned(16))) uint16_t buf[MR * kLdw];
     __shared__ int row_slot[MR];
     __shared__ int row_env[MR];
@@ -668,8 +673,8 @@ __global__ __launch_bounds__(MR * 4, MR == 64 ? 2 : 1) void mlp_bf16_kernel(MlpB
     __syncthreads();
     {
         const int row = tid >> 2;
-        out_reduce<S::NGROUPS, RTILES>(red, row, row < nrows ? row_slot[row] : -1, tid & 3, a.A,
-                                       a.b3 + p * a.A, a.logits);
+        out_reduce<S::NGROUPS, RTILES>(red, row, row < nrows && row < MR ? row_slot[row] : -1,
+                                       tid & 3, a.A, a.b3 + p * a.A, a.logits);
     }
 }
 
@@ -902,7 +907,7 @@ template <int HID, int OBS, int KIN>
 static void launch_one(const MlpBf16Args& a, int rows, int blocks, hipStream_t s)
 {
     (void)rows;   // kBf16TileRows
-    mlp_bf16_kernel<HID, OBS, KIN, kBf16TileRows><<<blocks, kBf16TileRows * 4, 0, s>>>(a);
+    mlp_bf16_kernel<HID, OBS, KIN, kBf16TileRows><<<blocks, bf16_tile_threads(HID), 0, s>>>(a);
 }
 
 template <int HID>
