@@ -260,7 +260,7 @@ void malib_pop_destroy(malib_pop_t p)
         if (q)
             (void)hipFree(q);
     for (DevBuf* b : {&p->perm, &p->perm_env, &p->tile_info, &p->hist, &p->base, &p->offsets, &p->tile_off, &p->logits,
-                      &p->actions, &p->ret, &p->state0, &p->state1, &p->wt, &p->done,
+                      &p->actions, &p->ret, &p->state0, &p->state1, &p->obs, &p->wt, &p->done,
                       &p->thresholds})
         release(*b);
     for (auto& ev : p->prof.pool) {
@@ -405,6 +405,13 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
         HIP_TRY(ensure(pop->done, n_envs));
     if (env->kind == MALIB_ENV_FEATURE)
         HIP_TRY(ensure(pop->wt, sizeof(float) * env->d * env->d));
+    // bf16 observation rows for the 64-row policy kernel (its gather reads half
+    // the bytes); the persistent kernel converts the fp32 state itself, since
+    // at d = 512 the extra rows cost the env step more than they save
+    const bool bf16_obs =
+        env->kind == MALIB_ENV_FEATURE && pop->kind == MALIB_POLICY_MLP_BF16 && !persist;
+    if (bf16_obs)
+        HIP_TRY(ensure(pop->obs, sizeof(uint16_t) * env->d * n_envs));
     if (mlp) {
         HIP_TRY(ensure(pop->perm, sizeof(int32_t) * ns));
         HIP_TRY(ensure(pop->perm_env, sizeof(int32_t) * ns));
@@ -415,6 +422,7 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
         HIP_TRY(ensure(pop->tile_off, sizeof(int32_t) * (pop->P + 1)));
     }
     ea.WT = (const float*)pop->wt.ptr;
+    ea.obs = bf16_obs ? (uint16_t*)pop->obs.ptr : nullptr;
     float* ret = (float*)pop->ret.ptr;
     float* logits = (float*)pop->logits.ptr;
     uint8_t* actions = (uint8_t*)pop->actions.ptr;
@@ -471,7 +479,8 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
         else
             HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d, tile_rows,
                                     perm, (const int32_t*)pop->perm_env.ptr,
-                                    (const int4*)pop->tile_info.ptr, ns, cur, logits, s));
+                                    (const int4*)pop->tile_info.ptr, ns,
+                                    bf16_obs ? (const void*)ea.obs : cur, logits, s));
         prof_end(*pop, pi, s);
         if (si >= 0 && trace->logits)
             HIP_TRY(hipMemcpyAsync(trace->logits + (int64_t)si * ns * pop->A, logits,

@@ -62,7 +62,7 @@ struct Pop {
     int64_t envs = 0;
     // scratch, grown on demand
     DevBuf perm, perm_env, tile_info, hist, base, offsets, tile_off, logits, actions, ret,
-        state0, state1, wt, done, thresholds;
+        state0, state1, obs, wt, done, thresholds;
     Profile prof;
 };
 
@@ -99,6 +99,10 @@ struct EnvArgs {
     const float* WT;     // transposed W (scratch)
     const float* emb;
     const float* u;
+    // FEATURE with bf16 policies: the observation bf16_rne(s) of every env,
+    // [n_envs][d], written by reset and by each step next to the fp32 state
+    // (the policy forward gathers these rows: half the bytes, no conversion)
+    uint16_t* obs;
 };
 hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,
                         void* state, uint8_t* done, hipStream_t s);

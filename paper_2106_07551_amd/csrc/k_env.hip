@@ -44,8 +44,8 @@ __global__ void reset_pursuit_kernel(uint8_t* __restrict__ pos, uint8_t* __restr
 
 // s0[k] = (2*(x_k>>9)+1 - 2^23) * 2^-23 with x_k lane k%8 of block k/8.
 // One thread per (env, block of 8 coordinates).
-__global__ void reset_feature_kernel(float* __restrict__ s, int64_t n, int d, uint64_t seed,
-                                     int64_t env_offset, int shared)
+__global__ void reset_feature_kernel(float* __restrict__ s, uint16_t* __restrict__ obs, int64_t n,
+                                     int d, uint64_t seed, int64_t env_offset, int shared)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     int nb = d / 8;
@@ -64,6 +64,10 @@ __global__ void reset_feature_kernel(float* __restrict__ s, int64_t n, int d, ui
     float4* dst = reinterpret_cast<float4*>(s + e * d + blk * 8);
     dst[0] = make_float4(v[0], v[1], v[2], v[3]);
     dst[1] = make_float4(v[4], v[5], v[6], v[7]);
+    if (obs)
+        *reinterpret_cast<uint4*>(obs + e * d + blk * 8) =
+            make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                       pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
 }
 
 hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,
@@ -78,7 +82,7 @@ hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t
     } else if (e.kind == MALIB_ENV_FEATURE) {
         int64_t total = n_envs * (e.d / 8);
         reset_feature_kernel<<<(int)((total + 255) / 256), 256, 0, s>>>(
-            (float*)state, n_envs, e.d, seed, env_offset, shared);
+            (float*)state, e.obs, n_envs, e.d, seed, env_offset, shared);
     }
     return hipGetLastError();
 }
@@ -236,6 +240,20 @@ struct FVec<4> {
     }
 };
 
+// bf16_rne of GW consecutive floats as one 2-, 4- or 8-byte store.
+template <int GW>
+__device__ __forceinline__ void store_bf16(uint16_t* p, const FVec<GW>& t)
+{
+    if constexpr (GW == 1) {
+        *p = bf16_bits(t.v[0]);
+    } else if constexpr (GW == 2) {
+        *reinterpret_cast<uint32_t*>(p) = pack_bf16x2(t.v[0], t.v[1]);
+    } else {
+        *reinterpret_cast<uint2*>(p) =
+            make_uint2(pack_bf16x2(t.v[0], t.v[1]), pack_bf16x2(t.v[2], t.v[3]));
+    }
+}
+
 template <int D, int EPT>
 __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     const float* __restrict__ WT, const float* __restrict__ emb, const float* __restrict__ u,
@@ -386,8 +404,11 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
 #pragma unroll
             for (int j = 0; j < GW; ++j)
                 t.v[j] = tanh_ref(pre[i][g * GW + j]);
-            if (e < n)
+            if (e < n) {
                 t.store(s_out + e * D + k0);
+                if (ea.obs)
+                    store_bf16<GW>(ea.obs + e * D + k0, t);
+            }
             t.store(Sl + el * SLD + k0);
         }
     }

@@ -233,6 +233,9 @@ struct MlpBf16Args {
     const uint4* w1; const uint4* w2; const uint4* w3;
     const float* b1; const float* b2; const float* b3;
     const int32_t* perm; const int32_t* perm_env; const int4* tile_info;
+    // feature observations: bf16 rows [n_envs][d] (bf16_rne of the state) for
+    // the 64-row kernel, the fp32 state for the persistent one; pursuit: the
+    // env positions; iterated game: the action histories
     const void* state;
     float* logits;
     int P, A, in_dim, n_agents, grid, d;
@@ -538,34 +541,34 @@ template <int OBS, int KIN, int MR, int THREADS>
 __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_slot,
                                           const int* row_env, uint16_t* buf, int tid)
 {
-    if (OBS == kObsFeature) {
-        // KIN == d: rows of d floats, as float4; thread t keeps column t % (KIN/4)
-        constexpr int Q4 = KIN / 4;
-        constexpr int ROWS_PER_PASS = THREADS / Q4;
+    if constexpr (OBS == kObsFeature) {
+        // KIN == d: bf16 rows of d, copied 8 columns (16 bytes) at a time;
+        // thread t keeps columns 8 (t % (KIN/8)) ..
+        constexpr int Q8 = KIN / 8;
+        constexpr int ROWS_PER_PASS = THREADS / Q8;
         constexpr int PASSES = MR / ROWS_PER_PASS;
-        const int c = (tid % Q4) * 4, r0 = tid / Q4;
+        static_assert(KIN % 8 == 0 && THREADS % Q8 == 0 && PASSES * ROWS_PER_PASS == MR,
+                      "whole rows per pass");
+        const int c = (tid % Q8) * 8, r0 = tid / Q8;
         constexpr int BATCH = PASSES < 16 ? PASSES : 16;
-        typedef float v4f __attribute__((ext_vector_type(4)));
-        const float* S = (const float*)a.state + c;
+        const uint16_t* S = (const uint16_t*)a.state + c;
 #pragma unroll
         for (int u0 = 0; u0 < PASSES; u0 += BATCH) {
-            v4f v[BATCH];
+            uint4 v[BATCH];
 #pragma unroll
             for (int u = 0; u < BATCH; ++u) {
                 // padding rows (env < 0) read env 0's row and drop it: a
                 // conditional load here made the compiler spill
                 const int env = row_env[r0 + (u0 + u) * ROWS_PER_PASS];
-                const v4f t =
-                    *reinterpret_cast<const v4f*>(S + (uint32_t)max(env, 0) * (uint32_t)KIN);
-                v[u] = env >= 0 ? t : v4f{0.f, 0.f, 0.f, 0.f};
+                const uint4 t =
+                    *reinterpret_cast<const uint4*>(S + (uint32_t)max(env, 0) * (uint32_t)KIN);
+                v[u] = env >= 0 ? t : make_uint4(0, 0, 0, 0);
             }
 #pragma unroll
-            for (int u = 0; u < BATCH; ++u) {
-                uint2 pk = make_uint2(pack_bf16x2(v[u].x, v[u].y), pack_bf16x2(v[u].z, v[u].w));
-                *reinterpret_cast<uint2*>(buf + (r0 + (u0 + u) * ROWS_PER_PASS) * kLdw + c) = pk;
-            }
+            for (int u = 0; u < BATCH; ++u)
+                *reinterpret_cast<uint4*>(buf + (r0 + (u0 + u) * ROWS_PER_PASS) * kLdw + c) = v[u];
         }
-    } else if (OBS == kObsPursuit) {
+    } else if constexpr (OBS == kObsPursuit) {
         const uint8_t* pos = (const uint8_t*)a.state;
         for (int i = tid; i < MR * KIN; i += THREADS) {
             const int r = i / KIN, c = i - r * KIN;
