@@ -71,6 +71,8 @@ def algorithmic_work(wl):
         # state in and out, joint actions, returns read-modify-write, W and the
         # embedding table once
         b = n * (8 * d + na + 8 * na) + 4 * d * d + 4 * na * A * d + 4 * d
+        if wl.pol_kind == W.MLP_BF16 and policy_kernel(wl) == "mlp_bf16_kernel":
+            b += n * 2 * d       # the bf16 observation rows for the 64-row kernel
         out["env"] = {"bytes": b, "flops": 2 * d * d * n}
     elif wl.env_kind == W.PURSUIT:
         out["env"] = {"bytes": n * (2 * 2 + 2 + 1 + 8 * na)}
@@ -81,7 +83,11 @@ def algorithmic_work(wl):
     if wl.dims:
         wbytes = (2 if wl.pol_kind == W.MLP_BF16 else 4) * wl.P * sum(
             wl.dims[i] * wl.dims[i + 1] for i in range(len(wl.dims) - 1))
-        obs = n * wl.d * 4 if wl.env_kind == W.FEATURE else 0
+        # feature observations, each env's once: fp32 state rows for the
+        # persistent kernel, the env step's bf16 rows for the 64-row kernel
+        obs = 0
+        if wl.env_kind == W.FEATURE:
+            obs = n * wl.d * (4 if policy_kernel(wl) == "mlp_bf16_persist_kernel" else 2)
         out["policy"] = {"bytes": wbytes + obs + ns * 4 * A,
                          "flops": policy_flops_per_frame(wl.dims) * ns}
     else:
