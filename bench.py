@@ -64,22 +64,23 @@ def algorithmic_work(wl):
     n, na, A = wl.n_envs, wl.n_agents, wl.n_actions
     ns = n * na
     out = {}
-    # sampling: logits in, action byte out
-    out["sample"] = {"bytes": ns * (4 * A + 1)}
+    # the env step also samples the actions: the step's logits are read once
+    sample = ns * 4 * A
     if wl.env_kind == W.FEATURE:
         d = wl.d
-        # state in and out, joint actions, returns read-modify-write, W and the
-        # embedding table once
-        b = n * (8 * d + na + 8 * na) + 4 * d * d + 4 * na * A * d + 4 * d
+        # state in and out, returns read-modify-write, W and the embedding
+        # table once
+        b = n * (8 * d + 8 * na) + 4 * d * d + 4 * na * A * d + 4 * d
         if wl.pol_kind == W.MLP_BF16 and policy_kernel(wl) == "mlp_bf16_kernel":
             b += n * 2 * d       # the bf16 observation rows for the 64-row kernel
         out["env"] = {"bytes": b, "flops": 2 * d * d * n}
     elif wl.env_kind == W.PURSUIT:
-        out["env"] = {"bytes": n * (2 * 2 + 2 + 1 + 8 * na)}
+        out["env"] = {"bytes": n * (2 * 2 + 1 + 8 * na)}     # cells, done, returns
     elif wl.env_kind == W.ITER_MATRIX:
-        out["env"] = {"bytes": n * (2 * 2 + na + 8 * na)}
+        out["env"] = {"bytes": n * (2 * 2 + 8 * na)}         # history, returns
     else:
-        out["env"] = {"bytes": n * (na + 8 * na)}
+        out["env"] = {"bytes": n * 8 * na}                   # returns
+    out["env"]["bytes"] += sample
     if wl.dims:
         wbytes = (2 if wl.pol_kind == W.MLP_BF16 else 4) * wl.P * sum(
             wl.dims[i] * wl.dims[i + 1] for i in range(len(wl.dims) - 1))
@@ -231,8 +232,8 @@ def main():
     pop.profile_enable(True)
     one_step()
     work = algorithmic_work(wl)
-    for name, k in (("policy", M.K_POLICY), ("sample", M.K_SAMPLE), ("env", M.K_ENV),
-                    ("setup", M.K_SETUP), ("payoff", M.K_PAYOFF)):
+    for name, k in (("policy", M.K_POLICY), ("env", M.K_ENV), ("setup", M.K_SETUP),
+                    ("payoff", M.K_PAYOFF)):
         ms, cnt = pop.profile_read(k)
         kern[name] = {"total_ms": round(ms, 3), "launches": cnt,
                       "avg_us": round(1000.0 * ms / max(cnt, 1), 3)}

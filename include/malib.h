@@ -248,7 +248,9 @@ const char* malib_last_error(void);
 
 enum {
     MALIB_K_POLICY = 0,   /* grouped policy forward */
-    MALIB_K_SAMPLE = 1,   /* Gumbel-max action sampling */
+    MALIB_K_SAMPLE = 1,   /* Gumbel-max action sampling: runs inside the env
+                             step (MALIB_K_ENV), so this class records no
+                             launches */
     MALIB_K_ENV = 2,      /* environment step + return accumulation */
     MALIB_K_SETUP = 3,    /* bucketing + reset */
     MALIB_K_PAYOFF = 4,   /* payoff reduction */

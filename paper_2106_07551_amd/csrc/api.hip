@@ -260,7 +260,7 @@ void malib_pop_destroy(malib_pop_t p)
         if (q)
             (void)hipFree(q);
     for (DevBuf* b : {&p->perm, &p->perm_env, &p->tile_info, &p->hist, &p->base, &p->offsets, &p->tile_off, &p->logits,
-                      &p->actions, &p->ret, &p->state0, &p->state1, &p->obs, &p->wt, &p->done,
+                      &p->ret, &p->state0, &p->state1, &p->obs, &p->wt, &p->done,
                       &p->thresholds})
         release(*b);
     for (auto& ev : p->prof.pool) {
@@ -393,7 +393,6 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
     const int max_tiles = max_tiles_for(ns, pop->P, tile_rows);
     const int n_chunks = (int)((ns + kBucketChunk - 1) / kBucketChunk);
     HIP_TRY(ensure(pop->logits, sizeof(float) * ns * pop->A));
-    HIP_TRY(ensure(pop->actions, ns));
     HIP_TRY(ensure(pop->ret, sizeof(float) * ns));
     int64_t sb = state_bytes_per_env(env->kind, env->d) * n_envs;
     if (sb > 0) {
@@ -425,7 +424,6 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
     ea.obs = bf16_obs ? (uint16_t*)pop->obs.ptr : nullptr;
     float* ret = (float*)pop->ret.ptr;
     float* logits = (float*)pop->logits.ptr;
-    uint8_t* actions = (uint8_t*)pop->actions.ptr;
     uint8_t* done = env->kind == MALIB_ENV_PURSUIT ? (uint8_t*)pop->done.ptr : nullptr;
     void* cur = pop->state0.ptr;
     void* nxt = env->kind == MALIB_ENV_FEATURE ? pop->state1.ptr : pop->state0.ptr;
@@ -485,13 +483,16 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
         if (si >= 0 && trace->logits)
             HIP_TRY(hipMemcpyAsync(trace->logits + (int64_t)si * ns * pop->A, logits,
                                    sizeof(float) * ns * pop->A, hipMemcpyDeviceToDevice, s));
-        pi = prof_begin(*pop, MALIB_K_SAMPLE, s);
-        uint8_t* log = (trace && trace->actions) ? trace->actions + (int64_t)t * ns : nullptr;
-        HIP_TRY(launch_gumbel(logits, n_envs, n_agents, pop->A, seed, env_offset, t, done,
-                              actions, log, pop->dev_flags, s));
-        prof_end(*pop, pi, s);
+        // action sampling happens inside the env step (one launch fewer per step)
+        SampleArgs sa;
+        sa.logits = logits;
+        sa.seed = seed;
+        sa.env_offset = env_offset;
+        sa.t = t;
+        sa.log = (trace && trace->actions) ? trace->actions + (int64_t)t * ns : nullptr;
+        sa.flags = pop->dev_flags;
         pi = prof_begin(*pop, MALIB_K_ENV, s);
-        HIP_TRY(launch_env_step(ea, n_envs, actions, cur, nxt, done, ret, pop->dev_frames, s));
+        HIP_TRY(launch_env_step(ea, sa, n_envs, cur, nxt, done, ret, pop->dev_frames, s));
         prof_end(*pop, pi, s);
         std::swap(cur, nxt);
         if (env->kind != MALIB_ENV_FEATURE)

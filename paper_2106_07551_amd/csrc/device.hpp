@@ -152,4 +152,53 @@ __device__ __forceinline__ float tanh_ref(float x)
 // Device error flags (bit values of malib_eval_stats.device_flags).
 enum : int { kErrPid = 1, kErrNaN = 2 };
 
+// Gumbel noise -ln(-ln u) for u in [2^-24, 1 - 2^-24] (uniform01's range):
+// both logarithms see normal fp32 inputs, so each is the hardware log2
+// (v_log_f32, 1 ulp) times ln 2, without the denormal scaling of logf.
+__device__ __forceinline__ float gumbel01(float u)
+{
+    const float ln2 = 0x1.62e430p-1f;
+    const float e = -(__builtin_amdgcn_logf(u) * ln2);
+    return -(__builtin_amdgcn_logf(e) * ln2);
+}
+
+// Gumbel-max action of one agent slot from its A logits l[0..A-1]:
+// z_a = l_a + g_a with g_a = gumbel01(u_a) in fp32, u_a from lane a%8 of
+// block a/8 of (global env g, step t, kPurposeAction<<32 | seat); the first
+// index of the maximum wins.  AMAX >= A (a multiple of 8): all logits are
+// loaded and all Philox blocks drawn before the arithmetic, so their
+// latencies overlap.  A NaN logit sets `nan` and gives action 0.
+template <int AMAX>
+__device__ __forceinline__ int gumbel_action(const float* __restrict__ l, int A, uint64_t seed,
+                                             uint64_t g, int t, int seat, bool& nan)
+{
+    float lv[AMAX];
+#pragma unroll
+    for (int a = 0; a < AMAX; ++a)
+        lv[a] = a < A ? l[a] : 0.0f;
+    u64x4 blk[AMAX / 8];
+#pragma unroll
+    for (int b = 0; b < AMAX / 8; ++b)
+        if (b * 8 < A)
+            blk[b] = stream_block(seed, g, (uint64_t)t, kPurposeAction, (uint32_t)seat,
+                                  (uint64_t)b);
+    float zbest = 0.0f;
+    int best = 0;
+    bool bad = false;
+#pragma unroll
+    for (int a = 0; a < AMAX; ++a) {
+        if (a < A) {
+            const float gn = gumbel01(uniform01(block_lane(blk[a >> 3], a & 7)));
+            bad |= __builtin_isnan(lv[a]);
+            const float z = lv[a] + gn;
+            if (a == 0 || z > zbest) {
+                zbest = z;
+                best = a;
+            }
+        }
+    }
+    nan = bad;
+    return bad ? 0 : best;
+}
+
 }  // namespace malib

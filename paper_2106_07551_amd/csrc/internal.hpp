@@ -61,8 +61,8 @@ struct Pop {
     int64_t host_frames = 0;   // frames of env families with no early termination
     int64_t envs = 0;
     // scratch, grown on demand
-    DevBuf perm, perm_env, tile_info, hist, base, offsets, tile_off, logits, actions, ret,
-        state0, state1, obs, wt, done, thresholds;
+    DevBuf perm, perm_env, tile_info, hist, base, offsets, tile_off, logits, ret, state0,
+        state1, obs, wt, done, thresholds;
     Profile prof;
 };
 
@@ -84,10 +84,18 @@ hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
                               int64_t n_envs, int n_agents, uint64_t seed, int64_t env_offset,
                               int32_t* out, hipStream_t s);
 
-// Gumbel-max action sampling.
-hipError_t launch_gumbel(const float* logits, int64_t n_envs, int n_agents, int A,
-                         uint64_t seed, int64_t env_offset, int t, const uint8_t* done,
-                         uint8_t* actions, uint8_t* log, int* flags, hipStream_t s);
+// Gumbel-max action sampling, done by the env-step kernels for the slots of
+// their envs (gumbel_action): the step's logits, the Philox key and counter
+// parts, the optional action log [n_slots] (255 for finished envs) and the
+// device error flags (kErrNaN).
+struct SampleArgs {
+    const float* logits;   // [n_slots][A]
+    uint64_t seed;
+    int64_t env_offset;
+    int t;
+    uint8_t* log;
+    int* flags;
+};
 
 // Environment kernels.
 struct EnvArgs {
@@ -107,7 +115,7 @@ struct EnvArgs {
 hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,
                         void* state, uint8_t* done, hipStream_t s);
 hipError_t launch_transpose(const float* W, float* WT, int d, hipStream_t s);
-hipError_t launch_env_step(const EnvArgs& e, int64_t n_envs, const uint8_t* actions,
+hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_envs,
                            const void* state_in, void* state_out, uint8_t* done, float* ret,
                            unsigned long long* frames, hipStream_t s);
 hipError_t launch_snapshot_pursuit(const void* state, const uint8_t* done, int64_t n_envs,

@@ -108,16 +108,36 @@ hipError_t launch_transpose(const float* W, float* WT, int d, hipStream_t s)
 
 // ---------------------------------------------------- matrix / iterated / pursuit
 
-// One thread per env.  MATRIX and ITER_MATRIX: r0 = A[a0][a1], r1 = -r0;
-// ITER also shifts the joint action into its history.
-__global__ void step_matrix_kernel(const float* __restrict__ Amat, int A, int iter,
-                                   int64_t n, const uint8_t* __restrict__ act,
-                                   uint16_t* __restrict__ hist, float* __restrict__ ret)
+// The two seats' actions of env e (Gumbel-max over their logits, logged when
+// asked); a NaN logit raises kErrNaN.
+template <int AMAX>
+__device__ __forceinline__ void sample_pair(const SampleArgs& sa, int A, int64_t e, int& a0,
+                                            int& a1)
+{
+    bool n0, n1;
+    const uint64_t g = (uint64_t)(sa.env_offset + e);
+    a0 = gumbel_action<AMAX>(sa.logits + (2 * e) * A, A, sa.seed, g, sa.t, 0, n0);
+    a1 = gumbel_action<AMAX>(sa.logits + (2 * e + 1) * A, A, sa.seed, g, sa.t, 1, n1);
+    if (n0 || n1)
+        atomicOr(sa.flags, kErrNaN);
+    if (sa.log) {
+        sa.log[2 * e] = (uint8_t)a0;
+        sa.log[2 * e + 1] = (uint8_t)a1;
+    }
+}
+
+// One thread per env: both seats' actions, then MATRIX and ITER_MATRIX:
+// r0 = A[a0][a1], r1 = -r0; ITER also shifts the joint action into its history.
+template <int AMAX>
+__global__ void step_matrix_kernel(const float* __restrict__ Amat, int A, int iter, int64_t n,
+                                   SampleArgs sa, uint16_t* __restrict__ hist,
+                                   float* __restrict__ ret)
 {
     int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= n)
         return;
-    int a0 = act[2 * e], a1 = act[2 * e + 1];
+    int a0, a1;
+    sample_pair<AMAX>(sa, A, e, a0, a1);
     float v = Amat[a0 * A + a1];
     ret[e] = ret[e] + v;
     ret[n + e] = ret[n + e] + (-v);
@@ -141,12 +161,13 @@ __device__ __forceinline__ uint32_t torus_move(uint32_t cell, int a, int grid)
     return (uint32_t)(y * grid + x);
 }
 
-// One thread per env.  Simultaneous moves; capture if the two land on the
-// same cell or swap cells: pursuer +1, evader -1, env done.  Counts live
+// One thread per env: both seats' actions (5 each), then simultaneous moves;
+// capture if the two land on the same cell or swap cells: pursuer +1, evader
+// -1, env done.  Finished envs take no action (logged as 255).  Counts live
 // agent-frames (two per live env) with one atomic per workgroup.
 __global__ __launch_bounds__(256) void step_pursuit_kernel(
-    int grid, int64_t n, const uint8_t* __restrict__ act, uint8_t* __restrict__ pos,
-    uint8_t* __restrict__ done, float* __restrict__ ret, unsigned long long* frames)
+    int grid, int64_t n, SampleArgs sa, uint8_t* __restrict__ pos, uint8_t* __restrict__ done,
+    float* __restrict__ ret, unsigned long long* frames)
 {
     __shared__ int live_s;
     if (threadIdx.x == 0)
@@ -156,9 +177,11 @@ __global__ __launch_bounds__(256) void step_pursuit_kernel(
     int live = 0;
     if (e < n && !done[e]) {
         live = 1;
+        int a0, a1;
+        sample_pair<8>(sa, 5, e, a0, a1);
         uint32_t p0 = pos[e], e0 = pos[n + e];
-        uint32_t p1 = torus_move(p0, act[2 * e], grid);
-        uint32_t e1 = torus_move(e0, act[2 * e + 1], grid);
+        uint32_t p1 = torus_move(p0, a0, grid);
+        uint32_t e1 = torus_move(e0, a1, grid);
         pos[e] = (uint8_t)p1;
         pos[n + e] = (uint8_t)e1;
         if (p1 == e1 || (p1 == e0 && e1 == p0)) {
@@ -166,6 +189,9 @@ __global__ __launch_bounds__(256) void step_pursuit_kernel(
             ret[e] = ret[e] + 1.0f;
             ret[n + e] = ret[n + e] + (-1.0f);
         }
+    } else if (e < n && sa.log) {
+        sa.log[2 * e] = 255;
+        sa.log[2 * e + 1] = 255;
     }
     unsigned long long b = __ballot(live);
     if ((threadIdx.x & 63) == 0 && b)
@@ -257,7 +283,7 @@ __device__ __forceinline__ void store_bf16(uint16_t* p, const FVec<GW>& t)
 template <int D, int EPT>
 __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     const float* __restrict__ WT, const float* __restrict__ emb, const float* __restrict__ u,
-    EnvArgs ea, int64_t n, const uint8_t* __restrict__ act, const float* __restrict__ s_in,
+    EnvArgs ea, SampleArgs sa, int64_t n, const float* __restrict__ s_in,
     float* __restrict__ s_out, float* __restrict__ ret)
 {
     constexpr int kFeatEnvs = kFeatWaves * EPT;
@@ -271,26 +297,6 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     __shared__ __attribute__((aligned(16))) float Ss[kFeatKC * SSTR];
     const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
     const int64_t e0 = (int64_t)blockIdx.x * kFeatEnvs;
-
-    // the actions of this thread's envs, packed 8 bits per seat (at most 8
-    // seats); envs past the end read as action 0 and are never stored
-    uint64_t act_pk[EPT];
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-        const int64_t e = e0 + ty * EPT + i;
-        uint64_t v = 0;
-        if (e < n)
-            for (int q = 0; q < ea.n_agents; ++q)
-                v |= (uint64_t)act[e * ea.n_agents + q] << (8 * q);
-        act_pk[i] = v;
-    }
-
-    float acc[EPT][NJ];
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j)
-            acc[i][j] = 0.0f;
 
     // Staging: chunk c0 of WT (KC x D floats, c-major) and of the state (32 envs
     // x KC) goes global -> registers -> LDS; the loads of chunk c0+KC are issued
@@ -310,6 +316,42 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     for (int q = 0; q < WQ; ++q)
         wreg[q] = wsrc[q * kFeatThreads];
     sreg = *reinterpret_cast<const v4f*>(ssrc);
+
+    // the actions of the workgroup's slots while the first chunk loads are in
+    // flight: one thread per slot, Gumbel-max over its logits (envs past the
+    // end take action 0 and are never stored)
+    __shared__ __attribute__((aligned(8))) uint8_t act_s[kFeatEnvs * kMaxAgents];
+    if (tid < kFeatEnvs * ea.n_agents) {
+        const int el = tid / ea.n_agents, seat = tid - el * ea.n_agents;
+        const int64_t e = e0 + el;
+        int a = 0;
+        if (e < n) {
+            const int64_t slot = e * ea.n_agents + seat;
+            bool nan;
+            a = gumbel_action<kMaxActions>(sa.logits + slot * ea.A, ea.A, sa.seed,
+                                            (uint64_t)(sa.env_offset + e), sa.t, seat, nan);
+            if (nan)
+                atomicOr(sa.flags, kErrNaN);
+            if (sa.log)
+                sa.log[slot] = (uint8_t)a;
+        }
+        act_s[el * kMaxAgents + seat] = (uint8_t)a;
+    }
+    __syncthreads();
+    // the actions of this thread's envs, 8 bits per seat (bytes of seats
+    // >= n_agents are never read)
+    uint64_t act_pk[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+        act_pk[i] = *reinterpret_cast<const uint64_t*>(act_s + (ty * EPT + i) * kMaxAgents);
+
+    float acc[EPT][NJ];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+            acc[i][j] = 0.0f;
+
     for (int c0 = 0; c0 < D; c0 += kFeatKC) {
         v4f* dst = reinterpret_cast<v4f*>(Ws);
 #pragma unroll
@@ -437,37 +479,50 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     }
 }
 
-hipError_t launch_env_step(const EnvArgs& e, int64_t n_envs, const uint8_t* actions,
+hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_envs,
                            const void* state_in, void* state_out, uint8_t* done, float* ret,
                            unsigned long long* frames, hipStream_t s)
 {
     int blocks = (int)((n_envs + 255) / 256);
     switch (e.kind) {
     case MALIB_ENV_MATRIX:
-        step_matrix_kernel<<<blocks, 256, 0, s>>>(e.Amat, e.A, 0, n_envs, actions, nullptr, ret);
+    case MALIB_ENV_ITER_MATRIX: {
+        const int iter = e.kind == MALIB_ENV_ITER_MATRIX;
+        uint16_t* hist = iter ? (uint16_t*)state_out : nullptr;
+        if (e.A <= 8)
+            step_matrix_kernel<8><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+        else if (e.A <= 16)
+            step_matrix_kernel<16><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+        else if (e.A <= 24)
+            step_matrix_kernel<24><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+        else if (e.A <= 32)
+            step_matrix_kernel<32><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+        else
+            return hipErrorInvalidValue;
         break;
-    case MALIB_ENV_ITER_MATRIX:
-        step_matrix_kernel<<<blocks, 256, 0, s>>>(e.Amat, e.A, 1, n_envs, actions,
-                                                  (uint16_t*)state_out, ret);
-        break;
+    }
     case MALIB_ENV_PURSUIT:
-        step_pursuit_kernel<<<blocks, 256, 0, s>>>(e.grid, n_envs, actions, (uint8_t*)state_out,
-                                                   done, ret, frames);
+        if (e.A != 5)
+            return hipErrorInvalidValue;
+        step_pursuit_kernel<<<blocks, 256, 0, s>>>(e.grid, n_envs, sa, (uint8_t*)state_out, done,
+                                                   ret, frames);
         break;
     case MALIB_ENV_FEATURE: {
         const float* si = (const float*)state_in;
         float* so = (float*)state_out;
+        if (e.A > kMaxActions)
+            return hipErrorInvalidValue;
         // 8 envs per thread for d = 512 (64-env workgroups), 4 below (32 envs)
         const int fb8 = (int)((n_envs + 8 * kFeatWaves - 1) / (8 * kFeatWaves));
         const int fb4 = (int)((n_envs + 4 * kFeatWaves - 1) / (4 * kFeatWaves));
         if (e.d == 64)
-            step_feature_kernel<64, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<64, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
         else if (e.d == 128)
-            step_feature_kernel<128, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<128, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
         else if (e.d == 256)
-            step_feature_kernel<256, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<256, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
         else if (e.d == 512)
-            step_feature_kernel<512, 8><<<fb8, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, n_envs, actions, si, so, ret);
+            step_feature_kernel<512, 8><<<fb8, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
         else
             return hipErrorInvalidValue;
         break;

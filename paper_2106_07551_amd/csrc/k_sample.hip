@@ -1,5 +1,5 @@
-// Sampling kernels: meta-strategy draws (policy id per env seat) and
-// Gumbel-max action sampling, both on the Philox4x64-10 stream.
+// Meta-strategy draws (policy id per env seat) on the Philox4x64-10 stream.
+// (Gumbel-max action sampling runs inside the env-step kernels: gumbel_action.)
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -40,93 +40,6 @@ hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
     int blocks = (int)((total + 255) / 256);
     meta_sample_kernel<<<blocks, 256, 0, s>>>(thr, n_sigma, P, n_envs, n_agents, seed,
                                               env_offset, out);
-    return hipGetLastError();
-}
-
-// Gumbel noise -ln(-ln u) for u in [2^-24, 1 - 2^-24] (uniform01's range):
-// both logarithms see normal fp32 inputs, so each is the hardware log2
-// (v_log_f32, 1 ulp) times ln 2, without the denormal scaling of logf.
-__device__ __forceinline__ float gumbel01(float u)
-{
-    const float ln2 = 0x1.62e430p-1f;
-    const float e = -(__builtin_amdgcn_logf(u) * ln2);
-    return -(__builtin_amdgcn_logf(e) * ln2);
-}
-
-// One thread per slot (env * n_agents + seat).  z_a = l_a + g_a with
-// g_a = -log(-log u_a) in fp32 (gumbel01), u_a from lane a%8 of block a/8 of (g, t,
-// kPurposeAction<<32 | seat); the first index of the maximum wins.  Finished
-// envs (done != 0) take no action (255).  AMAX >= A (a multiple of 8): the
-// slot's logits are all loaded and its Philox blocks all drawn before the
-// arithmetic, so their latencies overlap instead of one load per action.
-template <int AMAX>
-__global__ __launch_bounds__(256) void gumbel_kernel(
-    const float* __restrict__ logits, int64_t n_envs, int n_agents, int A, uint64_t seed,
-    int64_t env_offset, int t, const uint8_t* __restrict__ done, uint8_t* __restrict__ actions,
-    uint8_t* __restrict__ log, int* flags)
-{
-    int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (slot >= n_envs * n_agents)
-        return;
-    int64_t e = slot / n_agents;
-    int seat = (int)(slot - e * n_agents);
-    uint8_t best = 255;
-    if (!(done && done[e])) {
-        const float* l = logits + slot * A;
-        float lv[AMAX];
-#pragma unroll
-        for (int a = 0; a < AMAX; ++a)
-            lv[a] = a < A ? l[a] : 0.0f;
-        u64x4 blk[AMAX / 8];
-#pragma unroll
-        for (int b = 0; b < AMAX / 8; ++b)
-            if (b * 8 < A)
-                blk[b] = stream_block(seed, (uint64_t)(env_offset + e), (uint64_t)t,
-                                      kPurposeAction, seat, (uint64_t)b);
-        float zbest = 0.0f;
-        bool nan = false;
-#pragma unroll
-        for (int a = 0; a < AMAX; ++a) {
-            if (a < A) {
-                float g = gumbel01(uniform01(block_lane(blk[a >> 3], a & 7)));
-                nan |= __builtin_isnan(lv[a]);
-                float z = lv[a] + g;
-                if (a == 0 || z > zbest) {
-                    zbest = z;
-                    best = (uint8_t)a;
-                }
-            }
-        }
-        if (nan) {
-            atomicOr(flags, kErrNaN);
-            best = 0;
-        }
-    }
-    actions[slot] = best;
-    if (log)
-        log[slot] = best;
-}
-
-hipError_t launch_gumbel(const float* logits, int64_t n_envs, int n_agents, int A,
-                         uint64_t seed, int64_t env_offset, int t, const uint8_t* done,
-                         uint8_t* actions, uint8_t* log, int* flags, hipStream_t s)
-{
-    int64_t total = n_envs * n_agents;
-    int blocks = (int)((total + 255) / 256);
-    if (A <= 8)
-        gumbel_kernel<8><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset, t,
-                                                done, actions, log, flags);
-    else if (A <= 16)
-        gumbel_kernel<16><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset,
-                                                 t, done, actions, log, flags);
-    else if (A <= 24)
-        gumbel_kernel<24><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset,
-                                                 t, done, actions, log, flags);
-    else if (A <= 32)
-        gumbel_kernel<32><<<blocks, 256, 0, s>>>(logits, n_envs, n_agents, A, seed, env_offset,
-                                                 t, done, actions, log, flags);
-    else
-        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
