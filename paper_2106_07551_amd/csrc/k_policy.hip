@@ -289,7 +289,7 @@ __device__ __forceinline__ void ring_fill(WRing<NT, DEPTH>& ring, Frags frag,
 // rows).  acc[nt][rt] register r, lane i holds output unit nt*32 + (r/4)*8 +
 // (i/32)*4 + r%4 of tile row rt*32 + i%32.  The ring must hold k-steps
 // 0..DEPTH-1.  (The fp32 sum order of a unit is the bias, then the k-steps.)
-template <int NT, int RT, int DEPTH>
+template <int NT, int RT, int DEPTH, int LDW = kLdw>
 __device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring, Frags frag, int ksteps,
                                            int nt0,
                                            int rt0, const uint16_t* buf, int lane,
@@ -316,7 +316,7 @@ __device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring, Frags frag, i
     const uint16_t* bp[RT];
 #pragma unroll
     for (int r = 0; r < RT; ++r)
-        bp[r] = buf + ((rt0 + r) * 32 + brow) * kLdw + bcol;
+        bp[r] = buf + ((rt0 + r) * 32 + brow) * LDW + bcol;
     uint4 b[2][RT];
 #pragma unroll
     for (int r = 0; r < RT; ++r)
@@ -355,7 +355,7 @@ __device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring, Frags frag, i
 // The same layer with one B buffer: row tile r of the next k-step is read
 // from LDS as soon as this k-step's MFMAs on it are issued (row-tile-outer
 // order), which saves RT x 4 VGPRs for the wider wave tiles.
-template <int NT, int RT, int DEPTH>
+template <int NT, int RT, int DEPTH, int LDW = kLdw>
 __device__ __forceinline__ void mfma_layer_1b(WRing<NT, DEPTH>& ring, Frags frag, int ksteps,
                                               int nt0, int rt0, const uint16_t* buf, int lane,
                                               const float* __restrict__ bias,
@@ -377,11 +377,11 @@ __device__ __forceinline__ void mfma_layer_1b(WRing<NT, DEPTH>& ring, Frags frag
         for (int r = 0; r < RT; ++r)
             acc[n][r] = b0;
     }
-    const uint16_t* bp = buf + (rt0 * 32 + (lane & 31)) * kLdw + (lane >> 5) * 8;
+    const uint16_t* bp = buf + (rt0 * 32 + (lane & 31)) * LDW + (lane >> 5) * 8;
     uint4 b[RT];
 #pragma unroll
     for (int r = 0; r < RT; ++r)
-        b[r] = *reinterpret_cast<const uint4*>(bp + r * 32 * kLdw);
+        b[r] = *reinterpret_cast<const uint4*>(bp + r * 32 * LDW);
     for (int k0 = 0; k0 < ksteps; k0 += DEPTH) {
 #pragma unroll
         for (int s = 0; s < DEPTH; ++s) {
@@ -395,7 +395,7 @@ __device__ __forceinline__ void mfma_layer_1b(WRing<NT, DEPTH>& ring, Frags frag
                             __builtin_bit_cast(bf16x8, ring.a[s][n]),
                             __builtin_bit_cast(bf16x8, b[r]), acc[n][r], 0, 0, 0);
                     if (ks + 1 < ksteps)
-                        b[r] = *reinterpret_cast<const uint4*>(bp + r * 32 * kLdw + (ks + 1) * 16);
+                        b[r] = *reinterpret_cast<const uint4*>(bp + r * 32 * LDW + (ks + 1) * 16);
                 }
                 if (ks + DEPTH < ksteps) {
 #pragma unroll
@@ -421,7 +421,7 @@ __device__ __forceinline__ uint32_t relu_pack(float lo, float hi)
 }
 
 // ReLU + bf16, written back as the next layer's input rows.
-template <int NT, int RT>
+template <int NT, int RT, int LDW = kLdw>
 __device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], int nt0, int rt0,
                                                 uint16_t* buf, int lane)
 {
@@ -435,7 +435,7 @@ __device__ __forceinline__ void hidden_epilogue(const f32x16 (&acc)[NT][RT], int
                 const int row = (rt0 + r) * 32 + (lane & 31);
                 uint2 pk = make_uint2(relu_pack(acc[n][r][g * 4 + 0], acc[n][r][g * 4 + 1]),
                                       relu_pack(acc[n][r][g * 4 + 2], acc[n][r][g * 4 + 3]));
-                *reinterpret_cast<uint2*>(buf + row * kLdw + u0) = pk;
+                *reinterpret_cast<uint2*>(buf + row * LDW + u0) = pk;
             }
         }
     }
@@ -486,25 +486,26 @@ __device__ __forceinline__ void out_from_acc(const f32x16 (&acc)[NT][RT],
     }
 }
 
-// Partials of wave group ng for row tiles rt0.. into red[NG][RTILES][16][64]
-// (registers of output groups g < G3 only: the real actions).
-template <int RT, int RTILES>
+// Partials of wave group ng for row tiles rt0.. into red[NG][RTILES][G4][64]
+// (registers of output groups g < G3 only: the real actions; G4 >= 4 G3 is
+// 16 in general and 4 where at most 8 actions are known to be possible).
+template <int RT, int RTILES, int G4 = 16>
 __device__ __forceinline__ void out_partials(float* red, const f32x16 (&o)[RT], int ng, int rt0,
                                              int G3, int lane)
 {
 #pragma unroll
     for (int rr = 0; rr < RT; ++rr)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < G4 / 4; ++g)
             if (g < G3)
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                    red[((ng * RTILES + rt0 + rr) * 16 + g * 4 + q) * 64 + lane] = o[rr][g * 4 + q];
+                    red[((ng * RTILES + rt0 + rr) * G4 + g * 4 + q) * 64 + lane] = o[rr][g * 4 + q];
 }
 
 // Logit (row, u) = sum over wave groups (in order) + bias; thread (row, u0)
 // writes u0, u0+4, ... of its row.
-template <int NG, int RTILES>
+template <int NG, int RTILES, int G4 = 16>
 __device__ __forceinline__ void out_reduce(const float* red, int row, int slot, int u0, int A,
                                            const float* b3, float* __restrict__ logits)
 {
@@ -517,7 +518,7 @@ __device__ __forceinline__ void out_reduce(const float* red, int row, int slot, 
         float v = 0.0f;
 #pragma unroll
         for (int gq = 0; gq < NG; ++gq)
-            v += red[((gq * RTILES + (row >> 5)) * 16 + reg) * 64 + lr];
+            v += red[((gq * RTILES + (row >> 5)) * G4 + reg) * 64 + lr];
         out[u] = v + b3[u];
     }
 }
@@ -537,7 +538,7 @@ struct HidSplit {
 };
 
 // Observation rows of the tile -> LDS (bf16).  KIN is the padded input width.
-template <int OBS, int KIN, int MR, int THREADS>
+template <int OBS, int KIN, int MR, int THREADS, int LDW = kLdw>
 __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_slot,
                                           const int* row_env, uint16_t* buf, int tid)
 {
@@ -566,41 +567,74 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
             }
 #pragma unroll
             for (int u = 0; u < BATCH; ++u)
-                *reinterpret_cast<uint4*>(buf + (r0 + (u0 + u) * ROWS_PER_PASS) * kLdw + c) = v[u];
+                *reinterpret_cast<uint4*>(buf + (r0 + (u0 + u) * ROWS_PER_PASS) * LDW + c) = v[u];
         }
     } else if constexpr (OBS == kObsPursuit) {
-        const uint8_t* pos = (const uint8_t*)a.state;
-        for (int i = tid; i < MR * KIN; i += THREADS) {
-            const int r = i / KIN, c = i - r * KIN;
-            const int slot = row_slot[r];
-            float v = 0.0f;
-            if (slot >= 0 && c < 75) {
-                const int64_t env = slot / a.n_agents;
-                const int seat = slot - (int)env * a.n_agents;
+        // each row's cells are fetched once (one thread per row), packed as
+        // self x << 24 | self y << 16 | pursuer << 8 | evader (-1: padding
+        // row); then one item per (row, window cell) writes its 3 channels
+        __shared__ int cells[MR];
+        static_assert(THREADS >= MR && KIN >= 75, "one thread per row, 75 inputs");
+        const int G = a.grid;
+        if (tid < MR) {
+            const int env = row_env[tid];
+            int cv = -1;
+            if (env >= 0) {
+                const uint8_t* pos = (const uint8_t*)a.state;
+                const int seat = row_slot[tid] - env * a.n_agents;
                 const int pc = pos[env], ec = pos[a.n_envs + env];
                 const int self = seat == 0 ? pc : ec;
-                const int o = c / 3, ch = c - o * 3;
-                const int dy = o / 5 - 2, dx = o % 5 - 2;
-                const int G = a.grid;
-                const int x = ((self % G) + dx + G) % G, y = ((self / G) + dy + G) % G;
-                const int cell = y * G + x;
-                const bool on = ch == 0 ? cell == pc : (ch == 1 ? cell == ec : (dx == 0 && dy == 0));
-                v = on ? 1.0f : 0.0f;
+                cv = ((self % G) << 24) | ((self / G) << 16) | (pc << 8) | ec;
             }
-            buf[r * kLdw + c] = bf16_bits(v);
+            cells[tid] = cv;
+        }
+        __syncthreads();
+        for (int it = tid; it < MR * 25; it += THREADS) {
+            const int r = it / 25, o = it - r * 25;
+            const int cv = cells[r];
+            uint16_t* dst = buf + r * LDW + o * 3;
+            if (cv < 0) {
+                dst[0] = dst[1] = dst[2] = 0;
+                continue;
+            }
+            const int dy = o / 5 - 2, dx = o - (o / 5) * 5 - 2;
+            int x = (cv >> 24) + dx, y = ((cv >> 16) & 0xFF) + dy;   // |dx|, |dy| <= 2 < G
+            x += x < 0 ? G : 0;
+            x -= x >= G ? G : 0;
+            y += y < 0 ? G : 0;
+            y -= y >= G ? G : 0;
+            const int cell = y * G + x;
+            const uint16_t one = 0x3F80;   // bf16 1.0
+            dst[0] = cell == ((cv >> 8) & 0xFF) ? one : 0;
+            dst[1] = cell == (cv & 0xFF) ? one : 0;
+            dst[2] = o == 12 ? one : 0;    // the centre cell: the agent itself
+        }
+        for (int it = tid; it < MR * (KIN - 75); it += THREADS) {
+            const int r = it / (KIN - 75);
+            buf[r * LDW + 75 + (it - r * (KIN - 75))] = 0;
         }
     } else {
-        const uint16_t* hist = (const uint16_t*)a.state;
+        // each row's history is fetched once (one thread per row), packed as
+        // seat << 16 | history (-1: padding row)
+        __shared__ int hs[MR];
+        static_assert(THREADS >= MR, "one thread per row");
+        if (tid < MR) {
+            const int env = row_env[tid];
+            int hv = -1;
+            if (env >= 0) {
+                const uint16_t* hist = (const uint16_t*)a.state;
+                hv = ((row_slot[tid] - env * a.n_agents) << 16) | hist[env];
+            }
+            hs[tid] = hv;
+        }
+        __syncthreads();
         for (int i = tid; i < MR * KIN; i += THREADS) {
             const int r = i / KIN, c = i - r * KIN;
-            const int slot = row_slot[r];
+            const int hv = hs[r];
             float v = 0.0f;
-            if (slot >= 0 && c < a.in_dim) {
-                const int64_t env = slot / a.n_agents;
-                const int seat = slot - (int)env * a.n_agents;
-                v = iter_obs(hist[env], seat, a.A, c);
-            }
-            buf[r * kLdw + c] = bf16_bits(v);
+            if (hv >= 0 && c < a.in_dim)
+                v = iter_obs((uint16_t)(hv & 0xFFFF), hv >> 16, a.A, c);
+            buf[r * LDW + c] = bf16_bits(v);
         }
     }
 }
@@ -615,11 +649,16 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     MlpBf16Args a)
 {
     constexpr int THREADS = bf16_tile_threads(HID), WAVES = THREADS / 64, RTILES = MR / 32;
-    __shared__ __attribute__((aligned(16))) uint16_t buf[MR * kLdw];
+    // row stride: the wider of the input and hidden rows, + 8 to spread banks
+    constexpr int LDW = (KIN > HID ? KIN : HID) + 8;
+    // partial-logit registers kept per (wave group, row tile): pursuit (5
+    // actions) and the iterated game (<= 3) need one accumulator group
+    constexpr int G4 = OBS == kObsFeature ? 16 : 4;
+    constexpr int PART = HidSplit<HID, WAVES, RTILES>::NGROUPS * RTILES * G4 * 64 * 2;   // in bf16
+    constexpr int BUF = MR * LDW > PART ? MR * LDW : PART;
+    __shared__ __attribute__((aligned(16))) uint16_t buf[BUF];
     __shared__ int row_slot[MR];
     __shared__ int row_env[MR];
-    static_assert(HidSplit<HID, WAVES, RTILES>::NGROUPS * RTILES * 16 * 64 * 4 <= MR * kLdw * 2,
-                  "output partials fit in the row buffer");
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -651,20 +690,20 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
         row_env[tid] = tid < nrows ? a.perm_env[r0 + tid] : -1;
     }
     __syncthreads();
-    build_obs<OBS, KIN, MR, THREADS>(a, row_slot, row_env, buf, tid);
+    build_obs<OBS, KIN, MR, THREADS, LDW>(a, row_slot, row_env, buf, tid);
     __syncthreads();
 
     f32x16 acc[S::NT][S::RT];
     // ---- layer 1: KIN -> HID
-    mfma_layer<S::NT, S::RT, S::DEPTH>(ring, W1, KIN / 16, nt0, rt0, buf, lane,
-                                       a.b1 + p * HID, acc);
+    mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W1, KIN / 16, nt0, rt0, buf, lane,
+                                            a.b1 + p * HID, acc);
     ring_fill(ring, W2, HID / 16, nt0, lane);      // overlaps the epilogue
     __syncthreads();
-    hidden_epilogue<S::NT, S::RT>(acc, nt0, rt0, buf, lane);
+    hidden_epilogue<S::NT, S::RT, LDW>(acc, nt0, rt0, buf, lane);
     __syncthreads();
     // ---- layer 2: HID -> HID
-    mfma_layer<S::NT, S::RT, S::DEPTH>(ring, W2, HID / 16, nt0, rt0, buf, lane,
-                                       a.b2 + p * HID, acc);
+    mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W2, HID / 16, nt0, rt0, buf, lane,
+                                            a.b2 + p * HID, acc);
     // ---- layer 3 from the accumulators, partial logits summed through LDS
     uint4 w3[S::NT][2];
     load_w3<S::NT>(w3, frag_src(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16), nt0, lane);
@@ -672,12 +711,13 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     out_from_acc<S::NT, S::RT>(acc, w3, o);
     __syncthreads();   // every wave is done reading the hidden rows: buf takes the partials
     float* red = reinterpret_cast<float*>(buf);
-    out_partials<S::RT, RTILES>(red, o, wave % S::NGROUPS, rt0, (a.A + 7) >> 3, lane);
+    out_partials<S::RT, RTILES, G4>(red, o, wave % S::NGROUPS, rt0, (a.A + 7) >> 3, lane);
     __syncthreads();
     {
         const int row = tid >> 2;
-        out_reduce<S::NGROUPS, RTILES>(red, row, row < nrows && row < MR ? row_slot[row] : -1,
-                                       tid & 3, a.A, a.b3 + p * a.A, a.logits);
+        out_reduce<S::NGROUPS, RTILES, G4>(red, row,
+                                           row < nrows && row < MR ? row_slot[row] : -1, tid & 3,
+                                           a.A, a.b3 + p * a.A, a.logits);
     }
 }
 
@@ -966,6 +1006,8 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
     a.max_tiles = max_tiles;
     int obs = env_kind == MALIB_ENV_FEATURE ? kObsFeature
               : env_kind == MALIB_ENV_PURSUIT ? kObsPursuit : kObsIter;
+    if (pop.A > (obs == kObsFeature ? kMaxActions : 8))
+        return hipErrorInvalidValue;   // the partial-logit layout holds one group of 8
     switch (pop.hid) {
     case 64: return launch_hid<64>(a, obs, pop.in_pad, tile_rows, blocks, s);
     case 128: return launch_hid<128>(a, obs, pop.in_pad, tile_rows, blocks, s);
