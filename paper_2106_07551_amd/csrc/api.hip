@@ -225,17 +225,15 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
             }
         }
     }
-    size_t acc = sizeof(unsigned long long) * (size_t)P * P;
-    TRY(hipMalloc((void**)&p->sum, acc));
-    TRY(hipMalloc((void**)&p->sumsq, acc));
-    TRY(hipMalloc((void**)&p->cnt, acc));
-    TRY(hipMalloc((void**)&p->dev_flags, sizeof(int)));
-    TRY(hipMalloc((void**)&p->dev_frames, sizeof(unsigned long long)));
-    TRY(hipMemsetAsync(p->sum, 0, acc, s));
-    TRY(hipMemsetAsync(p->sumsq, 0, acc, s));
-    TRY(hipMemsetAsync(p->cnt, 0, acc, s));
-    TRY(hipMemsetAsync(p->dev_flags, 0, sizeof(int), s));
-    TRY(hipMemsetAsync(p->dev_frames, 0, sizeof(unsigned long long), s));
+    const size_t PP = (size_t)P * P, acc_bytes = sizeof(unsigned long long) * (3 * PP + 2);
+    TRY(hipMalloc((void**)&p->acc, acc_bytes));
+    TRY(hipHostMalloc((void**)&p->host_acc, acc_bytes, hipHostMallocDefault));
+    p->sum = p->acc;
+    p->sumsq = p->acc + PP;
+    p->cnt = p->acc + 2 * PP;
+    p->dev_frames = p->acc + 3 * PP;
+    p->dev_flags = reinterpret_cast<int*>(p->acc + 3 * PP + 1);
+    TRY(hipMemsetAsync(p->acc, 0, acc_bytes, s));
     TRY(hipStreamSynchronize(s));
 #undef TRY
     *out = p;
@@ -255,10 +253,10 @@ void malib_pop_destroy(malib_pop_t p)
     }
     if (p->tab)
         (void)hipFree(p->tab);
-    for (void* q : {(void*)p->sum, (void*)p->sumsq, (void*)p->cnt, (void*)p->dev_flags,
-                    (void*)p->dev_frames})
-        if (q)
-            (void)hipFree(q);
+    if (p->acc)
+        (void)hipFree(p->acc);
+    if (p->host_acc)
+        (void)hipHostFree(p->host_acc);
     for (DevBuf* b : {&p->perm, &p->perm_env, &p->tile_info, &p->hist, &p->base, &p->offsets, &p->tile_off, &p->logits,
                       &p->ret, &p->state0, &p->state1, &p->obs, &p->wt, &p->done,
                       &p->thresholds})
@@ -520,16 +518,18 @@ malib_status malib_payoff_eval(malib_pop_t pop, void* stream, int32_t reset, dou
     if (!pop)
         return fail(MALIB_E_INVAL, "pop is NULL");
     hipStream_t s = (hipStream_t)stream;
-    HIP_TRY(hipStreamSynchronize(s));
     const size_t PP = (size_t)pop->P * pop->P;
-    std::vector<long long> sum(PP), sq(PP), cnt(PP);
-    int flags = 0;
-    unsigned long long frames = 0;
-    HIP_TRY(hipMemcpy(sum.data(), pop->sum, 8 * PP, hipMemcpyDeviceToHost));
-    HIP_TRY(hipMemcpy(sq.data(), pop->sumsq, 8 * PP, hipMemcpyDeviceToHost));
-    HIP_TRY(hipMemcpy(cnt.data(), pop->cnt, 8 * PP, hipMemcpyDeviceToHost));
-    HIP_TRY(hipMemcpy(&flags, pop->dev_flags, sizeof(int), hipMemcpyDeviceToHost));
-    HIP_TRY(hipMemcpy(&frames, pop->dev_frames, sizeof(frames), hipMemcpyDeviceToHost));
+    // the whole accumulator block in one copy (stream-ordered after the
+    // batches), into the handle's pinned buffer
+    HIP_TRY(hipMemcpyAsync(pop->host_acc, pop->acc, sizeof(unsigned long long) * (3 * PP + 2),
+                           hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    const long long* sum = reinterpret_cast<const long long*>(pop->host_acc);
+    const long long* sq = sum + PP;
+    const long long* cnt = sum + 2 * PP;
+    const unsigned long long frames = pop->host_acc[3 * PP];
+    int flags;
+    memcpy(&flags, pop->host_acc + 3 * PP + 1, sizeof(int));
     for (size_t i = 0; i < PP; ++i) {
         double n = (double)cnt[i];
         double m = cnt[i] > 0 ? ldexp((double)sum[i], -32) / n : NAN;
@@ -552,23 +552,21 @@ malib_status malib_payoff_eval(malib_pop_t pop, void* stream, int32_t reset, dou
         stats->envs = pop->envs;
         stats->device_flags = flags;
     }
+    // clears are stream-ordered and complete before returning, so the next
+    // batch may run on any stream
     if (reset) {
-        HIP_TRY(hipMemset(pop->sum, 0, 8 * PP));
-        HIP_TRY(hipMemset(pop->sumsq, 0, 8 * PP));
-        HIP_TRY(hipMemset(pop->cnt, 0, 8 * PP));
-        HIP_TRY(hipMemset(pop->dev_frames, 0, sizeof(unsigned long long)));
+        HIP_TRY(hipMemsetAsync(pop->acc, 0, sizeof(unsigned long long) * (3 * PP + 1), s));
         pop->host_frames = 0;
         pop->envs = 0;
     }
-    if (flags) {
-        HIP_TRY(hipMemset(pop->dev_flags, 0, sizeof(int)));
-        HIP_TRY(hipDeviceSynchronize());
+    if (flags)
+        HIP_TRY(hipMemsetAsync(pop->dev_flags, 0, sizeof(int), s));
+    if (reset || flags)
+        HIP_TRY(hipStreamSynchronize(s));
+    if (flags)
         return fail(MALIB_E_DEVICE, "device flagged bad data (flags 0x%x:%s%s)", flags,
                     (flags & kErrPid) ? " policy id out of range" : "",
                     (flags & kErrNaN) ? " NaN logit" : "");
-    }
-    if (reset)
-        HIP_TRY(hipDeviceSynchronize());
     return MALIB_OK;
 }
 

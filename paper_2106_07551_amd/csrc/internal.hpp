@@ -52,12 +52,16 @@ struct Pop {
     void* w[3] = {nullptr, nullptr, nullptr};
     float* b[3] = {nullptr, nullptr, nullptr};  // fp32 [P][out] (zero-filled when absent)
     float* tab = nullptr;                       // fp32 [P][A]
-    // payoff accumulators: [P*P] each
+    // payoff accumulators, one allocation acc[3 P*P + 2] so that the table
+    // comes back in one copy: sum, sumsq, cnt ([P*P] each), the live-frame
+    // counter and the device error flags (the low half of the last word)
+    unsigned long long* acc = nullptr;
     unsigned long long* sum = nullptr;   // int64 fixed point 2^-32 (two's complement)
     unsigned long long* sumsq = nullptr; // int64 fixed point 2^-20
     unsigned long long* cnt = nullptr;
-    int* dev_flags = nullptr;
     unsigned long long* dev_frames = nullptr;
+    int* dev_flags = nullptr;
+    unsigned long long* host_acc = nullptr;   // pinned copy of acc
     int64_t host_frames = 0;   // frames of env families with no early termination
     int64_t envs = 0;
     // scratch, grown on demand

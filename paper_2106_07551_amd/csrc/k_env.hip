@@ -161,7 +161,9 @@ __device__ __forceinline__ uint32_t torus_move(uint32_t cell, int a, int grid)
     return (uint32_t)(y * grid + x);
 }
 
-// One thread per env: both seats' actions (5 each), then simultaneous moves;
+// One thread per slot (lanes 2e and 2e+1: pursuer and evader of env e), all
+// loads issued first: each lane samples its seat's action (5 actions), the
+// pair exchange them, and the pursuer's lane makes the simultaneous moves;
 // capture if the two land on the same cell or swap cells: pursuer +1, evader
 // -1, env done.  Finished envs take no action (logged as 255).  Counts live
 // agent-frames (two per live env) with one atomic per workgroup.
@@ -173,27 +175,34 @@ __global__ __launch_bounds__(256) void step_pursuit_kernel(
     if (threadIdx.x == 0)
         live_s = 0;
     __syncthreads();
-    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    int live = 0;
-    if (e < n && !done[e]) {
-        live = 1;
-        int a0, a1;
-        sample_pair<8>(sa, 5, e, a0, a1);
-        uint32_t p0 = pos[e], e0 = pos[n + e];
-        uint32_t p1 = torus_move(p0, a0, grid);
-        uint32_t e1 = torus_move(e0, a1, grid);
+    const int64_t slot = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t e = slot >> 1;
+    const int seat = (int)(slot & 1);
+    const bool valid = e < n;                 // both lanes of a pair agree
+    const int64_t ec = valid ? e : 0;
+    const bool dn = done[ec] != 0;
+    const uint32_t p0 = pos[ec], q0 = pos[n + ec];
+    bool nan = false;
+    const int a = gumbel_action<8>(sa.logits + (valid ? slot : 0) * 5, 5, sa.seed,
+                                   (uint64_t)(sa.env_offset + ec), sa.t, seat, nan);
+    const int a_other = __shfl_xor(a, 1);
+    const bool live = valid && !dn;
+    if (live && nan)
+        atomicOr(sa.flags, kErrNaN);
+    if (valid && sa.log)
+        sa.log[slot] = live ? (uint8_t)a : (uint8_t)255;
+    if (live && seat == 0) {
+        const uint32_t p1 = torus_move(p0, a, grid);
+        const uint32_t q1 = torus_move(q0, a_other, grid);
         pos[e] = (uint8_t)p1;
-        pos[n + e] = (uint8_t)e1;
-        if (p1 == e1 || (p1 == e0 && e1 == p0)) {
+        pos[n + e] = (uint8_t)q1;
+        if (p1 == q1 || (p1 == q0 && q1 == p0)) {
             done[e] = 1;
             ret[e] = ret[e] + 1.0f;
             ret[n + e] = ret[n + e] + (-1.0f);
         }
-    } else if (e < n && sa.log) {
-        sa.log[2 * e] = 255;
-        sa.log[2 * e + 1] = 255;
     }
-    unsigned long long b = __ballot(live);
+    const unsigned long long b = __ballot(live && seat == 0);
     if ((threadIdx.x & 63) == 0 && b)
         atomicAdd(&live_s, __popcll(b));
     __syncthreads();
@@ -504,8 +513,9 @@ hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_env
     case MALIB_ENV_PURSUIT:
         if (e.A != 5)
             return hipErrorInvalidValue;
-        step_pursuit_kernel<<<blocks, 256, 0, s>>>(e.grid, n_envs, sa, (uint8_t*)state_out, done,
-                                                   ret, frames);
+        // one thread per slot
+        step_pursuit_kernel<<<(int)((2 * n_envs + 255) / 256), 256, 0, s>>>(
+            e.grid, n_envs, sa, (uint8_t*)state_out, done, ret, frames);
         break;
     case MALIB_ENV_FEATURE: {
         const float* si = (const float*)state_in;
