@@ -86,17 +86,36 @@ __global__ __launch_bounds__(1024) void bucket_scan_kernel(
         __syncthreads();
     }
     __syncthreads();
-    if (tid == 0) {
-        int toff = 0;
-        for (int p = 0; p < P; ++p) {
-            int start = base[(int64_t)p * n_chunks];
-            int end = p + 1 < P ? base[(int64_t)(p + 1) * n_chunks] : carry_s;
-            offsets[p] = start;
-            tile_off[p] = toff;
-            toff += (end - start + tile_rows - 1) / tile_rows;
-        }
-        offsets[P] = carry_s;
-        tile_off[P] = toff;
+    // bucket bounds and the first tile of each policy: one thread per policy
+    // (P <= 1024), tiles per policy scanned across the workgroup
+    const int total_rows = carry_s;
+    int start = 0, tiles = 0;
+    if (tid < P) {
+        start = base[(int64_t)tid * n_chunks];
+        const int end = tid + 1 < P ? base[(int64_t)(tid + 1) * n_chunks] : total_rows;
+        tiles = (end - start + tile_rows - 1) / tile_rows;
+    }
+    int x = tiles;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        int y = __shfl_up(x, off, 64);
+        if (lane >= off)
+            x += y;
+    }
+    __syncthreads();   // wsum is reused
+    if (lane == 63)
+        wsum[wave] = x;
+    __syncthreads();
+    int wpre = 0;
+    for (int w = 0; w < wave; ++w)
+        wpre += wsum[w];
+    if (tid < P) {
+        offsets[tid] = start;
+        tile_off[tid] = wpre + x - tiles;
+    }
+    if (tid == P - 1) {
+        offsets[P] = total_rows;
+        tile_off[P] = wpre + x;
     }
 }
 
@@ -132,30 +151,32 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
     __syncthreads();
     const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     for (int seg = 0; seg < kPerWave; seg += 64) {
-        int64_t i = wbase + seg + lane;
-        bool valid = i < n_slots;
+        const int64_t i = wbase + seg + lane;
+        const bool valid = i < n_slots;
         int p = 0;
         if (valid) {
             p = pids[i];
             p = (p < 0 || p >= P) ? 0 : p;
         }
-        bool pending = valid;
-        while (__ballot(pending) != 0ull) {
-            unsigned long long act = __ballot(pending);
-            int leader = __ffsll((unsigned long long)act) - 1;
-            int lp = __shfl(p, leader, 64);
-            bool mine = pending && p == lp;
-            unsigned long long m = __ballot(mine);
-            int dst0 = run[wave][lp];
-            if (mine) {
-                int rank = __popcll(m & lt_mask);
-                perm[dst0 + rank] = (int32_t)i;
-                perm_env[dst0 + rank] = (int32_t)(i / n_agents);
-            }
-            if (lane == leader)
-                run[wave][lp] = dst0 + __popcll(m);
-            if (mine)
-                pending = false;
+        // lanes holding the same policy id: intersect, bit by bit of the id
+        // (P <= 256: 8 bits), the ballot of lanes that agree with this lane
+        unsigned long long same = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const unsigned long long ones = __ballot(valid && ((p >> b) & 1));
+            same &= ((p >> b) & 1) ? ones : ~ones;
+        }
+        // the group's lowest lane takes the group's destination range; the
+        // others rank themselves by lane (slot) order within it
+        const int leader = __ffsll((unsigned long long)same) - 1;
+        int dst0 = 0;
+        if (valid && leader == lane)
+            dst0 = atomicAdd(&run[wave][p], __popcll(same));
+        dst0 = __shfl(dst0, leader < 0 ? 0 : leader, 64);
+        if (valid) {
+            const int rank = __popcll(same & lt_mask);
+            perm[dst0 + rank] = (int32_t)i;
+            perm_env[dst0 + rank] = (int32_t)(i / n_agents);
         }
     }
 }
