@@ -161,10 +161,10 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
         if (desc->kind == MALIB_POLICY_MLP_F32) {
             if (!(hid == 32 || hid == 64))
                 return fail(MALIB_E_UNSUPPORTED, "fp32 MLP hidden width must be 32 or 64");
-            if (in != 24 || A > 3)
+            if (in != 24 || A != 3)
                 return fail(MALIB_E_UNSUPPORTED,
                             "fp32 MLP policies take the iterated-game observation (24 inputs, "
-                            "<= 3 actions)");
+                            "3 actions)");
         } else {
             if (!(hid == 64 || hid == 128 || hid == 256 || hid == 512))
                 return fail(MALIB_E_UNSUPPORTED, "bf16 MLP hidden width must be 64/128/256/512");
@@ -212,9 +212,11 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
             else
                 TRY(hipMemsetAsync(p->b[l], 0, nb, s));
             if (desc->kind == MALIB_POLICY_MLP_F32) {
+                // repacked into the MFMA operand layouts (same size)
                 size_t wb = sizeof(float) * (size_t)P * fo * fi;
                 TRY(hipMalloc(&p->w[l], wb));
-                TRY(hipMemcpyAsync(p->w[l], desc->weights[l], wb, hipMemcpyDeviceToDevice, s));
+                TRY(launch_pack_f32((const float*)desc->weights[l], P, l, hid, A,
+                                    (float*)p->w[l], s));
             } else {
                 int ip = l == 0 ? p->in_pad : round_up(fi, 16);
                 int op = round_up(fo, 32);

@@ -16,7 +16,7 @@ namespace malib {
 constexpr int kMaxP = 256;
 constexpr int kMaxActions = 32;
 constexpr int kMaxAgents = 8;
-constexpr int kF32TileRows = 64;   // rows per fp32 policy tile (one wavefront)
+constexpr int kF32TileRows = 32;   // rows per fp32 policy tile (one wavefront)
 constexpr int kBucketChunk = 2048; // slots per bucketing workgroup
 
 // Growable device buffer owned by a handle.
@@ -133,6 +133,8 @@ hipError_t launch_payoff(const float* ret, const int32_t* pids, int64_t n_envs, 
 // Policy forwards.
 hipError_t launch_pack_bf16(const float* w, int P, int out, int in, int out_pad, int in_pad,
                             int kperm, void* dst, hipStream_t s);
+hipError_t launch_pack_f32(const float* w, int P, int layer, int hid, int A, float* dst,
+                           hipStream_t s);
 hipError_t launch_tabular(const float* tab, const int32_t* pids, int64_t n_slots, int A, int P,
                           int* flags, float* logits, hipStream_t s);
 hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int4* tile_info,

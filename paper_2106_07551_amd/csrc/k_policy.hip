@@ -123,10 +123,33 @@ struct MlpF32Args {
     int P, A, IN, n_agents, max_tiles;
 };
 
-template <int HID, int IN, int AMAX>
+// fp32 MLP of the iterated game on v_mfma_f32_32x32x2_f32: one wavefront per
+// 32-row tile, HID/32 n-tiles (32 rows keep both accumulator sets within 64
+// registers; the weight stream is then 256 bytes per 2 MFMAs, far below the
+// load path).
+//
+// MFMA 32x32x2 layouts: A (32 x 2) lane i holds A[i%32][i/32], B (2 x 32)
+// lane i holds B[i/32][i%32], the accumulator register 4g+q of lane i holds
+// C[8g + 4(i/32) + q][i%32].  So lane i always works on row (slot) i%32 of
+// its row tiles; its half h = i/32 picks which units or inputs it holds.
+//
+//   layer 1: B = the observation, built in place per lane (input 2s+h at
+//            k-step s); A = W1 in natural k order;
+//   layer 2: B = the layer-1 accumulators after ReLU, register r of n-tile nt
+//            at k-step 16nt+r, which holds unit u = 32nt + 8(r/4) + 4h + r%4:
+//            W2 is packed in that k order (pack_f32_kernel), so the hidden
+//            layer never leaves the registers;
+//   layer 3: (A <= 3 logits) on the VALU from the layer-2 accumulators, each
+//            half-wave summing its 16 NT units, the halves added by a shuffle.
+// Sums run in a different order than a plain loop; fp32 policies are compared
+// with a relative tolerance.
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+template <int HID, int AMAX>
 __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
 {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    constexpr int NT = HID / 32, RT = 1, K1 = 12, K2 = HID / 2, DEPTH = 4;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5, nn = lane & 31;
     const int t = blockIdx.x * 4 + wave;
     if (t >= a.max_tiles)
         return;
@@ -135,56 +158,174 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
     if (p < 0)
         return;
     const int r0 = __builtin_amdgcn_readfirstlane(ti.y);
-    // (tiles of kF32TileRows = 64 rows: one row per lane)
     const int r1 = r0 + __builtin_amdgcn_readfirstlane(ti.z);
-    const int row = r0 + lane;
-    const bool valid = row < r1;
-    const int slot = a.perm[valid ? row : r0];
-    const int env = slot / a.n_agents, seat = slot - env * a.n_agents;
-    const uint32_t hist = a.hist[env];
 
-    const float* W1 = a.w1 + (int64_t)p * HID * IN;
+    int slot[RT];
+    bool valid[RT];
+    float xb[RT][K1];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+        const int row = r0 + 32 * rt + nn;
+        valid[rt] = row < r1;
+        slot[rt] = a.perm[valid[rt] ? row : r0];
+        const int env = slot[rt] / a.n_agents, seat = slot[rt] - env * a.n_agents;
+        const uint32_t hist = a.hist[env];
+        // 24 inputs: 3 actions (constant divisors in iter_obs)
+#pragma unroll
+        for (int s = 0; s < K1; ++s)
+            xb[rt][s] = iter_obs(hist, seat, 3, 2 * s + h);
+    }
+    const float* W1 = a.w1 + (int64_t)p * HID * 24;
+    float w1[NT][K1];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int s = 0; s < K1; ++s)
+            w1[nt][s] = W1[(nt * K1 + s) * 64 + lane];
+
+    // accumulators start from the bias of their units (32nt + 8g + 4h + q)
+    auto bias16 = [&](const float* b, int nt) {
+        f32x16_t v;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const float4 x = *reinterpret_cast<const float4*>(b + p * HID + 32 * nt + 8 * g + 4 * h);
+            v[4 * g + 0] = x.x;
+            v[4 * g + 1] = x.y;
+            v[4 * g + 2] = x.z;
+            v[4 * g + 3] = x.w;
+        }
+        return v;
+    };
+    f32x16_t acc[NT][RT], acc2[NT][RT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+            acc[nt][rt] = bias16(a.b1, nt);
+    // ---- layer 1
+#pragma unroll
+    for (int s = 0; s < K1; ++s)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+                acc[nt][rt] = __builtin_amdgcn_mfma_f32_32x32x2f32(w1[nt][s], xb[rt][s],
+                                                                   acc[nt][rt], 0, 0, 0);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[nt][rt][r] = acc[nt][rt][r] > 0.0f ? acc[nt][rt][r] : 0.0f;
+    // ---- layer 2 (k-step s2 = 16 nt + r takes register r of n-tile nt); the
+    // weights stream through a ring DEPTH k-steps ahead
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+            acc2[nt][rt] = bias16(a.b2, nt);
     const float* W2 = a.w2 + (int64_t)p * HID * HID;
+    float ring[DEPTH][NT];
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d)
+#pragma unroll
+        for (int ont = 0; ont < NT; ++ont)
+            ring[d][ont] = W2[(ont * K2 + d) * 64 + lane];
+#pragma unroll
+    for (int s2 = 0; s2 < K2; ++s2) {
+#pragma unroll
+        for (int ont = 0; ont < NT; ++ont)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+                acc2[ont][rt] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                    ring[s2 % DEPTH][ont], acc[s2 / 16][rt][s2 % 16], acc2[ont][rt], 0, 0, 0);
+        if (s2 + DEPTH < K2) {
+#pragma unroll
+            for (int ont = 0; ont < NT; ++ont)
+                ring[s2 % DEPTH][ont] = W2[(ont * K2 + s2 + DEPTH) * 64 + lane];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // ---- layer 3: W3 packed per (action, n-tile, half) as 16 floats
     const float* W3 = a.w3 + (int64_t)p * a.A * HID;
-    const float* B1 = a.b1 + p * HID;
-    const float* B2 = a.b2 + p * HID;
-    const float* B3 = a.b3 + p * a.A;
-
-    float x[IN];
 #pragma unroll
-    for (int c = 0; c < IN; ++c)
-        x[c] = iter_obs(hist, seat, a.A, c);
-    float h1[HID];
+    for (int o = 0; o < AMAX; ++o) {
+        if (o < a.A) {
+            float w3[NT][16];
 #pragma unroll
-    for (int j = 0; j < HID; ++j) {
-        float acc = B1[j];
+            for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int c = 0; c < IN; ++c)
-            acc = __builtin_fmaf(W1[j * IN + c], x[c], acc);
-        h1[j] = acc > 0.0f ? acc : 0.0f;
-    }
-    float h2[HID];
+                for (int g = 0; g < 4; ++g) {
+                    const float4 v =
+                        *reinterpret_cast<const float4*>(W3 + ((o * NT + nt) * 2 + h) * 16 + 4 * g);
+                    w3[nt][4 * g + 0] = v.x;
+                    w3[nt][4 * g + 1] = v.y;
+                    w3[nt][4 * g + 2] = v.z;
+                    w3[nt][4 * g + 3] = v.w;
+                }
+            const float bo = a.b3[p * a.A + o];
 #pragma unroll
-    for (int j = 0; j < HID; ++j) {
-        float acc = B2[j];
+            for (int rt = 0; rt < RT; ++rt) {
+                float part = 0.0f;
 #pragma unroll
-        for (int k = 0; k < HID; ++k)
-            acc = __builtin_fmaf(W2[j * HID + k], h1[k], acc);
-        h2[j] = acc > 0.0f ? acc : 0.0f;
-    }
-    if (valid) {
-        float* out = a.logits + (int64_t)slot * a.A;
+                for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int o = 0; o < AMAX; ++o) {
-            if (o < a.A) {
-                float acc = B3[o];
-#pragma unroll
-                for (int k = 0; k < HID; ++k)
-                    acc = __builtin_fmaf(W3[o * HID + k], h2[k], acc);
-                out[o] = acc;
+                    for (int r = 0; r < 16; ++r) {
+                        const float v = acc2[nt][rt][r];
+                        part = __builtin_fmaf(w3[nt][r], v > 0.0f ? v : 0.0f, part);
+                    }
+                const float tot = part + __shfl_xor(part, 32);
+                if (h == 0 && valid[rt])
+                    a.logits[(int64_t)slot[rt] * a.A + o] = bo + tot;
             }
         }
     }
+}
+
+// fp32 weights [P][out][in] -> the MFMA operand layouts of mlp_f32_kernel:
+//   layer 0: [P][nt][s][lane] = W1[32nt + lane%32][2s + lane/32]        (s < 12)
+//   layer 1: [P][ont][s][lane] = W2[32ont + lane%32][u(s, lane/32)]     (s < HID/2)
+//            with u(s, h) = 32(s/16) + 8((s%16)/4) + 4h + s%4
+//   layer 2: [P][o][nt][h][r] = W3[o][32nt + 8(r/4) + 4h + r%4]
+__global__ void pack_f32_kernel(const float* __restrict__ w, int P, int layer, int hid, int A,
+                                float* __restrict__ dst)
+{
+    const int per = layer == 0 ? hid * 24 : layer == 1 ? hid * hid : A * hid;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)P * per)
+        return;
+    const int p = (int)(i / per), e = (int)(i - (int64_t)p * per);
+    int out, in, in_dim;
+    if (layer == 0) {
+        const int lane = e % 64, s = (e / 64) % 12, nt = e / (64 * 12);
+        out = 32 * nt + lane % 32;
+        in = 2 * s + lane / 32;
+        in_dim = 24;
+    } else if (layer == 1) {
+        const int K2 = hid / 2;
+        const int lane = e % 64, s = (e / 64) % K2, ont = e / (64 * K2);
+        const int hh = lane / 32, r = s % 16;
+        out = 32 * ont + lane % 32;
+        in = 32 * (s / 16) + 8 * (r / 4) + 4 * hh + r % 4;
+        in_dim = hid;
+    } else {
+        const int NT = hid / 32;
+        const int r = e % 16, hh = (e / 16) % 2, nt = (e / 32) % NT, o = e / (32 * NT);
+        out = o;
+        in = 32 * nt + 8 * (r / 4) + 4 * hh + r % 4;
+        in_dim = hid;
+    }
+    dst[i] = w[(int64_t)p * per + (int64_t)out * in_dim + in];
+}
+
+hipError_t launch_pack_f32(const float* w, int P, int layer, int hid, int A, float* dst,
+                           hipStream_t s)
+{
+    const int per = layer == 0 ? hid * 24 : layer == 1 ? hid * hid : A * hid;
+    const int64_t total = (int64_t)P * per;
+    pack_f32_kernel<<<(int)((total + 255) / 256), 256, 0, s>>>(w, P, layer, hid, A, dst);
+    return hipGetLastError();
 }
 
 hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int4* tile_info,
@@ -212,12 +353,12 @@ hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int4* tile_
     const int max_tiles = max_tiles_for(n_slots, pop.P, kF32TileRows);
     a.max_tiles = max_tiles;
     int blocks = (max_tiles + 3) / 4;
-    if (pop.in_dim != 24 || pop.A > 3)
-        return hipErrorInvalidValue;
+    if (pop.in_dim != 24 || pop.A != 3)
+        return hipErrorInvalidValue;   // the iterated game: 3 actions, 8 x 3 inputs
     if (pop.hid == 32)
-        mlp_f32_kernel<32, 24, 3><<<blocks, 256, 0, s>>>(a);
+        mlp_f32_kernel<32, 3><<<blocks, 256, 0, s>>>(a);
     else if (pop.hid == 64)
-        mlp_f32_kernel<64, 24, 3><<<blocks, 256, 0, s>>>(a);
+        mlp_f32_kernel<64, 3><<<blocks, 256, 0, s>>>(a);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
