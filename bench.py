@@ -30,6 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_F32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0
 NAME_TO_C = {"matrix": 1, "iter": 2, "pursuit": 3, "feature": 4, "team": 5}
 
@@ -251,14 +252,19 @@ def main():
     ms_step = 1000.0 * el / args.steps
     value = frames / el
     roof = None
-    if wl.pol_kind == W.MLP_BF16:
+    if wl.pol_kind in (W.MLP_BF16, W.MLP_F32):
+        # the grouped policy forward on MFMA: bf16 operands (fp32 accumulation)
+        # or fp32 throughout (iterated game), each against its own dense peak
+        bf16 = wl.pol_kind == W.MLP_BF16
+        peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_MFMA_TFLOPS
+        kname = policy_kernel(wl) if bf16 else "mlp_f32_kernel"
         flops = policy_flops_per_frame(wl.dims) * n * na        # per launch
         avg_s = policy_avg_us * 1e-6
         ach = flops / avg_s / 1e12
         traffic, src = profiled_traffic(wl.name)
-        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic, "kernel": "grouped policy forward (" + policy_kernel(wl) + ")",
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                "traffic": traffic, "kernel": "grouped policy forward (" + kname + ")",
                 "flops_per_launch": flops, "avg_launch_us": round(policy_avg_us, 3),
                 "timed_launches": policy_timed}
         if traffic is not None:
