@@ -304,8 +304,13 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     constexpr int WS_FLOATS = kFeatKC * D > kFeatEnvs * SLD ? kFeatKC * D : kFeatEnvs * SLD;
     __shared__ __attribute__((aligned(16))) float Ws[WS_FLOATS];
     __shared__ __attribute__((aligned(16))) float Ss[kFeatKC * SSTR];
+    // the reward weights u, staged once: the chain then reads both of its
+    // operands from LDS (in-order returns, so its loads can run ahead)
+    __shared__ __attribute__((aligned(16))) float Us[D];
     const int tid = threadIdx.x, tx = tid & 63, ty = tid >> 6;
     const int64_t e0 = (int64_t)blockIdx.x * kFeatEnvs;
+    for (int k = tid; k < D; k += kFeatThreads)   // read after the main loop's barriers
+        Us[k] = u[k];
 
     // Staging: chunk c0 of WT (KC x D floats, c-major) and of the state (32 envs
     // x KC) goes global -> registers -> LDS; the loads of chunk c0+KC are issued
@@ -478,6 +483,7 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     if (rlane) {
         float r = 0.0f;
         const float* row = Sl + tid * SLD;
+        const float* u = Us;
 #pragma unroll
         for (int k = 0; k < D; ++k)
             r = __builtin_fmaf(u[k], row[k], r);
