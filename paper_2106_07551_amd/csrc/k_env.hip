@@ -470,8 +470,8 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     }
     // reward chain of the workgroup's envs (one lane each); the seats' running
     // returns are fetched before the chain so their latency overlaps it, and
-    // the chain is unrolled so that its LDS and scalar loads run ahead of the
-    // dependent FMAs
+    // the chain is unrolled so that its LDS loads run ahead of the dependent
+    // FMAs
     const int64_t er = e0 + tid;
     const bool rlane = tid < kFeatEnvs && er < n;
     float rv[kMaxAgents];
