@@ -148,7 +148,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 template <int HID, int AMAX>
 __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
 {
-    constexpr int NT = HID / 32, RT = 1, K1 = 12, K2 = HID / 2, DEPTH = 4;
+    constexpr int NT = HID / 32, RT = 1, K1 = 12, K2 = HID / 2;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, h = lane >> 5, nn = lane & 31;
     const int t = blockIdx.x * 4 + wave;
     if (t >= a.max_tiles)
@@ -175,13 +175,19 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
         for (int s = 0; s < K1; ++s)
             xb[rt][s] = iter_obs(hist, seat, 3, 2 * s + h);
     }
+    // each lane's A operands are contiguous in the packed weights (16-byte loads)
     const float* W1 = a.w1 + (int64_t)p * HID * 24;
     float w1[NT][K1];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int s = 0; s < K1; ++s)
-            w1[nt][s] = W1[(nt * K1 + s) * 64 + lane];
+        for (int s4 = 0; s4 < K1 / 4; ++s4) {
+            const float4 v = *reinterpret_cast<const float4*>(W1 + (nt * 64 + lane) * K1 + 4 * s4);
+            w1[nt][4 * s4 + 0] = v.x;
+            w1[nt][4 * s4 + 1] = v.y;
+            w1[nt][4 * s4 + 2] = v.z;
+            w1[nt][4 * s4 + 3] = v.w;
+        }
 
     // accumulators start from the bias of their units (32nt + 8g + 4h + q)
     auto bias16 = [&](const float* b, int nt) {
@@ -225,25 +231,36 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
             acc2[nt][rt] = bias16(a.b2, nt);
+    // A operands in groups of 4 k-steps (one 16-byte load per n-tile), the next
+    // group loaded while the current one is used (a deeper ring measured slower)
     const float* W2 = a.w2 + (int64_t)p * HID * HID;
-    float ring[DEPTH][NT];
+    constexpr int QDEPTH = 1, KQ = K2 / 4;
+    float4 ring[QDEPTH][NT];
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d)
-#pragma unroll
-        for (int ont = 0; ont < NT; ++ont)
-            ring[d][ont] = W2[(ont * K2 + d) * 64 + lane];
-#pragma unroll
-    for (int s2 = 0; s2 < K2; ++s2) {
+    for (int d = 0; d < QDEPTH; ++d)
 #pragma unroll
         for (int ont = 0; ont < NT; ++ont)
+            ring[d][ont] = *reinterpret_cast<const float4*>(W2 + (ont * 64 + lane) * K2 + 4 * d);
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-                acc2[ont][rt] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                    ring[s2 % DEPTH][ont], acc[s2 / 16][rt][s2 % 16], acc2[ont][rt], 0, 0, 0);
-        if (s2 + DEPTH < K2) {
+    for (int sq = 0; sq < KQ; ++sq) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int s2 = 4 * sq + j;
+#pragma unroll
+            for (int ont = 0; ont < NT; ++ont) {
+                const float4 g4 = ring[sq % QDEPTH][ont];
+                const float wv = j == 0 ? g4.x : j == 1 ? g4.y : j == 2 ? g4.z : g4.w;
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+                    acc2[ont][rt] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                        wv, acc[s2 / 16][rt][s2 % 16], acc2[ont][rt], 0, 0, 0);
+            }
+        }
+        if (sq + QDEPTH < KQ) {
 #pragma unroll
             for (int ont = 0; ont < NT; ++ont)
-                ring[s2 % DEPTH][ont] = W2[(ont * K2 + s2 + DEPTH) * 64 + lane];
+                ring[sq % QDEPTH][ont] = *reinterpret_cast<const float4*>(
+                    W2 + (ont * 64 + lane) * K2 + 4 * (sq + QDEPTH));
         }
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -284,8 +301,9 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
 }
 
 // fp32 weights [P][out][in] -> the MFMA operand layouts of mlp_f32_kernel:
-//   layer 0: [P][nt][s][lane] = W1[32nt + lane%32][2s + lane/32]        (s < 12)
-//   layer 1: [P][ont][s][lane] = W2[32ont + lane%32][u(s, lane/32)]     (s < HID/2)
+//   layer 0: [P][nt][lane][s] = W1[32nt + lane%32][2s + lane/32]        (s < 12)
+//   layer 1: [P][ont][lane][s] = W2[32ont + lane%32][u(s, lane/32)]     (s < HID/2)
+// (a lane's operands of consecutive k-steps are contiguous)
 //            with u(s, h) = 32(s/16) + 8((s%16)/4) + 4h + s%4
 //   layer 2: [P][o][nt][h][r] = W3[o][32nt + 8(r/4) + 4h + r%4]
 __global__ void pack_f32_kernel(const float* __restrict__ w, int P, int layer, int hid, int A,
@@ -298,13 +316,13 @@ __global__ void pack_f32_kernel(const float* __restrict__ w, int P, int layer, i
     const int p = (int)(i / per), e = (int)(i - (int64_t)p * per);
     int out, in, in_dim;
     if (layer == 0) {
-        const int lane = e % 64, s = (e / 64) % 12, nt = e / (64 * 12);
+        const int s = e % 12, lane = (e / 12) % 64, nt = e / (64 * 12);
         out = 32 * nt + lane % 32;
         in = 2 * s + lane / 32;
         in_dim = 24;
     } else if (layer == 1) {
         const int K2 = hid / 2;
-        const int lane = e % 64, s = (e / 64) % K2, ont = e / (64 * K2);
+        const int s = e % K2, lane = (e / K2) % 64, ont = e / (64 * K2);
         const int hh = lane / 32, r = s % 16;
         out = 32 * ont + lane % 32;
         in = 32 * (s / 16) + 8 * (r / 4) + 4 * hh + r % 4;
