@@ -140,7 +140,7 @@ def test_parity_matrix_full():
 
 def test_parity_iter_ragged():
     """Iterated game, fp32 MLP: 4 policies x 50 envs per pair (400 rows per
-    policy = 6 full 64-row tiles + a ragged one), horizon 32."""
+    policy = 12 full 32-row tiles + a ragged one), horizon 32."""
     wl = W.make(2, P=4, per_pair=50)
     g = run_gpu(wl, snaps=[0, 1, 5, 31])
     check_parity(wl, g)
@@ -366,3 +366,54 @@ def test_host_validation_errors():
         M.Population(M.POLICY_MLP_BF16, 2, 18, dims=[512, 500, 500, 18],
                      weights=[torch.zeros(1, device="cuda")] * 3)
     pop.close()
+
+
+# ------------------------------------------------------------ nonzero biases
+# The generated populations have zero biases; these cases give every layer a
+# random fp32 bias, so that the bias-to-unit mapping of each policy kernel
+# (accumulator layout, output reduction) is compared with the oracle.
+def _with_biases(wl, seed, scale=0.3):
+    rng = np.random.default_rng([2106, 7551, 77, seed])
+    wl.biases = [rng.normal(0.0, scale, b.shape).astype(np.float32) for b in wl.biases]
+    return wl
+
+
+def _with_dims(wl, dims, seed):
+    """Fresh fp32 weights of the given widths (iterated game)."""
+    rng = np.random.default_rng([2106, 7551, 78, seed])
+    wl.dims = dims
+    wl.weights, wl.biases = W._mlp(rng, wl.P, dims, bf16=wl.pol_kind == W.MLP_BF16)
+    return wl
+
+
+@pytest.mark.parametrize("hid", [32, 64])
+def test_parity_iter_biases_hidden_widths(hid):
+    """fp32 MFMA kernel, both hidden widths, nonzero biases: 3 policies x 37
+    envs per pair (111 rows per policy: three 32-row tiles + a ragged one)."""
+    wl = _with_biases(_with_dims(W.make(2, P=3, per_pair=37), [24, hid, hid, 3], hid), hid)
+    g = run_gpu(wl, snaps=[0, 7, 31])
+    check_parity(wl, g)
+
+
+def test_parity_team_biases():
+    """64-row bf16 kernel on feature observations (4v4, d=256), nonzero biases."""
+    wl = _with_biases(W.team_variant(8, d=256, P=4, n_envs=48, horizon=4,
+                                     dims=[256, 512, 512, 18]), 5)
+    g = run_gpu(wl, snaps=[0, 3])
+    check_parity(wl, g)
+
+
+def test_parity_pursuit_biases():
+    """64-row bf16 kernel on the pursuit window (one partial-logit group),
+    nonzero biases."""
+    wl = _with_biases(W.make(3, n_envs=300, horizon=30), 3)
+    g = run_gpu(wl, snaps=[0, 10, 29])
+    check_parity(wl, g)
+
+
+def test_parity_persistent_biases():
+    """Persistent d=512 kernel, nonzero biases: 2 policies x 320 slots."""
+    wl = _with_biases(W.team_variant(4, d=512, P=2, n_envs=160, horizon=3,
+                                     dims=[512, 512, 512, 18]), 4)
+    g = run_gpu(wl, snaps=[0, 2])
+    check_parity(wl, g)
