@@ -505,10 +505,13 @@ static void reset_env(const ora_config* c, int64_t g, env_state* st)
     st->done = 0;
     int64_t gr = c->init_mode == 1 ? 0 : g;
     if (c->env_kind == ENV_PURSUIT) {
-        int cells = c->grid * c->grid;  /* 64 */
+        /* G x G torus: pursuer floor(lane0 * G^2 / 2^32) (the top 6 bits of
+         * lane 0 when G = 8), evader pursuer + 1 + floor(lane1 * (G^2 - 1) / 2^32)
+         * mod G^2, so the two start on distinct cells */
+        int cells = c->grid * c->grid;
         uint32_t x0 = lane_of(c->seed, gr, 0, PURPOSE_RESET, 0, 0, 0);
         uint32_t x1 = lane_of(c->seed, gr, 0, PURPOSE_RESET, 0, 0, 1);
-        st->pc = (int)(x0 >> 26);
+        st->pc = (int)(((uint64_t)x0 * (uint64_t)cells) >> 32);
         uint32_t shift = (uint32_t)(((uint64_t)x1 * (uint64_t)(cells - 1)) >> 32);
         st->ec = (int)((st->pc + 1 + shift) % (uint32_t)cells);
     } else if (c->env_kind == ENV_FEATURE) {

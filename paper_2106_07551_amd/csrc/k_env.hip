@@ -21,8 +21,9 @@ __global__ void reset_iter_kernel(uint16_t* __restrict__ hist, int64_t n)
         hist[e] = 0xFFFF;
 }
 
-// Pursuer cell = top 6 bits of lane 0; evader = pursuer + 1 + floor(lane1 *
-// 63 / 2^32) mod 64, so the two never start on the same cell.
+// G x G torus: pursuer cell = floor(lane0 * G^2 / 2^32) (the top 6 bits of
+// lane 0 when G = 8); evader = pursuer + 1 + floor(lane1 * (G^2 - 1) / 2^32)
+// mod G^2, so the two never start on the same cell.
 __global__ void reset_pursuit_kernel(uint8_t* __restrict__ pos, uint8_t* __restrict__ done,
                                      int64_t n, int grid, uint64_t seed, int64_t env_offset,
                                      int shared)
@@ -34,7 +35,7 @@ __global__ void reset_pursuit_kernel(uint8_t* __restrict__ pos, uint8_t* __restr
     u64x4 b = stream_block(seed, g, 0, kPurposeReset, 0, 0);
     uint32_t x0 = (uint32_t)b.x, x1 = (uint32_t)(b.x >> 32);
     uint32_t cells = (uint32_t)(grid * grid);
-    uint32_t pc = x0 >> 26;
+    uint32_t pc = (uint32_t)(((uint64_t)x0 * (uint64_t)cells) >> 32);
     uint32_t shift = (uint32_t)(((uint64_t)x1 * (uint64_t)(cells - 1)) >> 32);
     uint32_t ec = (pc + 1 + shift) % cells;
     pos[e] = (uint8_t)pc;

@@ -417,3 +417,13 @@ def test_parity_persistent_biases():
                                      dims=[512, 512, 512, 18]), 4)
     g = run_gpu(wl, snaps=[0, 2])
     check_parity(wl, g)
+
+
+@pytest.mark.parametrize("grid", [5, 13])
+def test_parity_pursuit_other_grids(grid):
+    """Pursuit on a 5x5 and a 13x13 torus (reset cells, moves, captures and the
+    window's wrap-around off the 8x8 case)."""
+    wl = W.make(3, n_envs=256, horizon=40)
+    wl.grid = grid
+    g = run_gpu(wl, snaps=[0, 9, 39])
+    check_parity(wl, g)

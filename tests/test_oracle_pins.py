@@ -417,6 +417,27 @@ def test_pursuit_reset_distinct_uniform():
     assert st.chisquare(np.bincount(ecs, minlength=64)).pvalue > 1e-4
 
 
+@pytest.mark.parametrize("grid", [5, 8, 11, 16])
+def test_pursuit_reset_any_grid(grid):
+    """The reset cells on a G x G torus against lanes 0 and 1 of the reset block
+    drawn with numpy's Philox (independent of the oracle's generator): pursuer
+    floor(lane0 G^2 / 2^32), which is lane0 >> 26 for G = 8; evader pursuer + 1
+    + floor(lane1 (G^2 - 1) / 2^32) mod G^2."""
+    seed, cells = W.make(3).seed, grid * grid
+    for g in range(1, 400):
+        # the block of counter (g, 0, 1 << 32, 0) is numpy's first draw from (g - 1, ...)
+        gen = np.random.Philox(key=np.array([seed, 0], np.uint64),
+                               counter=np.array([g - 1, 0, 1 << 32, 0], np.uint64))
+        w0 = int(gen.random_raw(4)[0])
+        lane0, lane1 = w0 & 0xFFFFFFFF, w0 >> 32
+        pc, ec = oracle.pursuit_reset(seed, g, grid)
+        assert pc == (lane0 * cells) >> 32
+        if grid == 8:
+            assert pc == lane0 >> 26
+        assert ec == (pc + 1 + ((lane1 * (cells - 1)) >> 32)) % cells
+        assert 0 <= pc < cells and 0 <= ec < cells and pc != ec
+
+
 def test_pursuit_one_step_brute_force():
     """E[G_0] of a horizon-1 episode: average over the 64*63 distinct starts of
     sum_{a0,a1} pi_i(a0) pi_j(a1) [capture]; vs 16384 sampled episodes."""
