@@ -427,3 +427,17 @@ def test_parity_pursuit_other_grids(grid):
     wl.grid = grid
     g = run_gpu(wl, snaps=[0, 9, 39])
     check_parity(wl, g)
+
+
+@pytest.mark.parametrize("n_actions", [11, 20, 32])
+def test_parity_matrix_many_actions(n_actions):
+    """One-step matrix game with 11, 20 and 32 actions (tabular policies): the
+    sampling's two-, three- and four-block Philox cases inside the env step."""
+    rng = np.random.default_rng([2106, 7551, 79, n_actions])
+    wl = W.make(1, P=3, per_pair=300)
+    a = rng.uniform(-1.0, 1.0, (n_actions, n_actions)).astype(np.float32)
+    wl.A = np.triu(a, 1) - np.triu(a, 1).T
+    wl.n_actions = n_actions
+    wl.tab_logits = rng.normal(0.0, 1.0, (wl.P, n_actions)).astype(np.float32)
+    g = run_gpu(wl, snaps=[0])
+    check_parity(wl, g)
