@@ -64,15 +64,15 @@ enum {
 };
 
 /*
- * A population of P policies shared by every seat (a policy pool, Sec. 3.1:
- * "some of them can share the same policy pool").  MLP policies have two
+ * A population of P policies shared by every seat (a policy pool that the
+ * agents draw from, Sec. 3.1).  MLP policies have two
  * hidden ReLU layers: logits = W3 relu(W2 relu(W1 x + b1) + b2) + b3, with the
  * weight of layer l laid out [P][dims[l+1]][dims[l]] (row = output unit).
  *
  * Supported shapes:
  *  - TABULAR: n_layers = 0, tab_logits device fp32 [P][n_actions].
- *  - MLP_F32: n_layers = 3, dims = {24, h, h, A} with h in {32, 64}, A <= 3;
- *    used with the iterated matrix game (in = 8 * n_actions).
+ *  - MLP_F32: n_layers = 3, dims = {24, h, h, 3} with h in {32, 64}: the
+ *    iterated matrix game's observation (in = 8 * n_actions) and actions.
  *  - MLP_BF16: n_layers = 3, dims = {in, h, h, A} with 1 <= in <= 512,
  *    h in {64, 128, 256, 512}, A <= 32.  fp32 weights are rounded to bf16
  *    (nearest, ties to even) when the handle is created.
