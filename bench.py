@@ -233,13 +233,17 @@ def main():
     pop.profile_enable(True)
     one_step()
     work = algorithmic_work(wl)
+    # per step for the policy forward and the env step, per fill for set-up
+    # and payoff
     for name, k in (("policy", M.K_POLICY), ("env", M.K_ENV), ("setup", M.K_SETUP),
                     ("payoff", M.K_PAYOFF)):
         ms, cnt = pop.profile_read(k)
+        per = wl.horizon if name in ("policy", "env") else 1
         kern[name] = {"total_ms": round(ms, 3), "launches": cnt,
-                      "avg_us": round(1000.0 * ms / max(cnt, 1), 3)}
+                      "avg_us": round(1000.0 * ms / max(cnt, 1), 3),
+                      "per_step_us" if per > 1 else "per_fill_us": round(1000.0 * ms / per, 3)}
         if name in work and cnt:
-            t = ms * 1e-3 / cnt
+            t = ms * 1e-3 / per
             w = work[name]
             kern[name]["alg_bytes"] = w["bytes"]
             kern[name]["hbm_GBps"] = round(w["bytes"] / t / 1e9, 1)
