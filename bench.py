@@ -162,6 +162,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="team", choices=sorted(NAME_TO_C))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--event-every", type=int, default=0, metavar="K",
+                    help="time one grouped-forward launch in K with HIP events during the "
+                         "timed fills (default: about 16 per fill, at least every 4th)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the "
                          "reference kernel for scaling HBM byte counters) and exit")
@@ -211,9 +214,11 @@ def main():
         one_step()
     torch.cuda.synchronize()
 
-    # timed region: HIP events around one grouped-forward launch in four (the
-    # events' own cost would otherwise show up in the fill time)
-    pop.profile_enable(True, kernels=[M.K_POLICY], every=4)
+    # timed region: HIP events around one grouped-forward launch in `every`
+    # (about 16 per fill): the events' own cost shows up in the fill time, by
+    # ~1% on the 4v4 game and ~2% on pursuit at one launch in four
+    every = args.event_every or max(4, wl.horizon // 16)
+    pop.profile_enable(True, kernels=[M.K_POLICY], every=every)
     frames = 0
     torch.cuda.synchronize()
     t0 = time.perf_counter()
