@@ -86,6 +86,9 @@ def lib():
         L.ora_meta_sample.restype = C.c_int
         L.ora_meta_sample.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int64,
                                       C.c_int32, C.c_uint64, C.c_int64, C.c_void_p]
+        L.ora_solve_fp.restype = C.c_int
+        L.ora_solve_fp.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                                   C.c_void_p]
         L.ora_rollout.restype = C.c_int
         L.ora_rollout.argtypes = [C.POINTER(Config), C.c_int64, C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_double, C.c_void_p, C.c_void_p,
@@ -203,6 +206,29 @@ def meta_sample(sigma, P, n_envs, n_agents, seed, env_offset=0):
     if rc != 0:
         raise ValueError(f"ora_meta_sample rejected its input ({rc})")
     return out
+
+
+def solve_fp(M, T):
+    """Simultaneous fictitious play on the zero-sum game with row payoff M
+    (P x P, fp64; the column side receives -M) for T iterations (oracle.c,
+    ora_solve_fp).  Returns (cx, cy, gap): the play counts of the row and
+    column side (int32) and the exploitability of the average strategies."""
+    m = np.ascontiguousarray(M, dtype=np.float64)
+    P = m.shape[0]
+    assert m.shape == (P, P)
+    cx = np.zeros(P, np.int32)
+    cy = np.zeros(P, np.int32)
+    gap = np.zeros(1, np.float64)
+    rc = lib().ora_solve_fp(_ptr(m), P, int(T), _ptr(cx), _ptr(cy), _ptr(gap))
+    if rc != 0:
+        raise ValueError(f"ora_solve_fp rejected its input ({rc})")
+    return cx, cy, float(gap[0])
+
+
+def payoff_matrix(mean):
+    """The solver's game from a payoff table: the means, 0 where a cell has no
+    simulations."""
+    return np.where(np.isnan(mean), 0.0, mean)
 
 
 # ---------------------------------------------------------------- configuration

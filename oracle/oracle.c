@@ -297,6 +297,62 @@ int ora_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, int64_t n_en
 }
 
 /* ------------------------------------------------------------------------ */
+/* Meta-solver on the payoff table: the meta-update Comb_{t+1} ~ G(...) of    */
+/* Sec. 3.1 with a fictitious-play solver (the FP meta-solver of the PSRO     */
+/* experiments, Sec. 5; get_equilibrium of the example API, Appendix C.2).    */
+/* The table is a two-player zero-sum game: the row side receives M[i][j],   */
+/* the column side -M[i][j].  Simultaneous fictitious play: at iteration t   */
+/* each side best-responds to the other's empirical play so far,             */
+/*   i_t = first argmax_i v_i,  v = sum over s < t of M[:, j_s],             */
+/*   j_t = first argmin_j w_j,  w = sum over s < t of M[i_s, :],             */
+/* (fp64, one column / row added per iteration in iteration order), then     */
+/* both play counts are incremented.  The average strategies are cx/T and    */
+/* cy/T; gap = (max_i v_i - min_j w_j) / T after the last update is their    */
+/* exploitability (the sum of both sides' best-response gains).  M must be   */
+/* finite.                                                                   */
+/* ------------------------------------------------------------------------ */
+int ora_solve_fp(const double* M, int32_t P, int32_t T, int32_t* cx, int32_t* cy, double* gap)
+{
+    if (P <= 0 || T <= 0)
+        return -1;
+    double* v = (double*)calloc((size_t)P, sizeof(double));
+    double* w = (double*)calloc((size_t)P, sizeof(double));
+    if (!v || !w) {
+        free(v);
+        free(w);
+        return -2;
+    }
+    memset(cx, 0, sizeof(int32_t) * (size_t)P);
+    memset(cy, 0, sizeof(int32_t) * (size_t)P);
+    for (int32_t t = 0; t < T; ++t) {
+        int i = 0, j = 0;
+        for (int k = 1; k < P; ++k) {
+            if (v[k] > v[i])
+                i = k;
+            if (w[k] < w[j])
+                j = k;
+        }
+        cx[i] += 1;
+        cy[j] += 1;
+        for (int k = 0; k < P; ++k) {
+            v[k] = v[k] + M[(size_t)k * P + j];
+            w[k] = w[k] + M[(size_t)i * P + k];
+        }
+    }
+    double vmax = v[0], wmin = w[0];
+    for (int k = 1; k < P; ++k) {
+        if (v[k] > vmax)
+            vmax = v[k];
+        if (w[k] < wmin)
+            wmin = w[k];
+    }
+    *gap = (vmax - wmin) / (double)T;
+    free(v);
+    free(w);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Configuration                                                             */
 /* ------------------------------------------------------------------------ */
 enum { ENV_MATRIX = 0, ENV_ITER = 1, ENV_PURSUIT = 2, ENV_FEATURE = 3 };

@@ -596,3 +596,57 @@ def test_oracle_shard_invariant(c):
     a = oracle.rollout(wl, np.arange(h), pids[:h])["returns"]
     b = oracle.rollout(wl, np.arange(n - h), pids[h:], env_offset=h)["returns"]
     assert np.array_equal(full, np.concatenate([a, b]))
+
+
+# ------------------------------------------------------------ meta-solver (FP)
+def test_solve_fp_hand_trace():
+    """Three iterations on M = [[1, 2], [3, 0]] worked by hand: (i, j) =
+    (0, 0), (1, 0), (1, 1); v = [4, 6], w = [7, 2] afterwards."""
+    cx, cy, gap = oracle.solve_fp(np.array([[1.0, 2.0], [3.0, 0.0]]), 3)
+    assert cx.tolist() == [1, 2] and cy.tolist() == [2, 1]
+    assert gap == (6.0 - 2.0) / 3.0
+
+
+def test_solve_fp_zero_game_and_dominance():
+    """All-zero game: every tie goes to index 0.  Strictly dominant row 1 and
+    column 1 of [[3, 1], [4, 2]]: after the first iteration both sides play 1,
+    and the gap is 3/T in closed form."""
+    cx, cy, gap = oracle.solve_fp(np.zeros((5, 5)), 40)
+    assert cx.tolist() == [40, 0, 0, 0, 0] and cy.tolist() == [40, 0, 0, 0, 0] and gap == 0.0
+    T = 500
+    cx, cy, gap = oracle.solve_fp(np.array([[3.0, 1.0], [4.0, 2.0]]), T)
+    assert cx.tolist() == [1, T - 1] and cy.tolist() == [1, T - 1]
+    assert abs(gap - 3.0 / T) < 1e-15
+
+
+@pytest.mark.parametrize("M,x0,y0,value", [
+    # 2x2 without a saddle point: x* = (d-c)/D, y* = (d-b)/D, value (ad-bc)/D,
+    # D = a-b-c+d
+    ([[1.0, 2.0], [3.0, 0.0]], 0.75, 0.5, 1.5),
+    ([[2.0, -1.0], [-1.0, 1.0]], 0.4, 0.4, 0.2),
+])
+def test_solve_fp_converges_to_the_2x2_equilibrium(M, x0, y0, value):
+    T = 20000
+    M = np.array(M)
+    cx, cy, gap = oracle.solve_fp(M, T)
+    assert abs(cx[0] / T - x0) < 0.02 and abs(cy[0] / T - y0) < 0.02
+    # the averages' best-response values bracket the game value
+    lo, hi = (cx @ M).min() / T, (M @ cy).max() / T
+    assert lo <= value + 1e-12 and value <= hi + 1e-12 and gap == pytest.approx(hi - lo, abs=1e-12)
+    assert gap < 0.02
+
+
+def test_solve_fp_rock_paper_scissors_and_gap_definition():
+    """Rock-paper-scissors: the averages approach uniform play, and the gap is
+    max(M cy) - min(cx M), recomputed from the counts."""
+    M = np.array([[0.0, -1.0, 1.0], [1.0, 0.0, -1.0], [-1.0, 1.0, 0.0]])
+    T = 30000
+    cx, cy, gap = oracle.solve_fp(M, T)
+    assert np.abs(cx / T - 1 / 3).max() < 0.03 and np.abs(cy / T - 1 / 3).max() < 0.03
+    assert gap == pytest.approx(((M @ cy).max() - (cx @ M).min()) / T, abs=1e-12)
+    assert 0.0 <= gap < 0.05
+    rng = np.random.default_rng(5)
+    R = rng.normal(size=(17, 17))
+    cx, cy, gap = oracle.solve_fp(R, 777)
+    assert cx.sum() == 777 and cy.sum() == 777
+    assert gap == pytest.approx(((R @ cy).max() - (cx @ R).min()) / 777, abs=1e-12)
