@@ -241,6 +241,48 @@ malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t n_po
                                int64_t n_envs, int32_t n_agents, uint64_t seed,
                                int64_t env_offset, int32_t* pair_assign_out, void* stream);
 
+/* ------------------------------------------------------------- meta-solver */
+
+/*
+ * The payoff table as the meta-solver's game: M [P][P] fp64 on the device,
+ * the mean of each cell as malib_payoff_eval computes it (sum / count), 0 for
+ * cells with no simulations.  Asynchronous on `stream`; M is caller-owned.
+ */
+malib_status malib_payoff_matrix(malib_pop_t pop, double* M, void* stream);
+
+/*
+ * Fictitious play on the table (the meta-update Comb_{t+1} ~ G(Eval) of
+ * Sec. 3.1 with the fictitious-play meta-solver of the PSRO experiments,
+ * Sec. 5; get_equilibrium of the example API, Appendix C.2).  The game is
+ * two-player zero-sum: the row side receives M[i][j], the column side
+ * -M[i][j].  Each of `iterations` (1 .. 2^24) simultaneous steps plays the
+ * first best response of each side to the other's empirical play so far:
+ * i_t = first argmax of v = sum over s < t of M[:, j_s], j_t = first argmin
+ * of w = sum over s < t of M[i_s, :], v and w kept in fp64 and grown by one
+ * column / row per step.
+ *  M:     device fp64 [P][P], finite (e.g. from malib_payoff_matrix).
+ *  sigma: device fp32 [2][P]: the row side's and the column side's play
+ *         counts, i.e. their average strategies times `iterations`, usable
+ *         directly as weight rows of malib_meta_sample_device.
+ *  gap:   device fp64 [1] or NULL: (max v - min w) / iterations, the
+ *         exploitability of the two average strategies.
+ * Asynchronous on `stream`; one workgroup (the solver is sequential in t).
+ */
+malib_status malib_solve_fp(const double* M, int32_t n_policies, int32_t iterations,
+                            float* sigma, double* gap, void* stream);
+
+/*
+ * malib_meta_sample with the weights on the device (e.g. from malib_solve_fp),
+ * same draws and the same fp64 thresholds.  Weights are checked on the device:
+ * a row with a negative or non-finite weight or no positive mass gives policy
+ * id -1 to its seats, which the next malib_rollout_batch flags (reported by
+ * malib_payoff_eval as MALIB_E_DEVICE).  Asynchronous on `stream`.
+ */
+malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32_t n_policies,
+                                      int64_t n_envs, int32_t n_agents, uint64_t seed,
+                                      int64_t env_offset, int32_t* pair_assign_out,
+                                      void* stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char* malib_last_error(void);
 

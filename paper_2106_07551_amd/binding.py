@@ -25,6 +25,7 @@ EXPORTS = [
     "malib_pop_create", "malib_pop_destroy", "malib_rollout_batch", "malib_payoff_eval",
     "malib_meta_sample", "malib_last_error", "malib_profile_enable", "malib_profile_read",
     "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
+    "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
 ]
 
 
@@ -93,6 +94,12 @@ def lib():
         L.malib_debug_bf16.restype = i32
         L.malib_debug_philox.argtypes = [vp, u64, u64, vp, i64, vp]
         L.malib_debug_philox.restype = i32
+        L.malib_payoff_matrix.argtypes = [vp, vp, vp]
+        L.malib_payoff_matrix.restype = i32
+        L.malib_solve_fp.argtypes = [vp, i32, i32, vp, vp, vp]
+        L.malib_solve_fp.restype = i32
+        L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, u64, i64, vp, vp]
+        L.malib_meta_sample_device.restype = i32
         _lib = L
     return _lib
 
@@ -160,6 +167,15 @@ class Population:
             self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
             horizon, _dptr(returns), C.byref(tr) if tr is not None else None,
             _stream(stream)))
+
+    def payoff_matrix(self, out=None, stream=None):
+        """malib_payoff_matrix: the table's means as a device fp64 [P][P] game
+        (0 for empty cells)."""
+        import torch
+        if out is None:
+            out = torch.empty((self.P, self.P), dtype=torch.float64, device="cuda")
+        _check(lib().malib_payoff_matrix(self.handle, _dptr(out), _stream(stream)))
+        return out
 
     def payoff(self, reset: bool = False, stream=None, check: bool = True):
         P = self.P
@@ -238,6 +254,35 @@ def meta_sample(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *
         out = torch.empty((n_envs, n_agents), dtype=torch.int32, device="cuda")
     _check(lib().malib_meta_sample(s.ctypes.data, s.shape[0], n_policies, n_envs, n_agents,
                                    seed, env_offset, _dptr(out), _stream(stream)))
+    return out
+
+
+def solve_fp(M, iterations: int, *, sigma=None, gap=None, stream=None):
+    """malib_solve_fp on a device fp64 [P][P] game: returns (sigma [2][P] play
+    counts as fp32, gap [1] fp64), both device tensors."""
+    import torch
+    P = M.shape[0]
+    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
+    if sigma is None:
+        sigma = torch.empty((2, P), dtype=torch.float32, device=M.device)
+    if gap is None:
+        gap = torch.empty(1, dtype=torch.float64, device=M.device)
+    _check(lib().malib_solve_fp(_dptr(M), P, iterations, _dptr(sigma), _dptr(gap),
+                                _stream(stream)))
+    return sigma, gap
+
+
+def meta_sample_device(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *,
+                       env_offset: int = 0, out=None, stream=None):
+    """malib_meta_sample_device: policy ids drawn from device weight rows
+    sigma [n_sigma][P] (fp32)."""
+    import torch
+    assert sigma.dtype == torch.float32 and sigma.is_contiguous()
+    n_sigma = sigma.numel() // n_policies
+    if out is None:
+        out = torch.empty((n_envs, n_agents), dtype=torch.int32, device=sigma.device)
+    _check(lib().malib_meta_sample_device(_dptr(sigma), n_sigma, n_policies, n_envs, n_agents,
+                                          seed, env_offset, _dptr(out), _stream(stream)))
     return out
 
 

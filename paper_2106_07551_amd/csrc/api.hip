@@ -622,6 +622,54 @@ malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, i
     return MALIB_OK;
 }
 
+// ---------------------------------------------------------------- meta-solver
+
+malib_status malib_payoff_matrix(malib_pop_t pop, double* M, void* stream)
+{
+    if (!pop || !M)
+        return fail(MALIB_E_INVAL, "pop and M must not be NULL");
+    HIP_TRY(launch_payoff_matrix(pop->sum, pop->cnt, pop->P, M, (hipStream_t)stream));
+    return MALIB_OK;
+}
+
+malib_status malib_solve_fp(const double* M, int32_t P, int32_t iterations, float* sigma,
+                            double* gap, void* stream)
+{
+    if (!M || !sigma)
+        return fail(MALIB_E_INVAL, "M and sigma must not be NULL");
+    if (P < 1 || P > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
+    if (iterations < 1 || iterations > (1 << 24))
+        return fail(MALIB_E_INVAL, "iterations must be in [1, 2^24]");
+    HIP_TRY(launch_solve_fp(M, P, iterations, sigma, gap, (hipStream_t)stream));
+    return MALIB_OK;
+}
+
+malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32_t P,
+                                      int64_t n_envs, int32_t n_agents, uint64_t seed,
+                                      int64_t env_offset, int32_t* out, void* stream)
+{
+    if (!sigma || !out)
+        return fail(MALIB_E_INVAL, "sigma and pair_assign_out must not be NULL");
+    if (P < 1 || P > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
+    if (n_agents < 1 || n_agents > kMaxAgents)
+        return fail(MALIB_E_INVAL, "n_agents must be in [1, %d]", kMaxAgents);
+    if (n_sigma != 1 && n_sigma != n_agents)
+        return fail(MALIB_E_INVAL, "n_sigma must be 1 or n_agents");
+    if (n_envs < 0 || n_envs * n_agents > ((int64_t)1 << 26) || env_offset < 0)
+        return fail(MALIB_E_INVAL, "bad n_envs / env_offset");
+    if (n_envs == 0)
+        return MALIB_OK;
+    hipStream_t s = (hipStream_t)stream;
+    unsigned long long* d_thr = nullptr;
+    HIP_TRY(hipMallocAsync((void**)&d_thr, sizeof(unsigned long long) * (size_t)n_sigma * P, s));
+    HIP_TRY(launch_thresholds(sigma, n_sigma, P, d_thr, s));
+    HIP_TRY(launch_meta_sample(d_thr, n_sigma, P, n_envs, n_agents, seed, env_offset, out, s));
+    HIP_TRY(hipFreeAsync(d_thr, s));
+    return MALIB_OK;
+}
+
 // ---------------------------------------------------------------- profiling
 
 malib_status malib_profile_enable(malib_pop_t pop, int32_t mask, int32_t every)

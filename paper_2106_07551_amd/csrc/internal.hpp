@@ -83,6 +83,15 @@ inline int max_tiles_for(int64_t n_slots, int P, int tile_rows)
     return (int)((n_slots + tile_rows - 1) / tile_rows + P);
 }
 
+// Meta-solver: the table as a game, fictitious play, thresholds from device
+// weights (k_solve.hip).
+hipError_t launch_payoff_matrix(const unsigned long long* sum, const unsigned long long* cnt,
+                                int P, double* M, hipStream_t s);
+hipError_t launch_solve_fp(const double* M, int P, int T, float* sigma, double* gap,
+                           hipStream_t s);
+hipError_t launch_thresholds(const float* sigma, int n_sigma, int P, unsigned long long* thr,
+                             hipStream_t s);
+
 // Meta-strategy sampling from precomputed thresholds [n_sigma][P].
 hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
                               int64_t n_envs, int n_agents, uint64_t seed, int64_t env_offset,

@@ -21,6 +21,10 @@ __global__ void meta_sample_kernel(const unsigned long long* __restrict__ thr, i
     u64x4 blk = stream_block(seed, (uint64_t)(env_offset + e), 0, kPurposeMeta, seat, 0);
     unsigned long long x = (uint32_t)blk.x;
     const unsigned long long* T = thr + (n_sigma == 1 ? 0 : seat) * P;
+    if (T[P - 1] == 0ull) {   // an invalid weight row (device weights only)
+        out[i] = -1;
+        return;
+    }
     int lo = 0, hi = P - 1;
     while (lo < hi) {
         int mid = (lo + hi) >> 1;
