@@ -155,6 +155,49 @@ def cpu_baseline(wl, budget_s=12.0, max_s=30.0):
             "cpu": platform.processor() or platform.machine()}
 
 
+def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
+    """The meta-update after a fill, on the device: the table as a game
+    (malib_payoff_matrix), `iters` steps of fictitious play (malib_solve_fp)
+    and the next policy ids drawn from the play counts, row side's counts for
+    the row-side seats and the column side's for the others
+    (malib_meta_sample_device).  Each stage timed with HIP events on the
+    stream it runs on, averaged over `reps` calls, after one untimed fill that
+    leaves the table full."""
+    import torch
+    n, na, P = wl.n_envs, wl.n_agents, wl.P
+    if wl.pairs is None:
+        M.meta_sample(wl.sigma, P, n, na, wl.seed, out=pairs)
+    pop.rollout(env, n, pairs, wl.seed, wl.horizon)
+    seat_row = (wl.team < 0).astype("int32")
+    game = torch.empty((P, P), dtype=torch.float64, device="cuda")
+    sigma = torch.empty((2, P), dtype=torch.float32, device="cuda")
+    gap = torch.empty(1, dtype=torch.float64, device="cuda")
+    ids = torch.empty((n, na), dtype=torch.int32, device="cuda")
+    stages = {
+        "payoff_matrix": lambda: pop.payoff_matrix(out=game),
+        "solve_fp": lambda: M.solve_fp(game, iters, sigma=sigma, gap=gap),
+        "meta_sample_device": lambda: M.meta_sample_device(sigma, P, n, na, wl.seed + 1,
+                                                           seat_row=seat_row, out=ids),
+    }
+    out = {"fp_iterations": iters, "policies": P, "envs": n}
+    for name, fn in stages.items():
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name + "_us"] = round(1000.0 * e0.elapsed_time(e1) / reps, 2)
+    out["solve_fp_ns_per_iteration"] = round(1000.0 * out["solve_fp_us"] / iters, 1)
+    out["total_us"] = round(sum(out[k + "_us"] for k in stages), 2)
+    out["gap"] = float(gap.cpu()[0])
+    pop.payoff(reset=True)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -165,6 +208,9 @@ def main():
     ap.add_argument("--event-every", type=int, default=0, metavar="K",
                     help="time one grouped-forward launch in K with HIP events during the "
                          "timed fills (default: about 16 per fill, at least every 4th)")
+    ap.add_argument("--fp-iters", type=int, default=1000, metavar="T",
+                    help="fictitious-play iterations of the meta-update timed after the "
+                         "fills (table -> game -> solver -> meta-sample)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the "
                          "reference kernel for scaling HBM byte counters) and exit")
@@ -257,6 +303,7 @@ def main():
                 kern[name]["fp32_TFLOPs"] = round(w["flops"] / t / 1e12, 2)
                 kern[name]["alu_frac"] = round(w["flops"] / t / 1e12 / PEAK_F32_ALU_TFLOPS, 4)
     pop.profile_enable(False)
+    meta = meta_update_timing(M, pop, env, wl, pairs, args.fp_iters)
 
     ms_step = 1000.0 * el / args.steps
     value = frames / el
@@ -299,6 +346,7 @@ def main():
         "config": describe(wl),
         "roofline": roof,
         "kernels": kern,
+        "meta_update": meta,
         "frames_per_step": frames // max(args.steps, 1),
     }
     if not args.no_cpu_baseline:

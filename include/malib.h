@@ -265,21 +265,32 @@ malib_status malib_payoff_matrix(malib_pop_t pop, double* M, void* stream);
  *         counts, i.e. their average strategies times `iterations`, usable
  *         directly as weight rows of malib_meta_sample_device.
  *  gap:   device fp64 [1] or NULL: (max v - min w) / iterations, the
- *         exploitability of the two average strategies.
- * Asynchronous on `stream`; one workgroup (the solver is sequential in t).
+ *         exploitability of the two average strategies; NaN if a NaN entered
+ *         v or w (the counts are then unspecified but still sum to
+ *         `iterations` per side).
+ * Asynchronous on `stream`; one wavefront (the solver is sequential in t),
+ * with M in LDS for P <= 128.
  */
 malib_status malib_solve_fp(const double* M, int32_t n_policies, int32_t iterations,
                             float* sigma, double* gap, void* stream);
 
 /*
  * malib_meta_sample with the weights on the device (e.g. from malib_solve_fp),
- * same draws and the same fp64 thresholds.  Weights are checked on the device:
- * a row with a negative or non-finite weight or no positive mass gives policy
- * id -1 to its seats, which the next malib_rollout_batch flags (reported by
- * malib_payoff_eval as MALIB_E_DEVICE).  Asynchronous on `stream`.
+ * same draws and the same fp64 thresholds.
+ *  sigma:    device fp32 [n_sigma][n_policies] weight rows.
+ *  seat_row: host int32 [n_agents] or NULL.  With NULL, n_sigma is 1 or
+ *            n_agents as for malib_meta_sample; otherwise seat k draws from
+ *            row seat_row[k] (in [0, n_sigma), n_sigma <= 8), e.g. row 0 (the
+ *            row side's counts from malib_solve_fp) for the seats of one team
+ *            and row 1 for the other.
+ * Weights are checked on the device: a row with a negative or non-finite
+ * weight or no positive mass gives policy id -1 to its seats, which the next
+ * malib_rollout_batch flags (reported by malib_payoff_eval as
+ * MALIB_E_DEVICE).  Asynchronous on `stream`.
  */
 malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32_t n_policies,
-                                      int64_t n_envs, int32_t n_agents, uint64_t seed,
+                                      int64_t n_envs, int32_t n_agents,
+                                      const int32_t* seat_row, uint64_t seed,
                                       int64_t env_offset, int32_t* pair_assign_out,
                                       void* stream);
 

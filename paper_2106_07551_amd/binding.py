@@ -98,7 +98,7 @@ def lib():
         L.malib_payoff_matrix.restype = i32
         L.malib_solve_fp.argtypes = [vp, i32, i32, vp, vp, vp]
         L.malib_solve_fp.restype = i32
-        L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, u64, i64, vp, vp]
+        L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, vp, u64, i64, vp, vp]
         L.malib_meta_sample_device.restype = i32
         _lib = L
     return _lib
@@ -273,16 +273,22 @@ def solve_fp(M, iterations: int, *, sigma=None, gap=None, stream=None):
 
 
 def meta_sample_device(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *,
-                       env_offset: int = 0, out=None, stream=None):
+                       env_offset: int = 0, seat_row=None, out=None, stream=None):
     """malib_meta_sample_device: policy ids drawn from device weight rows
-    sigma [n_sigma][P] (fp32)."""
+    sigma [n_sigma][P] (fp32); seat k uses row seat_row[k] (default: row 0
+    for all seats when there is one row, else row k)."""
     import torch
     assert sigma.dtype == torch.float32 and sigma.is_contiguous()
     n_sigma = sigma.numel() // n_policies
     if out is None:
         out = torch.empty((n_envs, n_agents), dtype=torch.int32, device=sigma.device)
+    sr = None
+    if seat_row is not None:
+        sr = np.ascontiguousarray(seat_row, dtype=np.int32)
+        assert sr.shape == (n_agents,)
     _check(lib().malib_meta_sample_device(_dptr(sigma), n_sigma, n_policies, n_envs, n_agents,
-                                          seed, env_offset, _dptr(out), _stream(stream)))
+                                          None if sr is None else sr.ctypes.data, seed,
+                                          env_offset, _dptr(out), _stream(stream)))
     return out
 
 

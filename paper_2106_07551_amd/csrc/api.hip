@@ -574,6 +574,12 @@ malib_status malib_payoff_eval(malib_pop_t pop, void* stream, int32_t reset, dou
 
 // -------------------------------------------------------------- meta-sample
 
+// Seat k draws from row 0 (one shared row) or row k (a row per seat).
+static uint32_t default_seat_map(int n_sigma)
+{
+    return n_sigma == 1 ? 0u : 0x76543210u;
+}
+
 malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, int64_t n_envs,
                                int32_t n_agents, uint64_t seed, int64_t env_offset,
                                int32_t* out, void* stream)
@@ -617,7 +623,8 @@ malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, i
     HIP_TRY(hipMallocAsync((void**)&d_thr, nb, s));
     HIP_TRY(hipMemcpyAsync(d_thr, thr.data(), nb, hipMemcpyHostToDevice, s));
     HIP_TRY(hipStreamSynchronize(s));
-    HIP_TRY(launch_meta_sample(d_thr, n_sigma, P, n_envs, n_agents, seed, env_offset, out, s));
+    HIP_TRY(launch_meta_sample(d_thr, default_seat_map(n_sigma), P, n_envs, n_agents, seed,
+                               env_offset, out, s));
     HIP_TRY(hipFreeAsync(d_thr, s));
     return MALIB_OK;
 }
@@ -646,8 +653,9 @@ malib_status malib_solve_fp(const double* M, int32_t P, int32_t iterations, floa
 }
 
 malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32_t P,
-                                      int64_t n_envs, int32_t n_agents, uint64_t seed,
-                                      int64_t env_offset, int32_t* out, void* stream)
+                                      int64_t n_envs, int32_t n_agents, const int32_t* seat_row,
+                                      uint64_t seed, int64_t env_offset, int32_t* out,
+                                      void* stream)
 {
     if (!sigma || !out)
         return fail(MALIB_E_INVAL, "sigma and pair_assign_out must not be NULL");
@@ -655,8 +663,21 @@ malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32
         return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
     if (n_agents < 1 || n_agents > kMaxAgents)
         return fail(MALIB_E_INVAL, "n_agents must be in [1, %d]", kMaxAgents);
-    if (n_sigma != 1 && n_sigma != n_agents)
-        return fail(MALIB_E_INVAL, "n_sigma must be 1 or n_agents");
+    uint32_t seat_map = 0;
+    if (seat_row) {
+        if (n_sigma < 1 || n_sigma > kMaxAgents)
+            return fail(MALIB_E_INVAL, "n_sigma must be in [1, %d]", kMaxAgents);
+        for (int k = 0; k < n_agents; ++k) {
+            if (seat_row[k] < 0 || seat_row[k] >= n_sigma)
+                return fail(MALIB_E_INVAL, "seat_row[%d] = %d is not a row of sigma", k,
+                            seat_row[k]);
+            seat_map |= (uint32_t)seat_row[k] << (4 * k);
+        }
+    } else {
+        if (n_sigma != 1 && n_sigma != n_agents)
+            return fail(MALIB_E_INVAL, "n_sigma must be 1 or n_agents");
+        seat_map = default_seat_map(n_sigma);
+    }
     if (n_envs < 0 || n_envs * n_agents > ((int64_t)1 << 26) || env_offset < 0)
         return fail(MALIB_E_INVAL, "bad n_envs / env_offset");
     if (n_envs == 0)
@@ -665,7 +686,7 @@ malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32
     unsigned long long* d_thr = nullptr;
     HIP_TRY(hipMallocAsync((void**)&d_thr, sizeof(unsigned long long) * (size_t)n_sigma * P, s));
     HIP_TRY(launch_thresholds(sigma, n_sigma, P, d_thr, s));
-    HIP_TRY(launch_meta_sample(d_thr, n_sigma, P, n_envs, n_agents, seed, env_offset, out, s));
+    HIP_TRY(launch_meta_sample(d_thr, seat_map, P, n_envs, n_agents, seed, env_offset, out, s));
     HIP_TRY(hipFreeAsync(d_thr, s));
     return MALIB_OK;
 }

@@ -93,7 +93,8 @@ hipError_t launch_thresholds(const float* sigma, int n_sigma, int P, unsigned lo
                              hipStream_t s);
 
 // Meta-strategy sampling from precomputed thresholds [n_sigma][P].
-hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
+// seat_map: 4 bits per seat, the threshold row that seat draws from
+hipError_t launch_meta_sample(const unsigned long long* thr, uint32_t seat_map, int P,
                               int64_t n_envs, int n_agents, uint64_t seed, int64_t env_offset,
                               int32_t* out, hipStream_t s);
 

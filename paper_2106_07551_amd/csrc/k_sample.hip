@@ -8,7 +8,7 @@ namespace malib {
 // One thread per (env, seat).  pid = min{m : x < T[m]} for the first lane x
 // of block (g, 0, kPurposeMeta<<32 | seat, 0); T is non-decreasing with
 // T[P-1] = 2^32, so the binary search always lands inside [0, P).
-__global__ void meta_sample_kernel(const unsigned long long* __restrict__ thr, int n_sigma,
+__global__ void meta_sample_kernel(const unsigned long long* __restrict__ thr, uint32_t seat_map,
                                    int P, int64_t n_envs, int n_agents, uint64_t seed,
                                    int64_t env_offset, int32_t* __restrict__ out)
 {
@@ -20,7 +20,7 @@ __global__ void meta_sample_kernel(const unsigned long long* __restrict__ thr, i
     int seat = (int)(i - e * n_agents);
     u64x4 blk = stream_block(seed, (uint64_t)(env_offset + e), 0, kPurposeMeta, seat, 0);
     unsigned long long x = (uint32_t)blk.x;
-    const unsigned long long* T = thr + (n_sigma == 1 ? 0 : seat) * P;
+    const unsigned long long* T = thr + (size_t)((seat_map >> (4 * seat)) & 0xFu) * P;
     if (T[P - 1] == 0ull) {   // an invalid weight row (device weights only)
         out[i] = -1;
         return;
@@ -36,13 +36,13 @@ __global__ void meta_sample_kernel(const unsigned long long* __restrict__ thr, i
     out[i] = lo;
 }
 
-hipError_t launch_meta_sample(const unsigned long long* thr, int n_sigma, int P,
+hipError_t launch_meta_sample(const unsigned long long* thr, uint32_t seat_map, int P,
                               int64_t n_envs, int n_agents, uint64_t seed, int64_t env_offset,
                               int32_t* out, hipStream_t s)
 {
     int64_t total = n_envs * n_agents;
     int blocks = (int)((total + 255) / 256);
-    meta_sample_kernel<<<blocks, 256, 0, s>>>(thr, n_sigma, P, n_envs, n_agents, seed,
+    meta_sample_kernel<<<blocks, 256, 0, s>>>(thr, seat_map, P, n_envs, n_agents, seed,
                                               env_offset, out);
     return hipGetLastError();
 }

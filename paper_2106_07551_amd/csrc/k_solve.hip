@@ -28,140 +28,193 @@ hipError_t launch_payoff_matrix(const unsigned long long* sum, const unsigned lo
     return hipGetLastError();
 }
 
-// (value, index) candidates of the best responses.  A beats B for the row side
-// when its value is larger, or equal with a lower index; for the column side
-// when smaller, or equal with a lower index.  For finite values these are
-// strict total orders, so any reduction order finds the first argmax /
-// argmin, the same choice as a sequential scan.
-struct Cand {
-    double v;
-    int i;
-};
+constexpr int kSolveLdsP = 128;   // up to this P the game sits in LDS
+static_assert(kMaxP <= 4 * 64, "the solver keeps at most 4 policies per lane");
 
-__device__ __forceinline__ Cand shfl_xor_cand(Cand c, int m)
+// A lane's fp64 value moved across lanes by one DPP pattern (both halves).
+// Only patterns that stay inside a 16-lane row are used, so every lane has a
+// source.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x)
 {
-    Cand o;
-    o.v = __shfl_xor(c.v, m);
-    o.i = __shfl_xor(c.i, m);
-    return o;
+    const long long b = __double_as_longlong(x);
+    const int lo = __builtin_amdgcn_mov_dpp((int)b, CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
 }
 
-template <bool MAX>
-__device__ __forceinline__ Cand better(Cand a, Cand b)
+__device__ __forceinline__ double readlane_f64(double x, int l)
 {
-    const bool a_wins = MAX ? (a.v > b.v || (a.v == b.v && a.i < b.i))
-                            : (a.v < b.v || (a.v == b.v && a.i < b.i));
-    return a_wins ? a : b;
+    const long long b = __double_as_longlong(x);
+    const int lo = __builtin_amdgcn_readlane((int)b, l);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
 }
 
-template <bool MAX>
-__device__ __forceinline__ Cand wave_best(Cand c)
-{
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1)
-        c = better<MAX>(c, shfl_xor_cand(c, m));
-    return c;
-}
+// DPP controls: swap neighbours, swap pairs in a quad, mirror each 8-lane
+// half row, mirror each 16-lane row.  After the four steps every lane holds
+// its row's result; the four rows are combined from lanes 0, 16, 32, 48.
+constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
 
-constexpr int kSolveThreads = kMaxP;           // one thread per policy
-constexpr int kSolveWaves = kSolveThreads / 64;
-constexpr int kSolveLdsP = 128;                // up to this P the game sits in LDS
+// The largest of x and the smallest of y over the wavefront, the same in
+// every lane (a NaN never replaces a number); the two reductions interleave.
+__device__ __forceinline__ void wave_max_min(double& x, double& y)
+{
+    auto hi = [](double a, double b) { return b > a ? b : a; };
+    auto lo = [](double a, double b) { return b < a ? b : a; };
+    double dx = dpp_f64<kDppQuadSwap1>(x), dy = dpp_f64<kDppQuadSwap1>(y);
+    x = hi(x, dx);
+    y = lo(y, dy);
+    dx = dpp_f64<kDppQuadSwap2>(x);
+    dy = dpp_f64<kDppQuadSwap2>(y);
+    x = hi(x, dx);
+    y = lo(y, dy);
+    dx = dpp_f64<kDppHalfMirror>(x);
+    dy = dpp_f64<kDppHalfMirror>(y);
+    x = hi(x, dx);
+    y = lo(y, dy);
+    dx = dpp_f64<kDppRowMirror>(x);
+    dy = dpp_f64<kDppRowMirror>(y);
+    x = hi(x, dx);
+    y = lo(y, dy);
+    x = hi(hi(readlane_f64(x, 0), readlane_f64(x, 16)),
+           hi(readlane_f64(x, 32), readlane_f64(x, 48)));
+    y = lo(lo(readlane_f64(y, 0), readlane_f64(y, 16)),
+           lo(readlane_f64(y, 32), readlane_f64(y, 48)));
+}
 
 // Simultaneous fictitious play on the zero-sum game with row payoff M
 // (P x P, fp64; meant for finite entries, a NaN anywhere in v or w leaves the
-// counts unspecified and sets gap to NaN): at iteration t, i_t = first argmax of v = sum over
-// s < t of M[:, j_s] and j_t = first argmin of w = sum over s < t of M[i_s, :];
-// then both play counts are incremented and v, w gain column j_t and row i_t
-// (one fp64 add per element per iteration, in iteration order).  Thread k keeps
-// v_k, w_k and both counts of policy k.  Writes sigma[0][k], sigma[1][k] = the
-// play counts (weights for meta-sampling) and gap = (max v - min w) / T.
-template <bool IN_LDS>
-__global__ __launch_bounds__(kSolveThreads) void solve_fp_kernel(const double* __restrict__ M,
-                                                                 int P, int T,
-                                                                 float* __restrict__ sigma,
-                                                                 double* __restrict__ gap)
+// counts unspecified and sets gap to NaN): at iteration t, i_t = first argmax
+// of v = sum over s < t of M[:, j_s] and j_t = first argmin of w = sum over
+// s < t of M[i_s, :]; then both play counts are incremented and v, w gain
+// column j_t and row i_t (one fp64 add per element per iteration, in
+// iteration order).  One wavefront: lane l keeps policies k = l + 64 q,
+// q < K, so an iteration needs no barrier.  The first argmax is the lowest k
+// whose v equals the wavefront's maximum: the lowest q with a match, then the
+// lowest lane (a ballot).  Writes sigma[0][k], sigma[1][k] = the play counts
+// (weights for meta-sampling) and gap = (v[i] - w[j]) / T at the best
+// responses i, j to the final sums.
+template <int K, bool IN_LDS>
+__global__ __launch_bounds__(64) void solve_fp_kernel(const double* __restrict__ M, int P, int T,
+                                                      float* __restrict__ sigma,
+                                                      double* __restrict__ gap)
 {
     // the game with a padded row stride (column reads hit different banks)
     constexpr int LDS_DOUBLES = IN_LDS ? kSolveLdsP * (kSolveLdsP + 1) : 1;
     __shared__ double Ms[LDS_DOUBLES];
-    __shared__ Cand red[2][2][kSolveWaves];    // [iteration parity][side][wave]
-    const int k = threadIdx.x, lane = k & 63, wave = k >> 6;
+    const int lane = threadIdx.x;
     const int stride = IN_LDS ? P + 1 : P;
     const double* G = M;
     if constexpr (IN_LDS) {
-        for (int e = k; e < P * P; e += kSolveThreads)
+        for (int e = lane; e < P * P; e += 64)
             Ms[(e / P) * stride + e % P] = M[e];
         __syncthreads();
         G = Ms;
     }
-    const bool mine = k < P;
-    double v = 0.0, w = 0.0;
-    int cx = 0, cy = 0;
-    for (int t = 0; t < T; ++t) {
-        Cand a{mine ? v : -INFINITY, mine ? k : P};
-        Cand b{mine ? w : INFINITY, mine ? k : P};
-        a = wave_best<true>(a);
-        b = wave_best<false>(b);
-        const int par = t & 1;
-        if (lane == 0) {
-            red[par][0][wave] = a;
-            red[par][1][wave] = b;
-        }
-        __syncthreads();   // (the other parity's slots are rewritten only after
-                           // the next barrier, when every thread has read these)
-        Cand ra = red[par][0][0], rb = red[par][1][0];
+    double v[K], w[K];
+    int cx[K], cy[K];
+    bool mine[K];
 #pragma unroll
-        for (int q = 1; q < kSolveWaves; ++q) {
-            ra = better<true>(ra, red[par][0][q]);
-            rb = better<false>(rb, red[par][1][q]);
-        }
-        // (an index of P is only possible when some value is NaN; clamping it
-        // keeps every read inside the game, and the gap then reports NaN)
-        const int i = ra.i < P ? ra.i : P - 1, j = rb.i < P ? rb.i : P - 1;
-        if (mine) {
-            cx += k == i;
-            cy += k == j;
-            v = v + G[k * stride + j];
-            w = w + G[i * stride + k];
-        }
+    for (int q = 0; q < K; ++q) {
+        v[q] = 0.0;
+        w[q] = 0.0;
+        cx[q] = 0;
+        cy[q] = 0;
+        mine[q] = lane + 64 * q < P;
     }
-    if (mine) {
-        sigma[k] = (float)cx;
-        sigma[P + k] = (float)cy;
-    }
-    const bool bad = __syncthreads_or(mine && (__builtin_isnan(v) || __builtin_isnan(w)));
-    if (gap) {
-        Cand a{mine ? v : -INFINITY, mine ? k : P};
-        Cand b{mine ? w : INFINITY, mine ? k : P};
-        a = wave_best<true>(a);
-        b = wave_best<false>(b);
-        const int par = T & 1;
-        __syncthreads();
-        if (lane == 0) {
-            red[par][0][wave] = a;
-            red[par][1][wave] = b;
-        }
-        __syncthreads();
-        if (k == 0) {
-            Cand ra = red[par][0][0], rb = red[par][1][0];
-            for (int q = 1; q < kSolveWaves; ++q) {
-                ra = better<true>(ra, red[par][0][q]);
-                rb = better<false>(rb, red[par][1][q]);
+    // first index of the best value (row side: largest v; column side:
+    // smallest w); P - 1 when no lane matches, which only NaN can cause
+    auto best = [&](int& i, int& j, double& vi, double& wj) {
+        double lv = -INFINITY, lw = INFINITY;
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            if (mine[q]) {
+                lv = v[q] > lv ? v[q] : lv;
+                lw = w[q] < lw ? w[q] : lw;
             }
-            *gap = bad ? (double)NAN : (ra.v - rb.v) / (double)T;
         }
+        wave_max_min(lv, lw);
+        vi = lv;
+        wj = lw;
+        i = P - 1;
+        j = P - 1;
+        bool fi = false, fj = false;
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            const unsigned long long bi = __ballot(mine[q] && v[q] == vi);
+            const unsigned long long bj = __ballot(mine[q] && w[q] == wj);
+            if (!fi && bi) {
+                i = 64 * q + __ffsll(bi) - 1;
+                fi = true;
+            }
+            if (!fj && bj) {
+                j = 64 * q + __ffsll(bj) - 1;
+                fj = true;
+            }
+        }
+    };
+    for (int t = 0; t < T; ++t) {
+        int i, j;
+        double vi, wj;
+        best(i, j, vi, wj);
+        // every slot reads (a slot past P reads policy P - 1 and is never
+        // looked at), so all loads issue before the first add waits
+#pragma unroll
+        for (int q = 0; q < K; ++q) {
+            const int k = lane + 64 * q;
+            const int kc = mine[q] ? k : P - 1;
+            cx[q] += k == i;
+            cy[q] += k == j;
+            v[q] = v[q] + G[kc * stride + j];
+            w[q] = w[q] + G[i * stride + kc];
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < K; ++q) {
+        if (mine[q]) {
+            sigma[lane + 64 * q] = (float)cx[q];
+            sigma[P + lane + 64 * q] = (float)cy[q];
+        }
+    }
+    if (gap) {
+        bool nan = false;
+#pragma unroll
+        for (int q = 0; q < K; ++q)
+            nan = nan || (mine[q] && (__builtin_isnan(v[q]) || __builtin_isnan(w[q])));
+        const bool any_nan = __ballot(nan) != 0ull;
+        int i, j;
+        double vi, wj;
+        best(i, j, vi, wj);
+        // the sums at the chosen indices themselves (of +0 and -0, the
+        // reductions may keep either)
+        double vs = v[0], ws = w[0];
+#pragma unroll
+        for (int q = 1; q < K; ++q) {
+            vs = q == (i >> 6) ? v[q] : vs;
+            ws = q == (j >> 6) ? w[q] : ws;
+        }
+        vi = __shfl(vs, i & 63);
+        wj = __shfl(ws, j & 63);
+        if (lane == 0)
+            *gap = any_nan ? (double)NAN : (vi - wj) / (double)T;
     }
 }
 
 hipError_t launch_solve_fp(const double* M, int P, int T, float* sigma, double* gap,
                            hipStream_t s)
 {
-    if (P < 1 || P > kSolveThreads || T < 1)
+    if (P < 1 || P > kMaxP || T < 1)
         return hipErrorInvalidValue;
-    if (P <= kSolveLdsP)
-        solve_fp_kernel<true><<<1, kSolveThreads, 0, s>>>(M, P, T, sigma, gap);
+    if (P <= 64)
+        solve_fp_kernel<1, true><<<1, 64, 0, s>>>(M, P, T, sigma, gap);
+    else if (P <= kSolveLdsP)
+        solve_fp_kernel<2, true><<<1, 64, 0, s>>>(M, P, T, sigma, gap);
     else
-        solve_fp_kernel<false><<<1, kSolveThreads, 0, s>>>(M, P, T, sigma, gap);
+        solve_fp_kernel<4, false><<<1, 64, 0, s>>>(M, P, T, sigma, gap);
     return hipGetLastError();
 }
 
@@ -170,38 +223,42 @@ hipError_t launch_solve_fp(const double* M, int P, int T, float* sigma, double* 
 // cumulative sum C of row r, T_{P-1} = 2^32.  A row with a negative or
 // non-finite weight or no positive mass gets T = 0 everywhere, which the
 // sampling kernel turns into policy id -1 (flagged by the next rollout).
-__global__ void thresholds_kernel(const float* __restrict__ sigma, int n_sigma, int P,
-                                  unsigned long long* __restrict__ thr)
+__global__ __launch_bounds__(64) void thresholds_kernel(const float* __restrict__ sigma, int P,
+                                                        unsigned long long* __restrict__ thr)
 {
-    const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= n_sigma)
-        return;
+    // one wavefront per row: lane 0 forms the sequential fp64 cumulative sum
+    // (the order of the host path), every lane then converts its share
+    __shared__ double run[kMaxP];
+    const int r = blockIdx.x, lane = threadIdx.x;
     const float* s = sigma + (size_t)r * P;
     unsigned long long* T = thr + (size_t)r * P;
-    double total = 0.0;
     bool ok = true;
-    for (int m = 0; m < P; ++m) {
+    for (int m = lane; m < P; m += 64) {
         const float x = s[m];
         ok = ok && __builtin_isfinite(x) && x >= 0.0f;
-        total += (double)x;
     }
-    ok = ok && total > 0.0;
-    double run = 0.0;
-    for (int m = 0; m < P; ++m) {
-        run += (double)s[m];
-        double c = floor(run / total * 4294967296.0);
+    if (lane == 0) {
+        double c = 0.0;
+        for (int m = 0; m < P; ++m) {
+            c += (double)s[m];
+            run[m] = c;
+        }
+    }
+    __syncthreads();
+    const double total = run[P - 1];
+    ok = !__syncthreads_or(!ok) && total > 0.0;
+    for (int m = lane; m < P; m += 64) {
+        double c = floor(run[m] / total * 4294967296.0);
         if (c > 4294967296.0)
             c = 4294967296.0;
-        T[m] = ok ? (unsigned long long)c : 0ull;
+        T[m] = !ok ? 0ull : m == P - 1 ? 4294967296ull : (unsigned long long)c;
     }
-    if (ok)
-        T[P - 1] = 4294967296ull;
 }
 
 hipError_t launch_thresholds(const float* sigma, int n_sigma, int P, unsigned long long* thr,
                              hipStream_t s)
 {
-    thresholds_kernel<<<(n_sigma + 63) / 64, 64, 0, s>>>(sigma, n_sigma, P, thr);
+    thresholds_kernel<<<n_sigma, 64, 0, s>>>(sigma, P, thr);
     return hipGetLastError();
 }
 

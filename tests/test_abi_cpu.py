@@ -61,6 +61,24 @@ def test_validation_before_device_work():
     sig = np.array([1.0, 1.0], np.float32)
     assert L.malib_meta_sample(sig.ctypes.data, 3, 2, 10, 2, 1, 0, out, None) == B.E_INVAL
     assert L.malib_meta_sample(sig.ctypes.data, 1, 2, 10, 9, 1, 0, out, None) == B.E_INVAL
+    # device-weight sampling and the solver: argument checks come before any
+    # device access (the pointers below are never dereferenced)
+    dev = C.c_void_p(16)
+    bad_rows = np.array([0, 2], np.int32)
+    assert L.malib_meta_sample_device(dev, 2, 4, 10, 2, bad_rows.ctypes.data, 1, 0, out,
+                                      None) == B.E_INVAL
+    assert b"seat_row[1]" in L.malib_last_error()
+    rows = np.zeros(2, np.int32)
+    assert L.malib_meta_sample_device(dev, 9, 4, 10, 2, rows.ctypes.data, 1, 0, out,
+                                      None) == B.E_INVAL
+    assert L.malib_meta_sample_device(dev, 3, 4, 10, 2, None, 1, 0, out, None) == B.E_INVAL
+    assert L.malib_meta_sample_device(None, 1, 4, 10, 2, None, 1, 0, out, None) == B.E_INVAL
+    assert L.malib_meta_sample_device(dev, 1, 0, 10, 2, None, 1, 0, out, None) == B.E_INVAL
+    assert L.malib_solve_fp(dev, 4, 0, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_fp(dev, 4, (1 << 24) + 1, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_fp(dev, 257, 10, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_fp(None, 4, 10, dev, None, None) == B.E_INVAL
+    assert L.malib_payoff_matrix(None, dev, None) == B.E_INVAL
     assert L.malib_profile_enable(None, 1, 1) == B.E_INVAL
     assert L.malib_debug_tanh_ref(None, None, 4, None) == B.E_INVAL
 

@@ -129,6 +129,27 @@ def test_meta_sample_device_weights(P, n_sigma):
             assert (seat_rows[a][g[:, a]] > 0).all()
 
 
+def test_meta_sample_device_seat_rows():
+    """Seats mapped onto weight rows (a 4v4 game: the row side's counts for
+    seats 0-3, the column side's for 4-7) draw as the oracle does with each
+    seat's row written out."""
+    import paper_2106_07551_amd as M
+    P, n = 128, 3000
+    rng = np.random.default_rng(11)
+    s = np.floor(rng.random((2, P)) * 50).astype(np.float32)
+    s[1, :64] = 0
+    seat_row = np.array([0, 0, 0, 0, 1, 1, 1, 1], np.int32)
+    g = M.meta_sample_device(torch.from_numpy(s).cuda(), P, n, 8, 99, env_offset=7,
+                             seat_row=seat_row).cpu().numpy()
+    ref = oracle.meta_sample(s[seat_row], P, n, 8, 99, 7)
+    assert np.array_equal(g, ref)
+    assert (g[:, 4:] >= 64).all()
+    # one row for all seats through the map equals the shared-row default
+    g1 = M.meta_sample_device(torch.from_numpy(s[:1].copy()).cuda(), P, n, 8, 99,
+                              seat_row=np.zeros(8, np.int32)).cpu().numpy()
+    assert np.array_equal(g1, oracle.meta_sample(s[:1], P, n, 8, 99, 0))
+
+
 def test_meta_sample_device_invalid_row_flags_rollout():
     """A device weight row with no mass, a negative or a NaN weight yields
     policy id -1 for its seat; the next rollout flags those envs and leaves
