@@ -221,6 +221,39 @@ malib_status malib_payoff_eval(malib_pop_t pop, void* stream, int32_t reset,
                                double* mean, int64_t* counts, double* stderr_out,
                                malib_eval_stats* stats);
 
+/* ------------------------------------------------------- table expansion */
+
+/*
+ * Grow the population by add->n_policies policies (the auto-curriculum adds
+ * policies to the pools, Sec. 3.1; extend_policy_pool of the example API,
+ * Appendix C.2).  `add` describes only the new policies, with the kind, dims
+ * and n_actions of the population; they take ids P0 .. P0 + k - 1.  The
+ * payoff table grows to (P0 + k)^2 cells: the P0 x P0 cells keep their sums
+ * and counts, the new cells start empty, the live-frame counter and the error
+ * flags carry over.  Synchronizes the device (the old buffers are freed); on
+ * an error the population is unchanged.
+ */
+malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* stream);
+
+/*
+ * Policy ids of the batch that simulates only the new cells after a
+ * population grew from first_new to n_policies policies
+ * (run_simulation_and_update_payoff of the example API, Appendix C.2, on the
+ * new combinations only): every cell (r, c) with r >= first_new or
+ * c >= first_new, n_policies^2 - first_new^2 cells, taken in row-major order
+ * of the grid; cell number q is played by envs q*per_pair .. (q+1)*per_pair-1.
+ * In each env the row-side seats (team +1) take r, the others c.
+ *  team: host [n_agents] of +1 / -1, or NULL for two seats (seat 0 row side).
+ *  pair_assign_out: device int32 [(n_policies^2 - first_new^2) * per_pair]
+ *                   [n_agents], caller-owned.
+ * Rolling that batch out into the same population (malib_rollout_batch with
+ * an env_offset past the envs already simulated) merges it into the table:
+ * the accumulators only add.  Asynchronous on `stream`.
+ */
+malib_status malib_expansion_pairs(int32_t n_policies, int32_t first_new, int32_t per_pair,
+                                   int32_t n_agents, const int8_t* team,
+                                   int32_t* pair_assign_out, void* stream);
+
 /* ------------------------------------------------------------ meta-strategy */
 
 /*

@@ -225,6 +225,20 @@ def solve_fp(M, T):
     return cx, cy, float(gap[0])
 
 
+def expansion_pairs(P, first_new, per_pair, team):
+    """The combinations to simulate after a population grew from first_new to P
+    policies: every cell (r, c) of the P x P grid with r >= first_new or
+    c >= first_new, in row-major order, each played by per_pair consecutive
+    envs; in each env the row-side seats (team +1) take r, the others c."""
+    team = np.asarray(team)
+    cells = [(r, c) for r in range(P) for c in range(P) if r >= first_new or c >= first_new]
+    out = np.empty((len(cells) * per_pair, len(team)), np.int32)
+    for q, (r, c) in enumerate(cells):
+        for k in range(len(team)):
+            out[q * per_pair:(q + 1) * per_pair, k] = r if team[k] > 0 else c
+    return out
+
+
 def payoff_matrix(mean):
     """The solver's game from a payoff table: the means, 0 where a cell has no
     simulations."""

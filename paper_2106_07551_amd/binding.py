@@ -26,6 +26,7 @@ EXPORTS = [
     "malib_meta_sample", "malib_last_error", "malib_profile_enable", "malib_profile_read",
     "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
+    "malib_pop_extend", "malib_expansion_pairs",
 ]
 
 
@@ -100,6 +101,10 @@ def lib():
         L.malib_solve_fp.restype = i32
         L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, vp, u64, i64, vp, vp]
         L.malib_meta_sample_device.restype = i32
+        L.malib_pop_extend.argtypes = [vp, vp, vp]
+        L.malib_pop_extend.restype = i32
+        L.malib_expansion_pairs.argtypes = [i32, i32, i32, i32, vp, vp, vp]
+        L.malib_expansion_pairs.restype = i32
         _lib = L
     return _lib
 
@@ -122,6 +127,29 @@ def _dptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
+def _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits):
+    """A malib_pop_desc over device tensors, with the ctypes arrays it points
+    into (keep them alive until the call returns)."""
+    d = PopDesc()
+    d.kind, d.n_policies, d.n_actions = kind, n_policies, n_actions
+    keep = []
+    if kind == POLICY_TABULAR:
+        d.n_layers = 0
+        d.tab_logits = _dptr(tab_logits)
+    else:
+        d.n_layers = len(dims) - 1
+        dd = (C.c_int32 * len(dims))(*dims)
+        ww = (C.c_void_p * d.n_layers)(*[_dptr(w) for w in weights])
+        keep += [dd, ww]
+        d.dims = C.cast(dd, C.POINTER(C.c_int32))
+        d.weights = C.cast(ww, C.POINTER(C.c_void_p))
+        if biases is not None:
+            bb = (C.c_void_p * d.n_layers)(*[_dptr(b) for b in biases])
+            keep.append(bb)
+            d.biases = C.cast(bb, C.POINTER(C.c_void_p))
+    return d, keep
+
+
 class Population:
     """A policy population handle (malib_pop_create / malib_pop_destroy) with its
     payoff table."""
@@ -129,29 +157,24 @@ class Population:
     def __init__(self, kind: int, n_policies: int, n_actions: int, *, dims=None,
                  weights: Sequence = (), biases: Optional[Sequence] = None,
                  tab_logits=None, stream=None):
-        d = PopDesc()
-        d.kind, d.n_policies, d.n_actions = kind, n_policies, n_actions
-        self._keep = []
-        if kind == POLICY_TABULAR:
-            d.n_layers = 0
-            d.tab_logits = _dptr(tab_logits)
-        else:
-            d.n_layers = len(dims) - 1
-            dd = (C.c_int32 * len(dims))(*dims)
-            ww = (C.c_void_p * d.n_layers)(*[_dptr(w) for w in weights])
-            self._keep += [dd, ww]
-            d.dims = C.cast(dd, C.POINTER(C.c_int32))
-            d.weights = C.cast(ww, C.POINTER(C.c_void_p))
-            if biases is not None:
-                bb = (C.c_void_p * d.n_layers)(*[_dptr(b) for b in biases])
-                self._keep.append(bb)
-                d.biases = C.cast(bb, C.POINTER(C.c_void_p))
+        d, keep = _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits)
         h = C.c_void_p()
         _check(lib().malib_pop_create(C.byref(d), _stream(stream), C.byref(h)))
+        del keep
         self.handle = h
+        self.kind = kind
+        self.dims = list(dims) if dims is not None else None
         self.P = n_policies
         self.A = n_actions
-        self._keep = []
+
+    def extend(self, n_new: int, *, weights: Sequence = (), biases: Optional[Sequence] = None,
+               tab_logits=None, stream=None):
+        """malib_pop_extend: append n_new policies (ids P .. P + n_new - 1); the
+        table keeps its cells and gains empty rows and columns."""
+        d, keep = _pop_desc(self.kind, n_new, self.A, self.dims, weights, biases, tab_logits)
+        _check(lib().malib_pop_extend(self.handle, C.byref(d), _stream(stream)))
+        del keep
+        self.P += n_new
 
     def close(self):
         if getattr(self, "handle", None):
@@ -254,6 +277,24 @@ def meta_sample(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *
         out = torch.empty((n_envs, n_agents), dtype=torch.int32, device="cuda")
     _check(lib().malib_meta_sample(s.ctypes.data, s.shape[0], n_policies, n_envs, n_agents,
                                    seed, env_offset, _dptr(out), _stream(stream)))
+    return out
+
+
+def expansion_pairs(n_policies: int, first_new: int, per_pair: int, n_agents: int = 2,
+                    team=None, *, out=None, stream=None):
+    """malib_expansion_pairs: policy ids [(P^2 - first_new^2) * per_pair][n_agents]
+    of the batch that simulates the cells of the new rows and columns."""
+    import torch
+    n = (n_policies * n_policies - first_new * first_new) * per_pair
+    if out is None:
+        out = torch.empty((max(n, 0), n_agents), dtype=torch.int32, device="cuda")
+    tm = None
+    if team is not None:
+        tm = np.ascontiguousarray(team, dtype=np.int8)
+        assert tm.shape == (n_agents,)
+    _check(lib().malib_expansion_pairs(n_policies, first_new, per_pair, n_agents,
+                                       None if tm is None else tm.ctypes.data, _dptr(out),
+                                       _stream(stream)))
     return out
 
 

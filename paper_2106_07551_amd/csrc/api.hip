@@ -124,14 +124,10 @@ const char* malib_last_error(void) { return g_last_error.c_str(); }
 
 // ------------------------------------------------------------------- create
 
-malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_pop_t* out)
+// Validates a population description; on success *in_dim and *hid hold the
+// MLP input and hidden widths (0 for tabular populations).
+static malib_status check_desc(const malib_pop_desc* desc, int* in_dim, int* hid_out)
 {
-    if (!out)
-        return fail(MALIB_E_INVAL, "out is NULL");
-    *out = nullptr;
-    if (!desc)
-        return fail(MALIB_E_INVAL, "desc is NULL");
-    hipStream_t s = (hipStream_t)stream;
     const int P = desc->n_policies, A = desc->n_actions;
     if (P < 1 || P > kMaxP)
         return fail(MALIB_E_INVAL, "n_policies must be in [1, %d], got %d", kMaxP, P);
@@ -173,6 +169,26 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
         }
     } else {
         return fail(MALIB_E_INVAL, "unknown policy kind %d", desc->kind);
+    }
+    *in_dim = in;
+    *hid_out = hid;
+    return MALIB_OK;
+}
+
+malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_pop_t* out)
+{
+    if (!out)
+        return fail(MALIB_E_INVAL, "out is NULL");
+    *out = nullptr;
+    if (!desc)
+        return fail(MALIB_E_INVAL, "desc is NULL");
+    hipStream_t s = (hipStream_t)stream;
+    const int P = desc->n_policies, A = desc->n_actions;
+    int in = 0, hid = 0;
+    {
+        const malib_status st = check_desc(desc, &in, &hid);
+        if (st != MALIB_OK)
+            return st;
     }
 
     malib_pop* p = new (std::nothrow) malib_pop();
@@ -268,6 +284,166 @@ void malib_pop_destroy(malib_pop_t p)
         (void)hipEventDestroy(ev.stop);
     }
     delete p;
+}
+
+// ---------------------------------------------------------------- extend
+
+malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* stream)
+{
+    if (!pop || !add)
+        return fail(MALIB_E_INVAL, "pop and add must not be NULL");
+    int in = 0, hid = 0;
+    {
+        const malib_status st = check_desc(add, &in, &hid);
+        if (st != MALIB_OK)
+            return st;
+    }
+    if (add->kind != pop->kind)
+        return fail(MALIB_E_INVAL, "policy kind %d differs from the population's (%d)",
+                    add->kind, pop->kind);
+    if (add->n_actions != pop->A)
+        return fail(MALIB_E_INVAL, "n_actions %d differs from the population's (%d)",
+                    add->n_actions, pop->A);
+    if (in != pop->in_dim || hid != pop->hid)
+        return fail(MALIB_E_INVAL, "dims (%d, %d) differ from the population's (%d, %d)", in,
+                    hid, pop->in_dim, pop->hid);
+    const int P0 = pop->P, k = add->n_policies, P = P0 + k, A = pop->A;
+    if (P > kMaxP)
+        return fail(MALIB_E_INVAL, "%d + %d policies exceed %d", P0, k, kMaxP);
+    hipStream_t s = (hipStream_t)stream;
+    // Everything new is built before the handle changes: on failure the
+    // population is left as it was.
+    void* w[3] = {nullptr, nullptr, nullptr};
+    float* b[3] = {nullptr, nullptr, nullptr};
+    float* tab = nullptr;
+    unsigned long long* acc = nullptr;
+    unsigned long long* host_acc = nullptr;
+    auto drop = [&]() {
+        (void)hipStreamSynchronize(s);
+        for (int l = 0; l < 3; ++l) {
+            if (w[l])
+                (void)hipFree(w[l]);
+            if (b[l])
+                (void)hipFree(b[l]);
+        }
+        if (tab)
+            (void)hipFree(tab);
+        if (acc)
+            (void)hipFree(acc);
+        if (host_acc)
+            (void)hipHostFree(host_acc);
+    };
+#define TRY(expr)                                                                         \
+    do {                                                                                  \
+        hipError_t e_ = (expr);                                                           \
+        if (e_ != hipSuccess) {                                                           \
+            drop();                                                                       \
+            return fail(e_ == hipErrorOutOfMemory ? MALIB_E_NOMEM : MALIB_E_HIP,          \
+                        "%s failed: %s", #expr, hipGetErrorString(e_));                   \
+        }                                                                                 \
+    } while (0)
+    if (pop->kind == MALIB_POLICY_TABULAR) {
+        const size_t per = sizeof(float) * A;
+        TRY(hipMalloc((void**)&tab, per * P));
+        TRY(hipMemcpyAsync(tab, pop->tab, per * P0, hipMemcpyDeviceToDevice, s));
+        TRY(hipMemcpyAsync(tab + (size_t)P0 * A, add->tab_logits, per * k,
+                           hipMemcpyDeviceToDevice, s));
+    } else {
+        const int dims[4] = {in, hid, hid, A};
+        for (int l = 0; l < 3; ++l) {
+            const int fi = dims[l], fo = dims[l + 1];
+            const size_t bper = sizeof(float) * fo;
+            TRY(hipMalloc((void**)&b[l], bper * P));
+            TRY(hipMemcpyAsync(b[l], pop->b[l], bper * P0, hipMemcpyDeviceToDevice, s));
+            if (add->biases && add->biases[l])
+                TRY(hipMemcpyAsync(b[l] + (size_t)P0 * fo, add->biases[l], bper * k,
+                                   hipMemcpyDeviceToDevice, s));
+            else
+                TRY(hipMemsetAsync(b[l] + (size_t)P0 * fo, 0, bper * k, s));
+            // packed layouts keep each policy's weights contiguous, policy-major
+            if (pop->kind == MALIB_POLICY_MLP_F32) {
+                const size_t wper = sizeof(float) * (size_t)fo * fi;
+                TRY(hipMalloc(&w[l], wper * P));
+                TRY(hipMemcpyAsync(w[l], pop->w[l], wper * P0, hipMemcpyDeviceToDevice, s));
+                TRY(launch_pack_f32((const float*)add->weights[l], k, l, hid, A,
+                                    (float*)((char*)w[l] + wper * P0), s));
+            } else {
+                const int ip = l == 0 ? pop->in_pad : round_up(fi, 16);
+                const int op = round_up(fo, 32);
+                const size_t wper = (size_t)(op / 32) * (ip / 16) * 64 * 16;
+                TRY(hipMalloc(&w[l], wper * P));
+                TRY(hipMemcpyAsync(w[l], pop->w[l], wper * P0, hipMemcpyDeviceToDevice, s));
+                TRY(launch_pack_bf16(add->weights[l], k, fo, fi, op, ip, l == 2,
+                                     (char*)w[l] + wper * P0, s));
+            }
+        }
+    }
+    const size_t PP = (size_t)P * P, acc_bytes = sizeof(unsigned long long) * (3 * PP + 2);
+    TRY(hipMalloc((void**)&acc, acc_bytes));
+    TRY(hipHostMalloc((void**)&host_acc, acc_bytes, hipHostMallocDefault));
+    TRY(launch_remap_table(pop->acc, P0, acc, P, s));
+    // the old buffers may still be read by work queued on any stream
+    TRY(hipDeviceSynchronize());
+#undef TRY
+    for (int l = 0; l < 3; ++l) {
+        if (pop->w[l]) {
+            (void)hipFree(pop->w[l]);
+            pop->w[l] = w[l];
+        }
+        if (pop->b[l]) {
+            (void)hipFree(pop->b[l]);
+            pop->b[l] = b[l];
+        }
+    }
+    if (pop->tab) {
+        (void)hipFree(pop->tab);
+        pop->tab = tab;
+    }
+    (void)hipFree(pop->acc);
+    (void)hipHostFree(pop->host_acc);
+    pop->acc = acc;
+    pop->host_acc = host_acc;
+    pop->sum = acc;
+    pop->sumsq = acc + PP;
+    pop->cnt = acc + 2 * PP;
+    pop->dev_frames = acc + 3 * PP;
+    pop->dev_flags = reinterpret_cast<int*>(acc + 3 * PP + 1);
+    pop->P = P;
+    return MALIB_OK;
+}
+
+malib_status malib_expansion_pairs(int32_t n_policies, int32_t first_new, int32_t per_pair,
+                                   int32_t n_agents, const int8_t* team, int32_t* out,
+                                   void* stream)
+{
+    if (!out)
+        return fail(MALIB_E_INVAL, "pair_assign_out is NULL");
+    if (n_policies < 1 || n_policies > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
+    if (first_new < 0 || first_new >= n_policies)
+        return fail(MALIB_E_INVAL, "first_new must be in [0, n_policies)");
+    if (per_pair < 1)
+        return fail(MALIB_E_INVAL, "per_pair must be >= 1");
+    if (n_agents < 2 || n_agents > kMaxAgents)
+        return fail(MALIB_E_INVAL, "n_agents must be in [2, %d]", kMaxAgents);
+    if (!team && n_agents != 2)
+        return fail(MALIB_E_INVAL, "team may be NULL only for two seats");
+    uint32_t row = 0, col = 0;
+    for (int k = 0; k < n_agents; ++k) {
+        const int t = team ? team[k] : (k == 0 ? 1 : -1);
+        if (t != 1 && t != -1)
+            return fail(MALIB_E_INVAL, "team entries must be +1 or -1");
+        (t > 0 ? row : col) |= 1u << k;
+    }
+    if (row == 0 || col == 0)
+        return fail(MALIB_E_INVAL, "both sides need at least one seat");
+    const int64_t cells = (int64_t)n_policies * n_policies - (int64_t)first_new * first_new;
+    const int64_t n_envs = cells * per_pair;
+    if (n_envs * n_agents > ((int64_t)1 << 26))
+        return fail(MALIB_E_INVAL, "the expansion batch exceeds 2^26 slots");
+    HIP_TRY(launch_expansion_pairs(n_policies, first_new, per_pair, n_agents, row, n_envs, out,
+                                   (hipStream_t)stream));
+    return MALIB_OK;
 }
 
 // ------------------------------------------------------------------ rollout

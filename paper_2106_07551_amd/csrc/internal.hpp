@@ -92,6 +92,15 @@ hipError_t launch_solve_fp(const double* M, int P, int T, float* sigma, double* 
 hipError_t launch_thresholds(const float* sigma, int n_sigma, int P, unsigned long long* thr,
                              hipStream_t s);
 
+// Incremental table expansion (k_expand.hip): the P0 x P0 accumulators copied
+// into a P x P table (new cells zero), and the policy ids of the batch that
+// simulates every cell with row or column >= first (row-major over the grid,
+// per_pair envs per cell; team_row: bit k set = seat k takes the row policy).
+hipError_t launch_remap_table(const unsigned long long* src, int P0, unsigned long long* dst,
+                              int P, hipStream_t s);
+hipError_t launch_expansion_pairs(int P, int first, int per_pair, int n_agents, uint32_t team_row,
+                                  int64_t n_envs, int32_t* out, hipStream_t s);
+
 // Meta-strategy sampling from precomputed thresholds [n_sigma][P].
 // seat_map: 4 bits per seat, the threshold row that seat draws from
 hipError_t launch_meta_sample(const unsigned long long* thr, uint32_t seat_map, int P,

@@ -650,3 +650,50 @@ def test_solve_fp_rock_paper_scissors_and_gap_definition():
     cx, cy, gap = oracle.solve_fp(R, 777)
     assert cx.sum() == 777 and cy.sum() == 777
     assert gap == pytest.approx(((R @ cy).max() - (cx @ R).min()) / 777, abs=1e-12)
+
+
+# ---------------------------------------------------- incremental expansion
+
+@pytest.mark.parametrize("P,f,per_pair", [(1, 0, 3), (4, 0, 5), (5, 3, 2), (7, 6, 1),
+                                           (9, 1, 2)])
+def test_expansion_pairs_cover_exactly_the_new_cells(P, f, per_pair):
+    """The expansion batch plays every cell of the grown grid that is outside
+    the old f x f block exactly per_pair times and no old cell; with no old
+    block it is the blocked all-pairs assignment (an independent generator)."""
+    team = np.array([1, -1], np.int8)
+    pairs = oracle.expansion_pairs(P, f, per_pair, team)
+    assert pairs.shape == ((P * P - f * f) * per_pair, 2)
+    grid = np.zeros((P, P), np.int64)
+    np.add.at(grid, (pairs[:, 0], pairs[:, 1]), 1)
+    want = np.full((P, P), per_pair)
+    want[:f, :f] = 0
+    assert np.array_equal(grid, want)
+    # row-major order of the cells, per_pair consecutive envs each
+    cells = pairs[::per_pair]
+    key = cells[:, 0] * P + cells[:, 1]
+    assert np.all(np.diff(key) > 0)
+    assert np.array_equal(pairs, np.repeat(cells, per_pair, axis=0))
+    if f == 0:
+        assert np.array_equal(pairs, W.blocked_pairs(P, per_pair))
+
+
+def test_expansion_merge_keeps_old_cells():
+    """A table filled with the P0 blocked pairs, grown, then filled with the
+    expansion batch: the old block keeps its sums and counts (the batch never
+    touches it) and every new cell gets the team game's seat pairs per env."""
+    rng = np.random.default_rng(4)
+    P0, P, per_pair = 3, 5, 4
+    team = np.array([1, 1, -1, -1, -1], np.int8)
+    p0 = W.blocked_pairs(P0, per_pair)
+    p0 = np.stack([p0[:, 0], p0[:, 0], p0[:, 1], p0[:, 1], p0[:, 1]], 1)
+    r0 = rng.standard_normal((len(p0), 5)).astype(np.float32)
+    p1 = oracle.expansion_pairs(P, P0, per_pair, team)
+    r1 = rng.standard_normal((len(p1), 5)).astype(np.float32)
+    m0, c0, s0, _ = oracle.payoff(r0, p0, team, P)
+    m1, c1, s1, _ = oracle.payoff(np.concatenate([r0, r1]), np.concatenate([p0, p1]), team, P)
+    assert np.array_equal(c1[:P0, :P0], c0[:P0, :P0])
+    assert np.array_equal(s1[:P0, :P0], s0[:P0, :P0])
+    new = np.ones((P, P), bool)
+    new[:P0, :P0] = False
+    assert (c1[new] == per_pair * 2 * 3).all()
+    assert (c0[new] == 0).all()
