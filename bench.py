@@ -198,6 +198,44 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
     return out
 
 
+def expansion_timing(M, IO, W, pop, env, wl, fill_ms):
+    """Growing the population by one policy and simulating only the new row
+    and column (2P + 1 cells) into the same table: malib_pop_extend, then
+    malib_expansion_pairs + rollout + table read-back.  Blocked workloads
+    play as many envs per new cell as the fill gives each cell; the sampled
+    ones (pursuit, team) per_pair = n_envs / P^2, at least 1.  The new
+    policy's weights come from the workload generator with one more policy."""
+    import numpy as np
+    import torch
+    n, na, P = wl.n_envs, wl.n_agents, wl.P
+    per_pair = max(1, n // (P * P))
+    big = W.make(wl.number, P=P + 1, **({"per_pair": per_pair} if wl.pairs is not None else {}))
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    if wl.pol_kind == W.TABULAR:
+        new = {"tab_logits": dev(big.tab_logits[P:])}
+    else:
+        new = {"weights": [dev(w[P:]) for w in big.weights],
+               "biases": [dev(b[P:]) for b in big.biases] if big.biases else None}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    pop.extend(1, **new)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pairs = M.expansion_pairs(P + 1, P, per_pair, na, wl.team)
+    n_new = pairs.shape[0]
+    pop.rollout(env, n_new, pairs, wl.seed, wl.horizon, env_offset=n)
+    tab = pop.payoff(reset=True)
+    t2 = time.perf_counter()
+    cells = (P + 1) ** 2 - P * P
+    return {"policies": f"{P} -> {P + 1}", "cells": cells, "per_pair": per_pair,
+            "envs": n_new, "extend_ms": round(1000.0 * (t1 - t0), 3),
+            "fill_ms": round(1000.0 * (t2 - t1), 3),
+            "agent_frames_per_s": round(tab["live_frames"] / (t2 - t1), 1),
+            "full_refill_cells": (P + 1) ** 2,
+            "full_fill_ms_at_P": round(fill_ms, 3)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -304,6 +342,7 @@ def main():
                 kern[name]["alu_frac"] = round(w["flops"] / t / 1e12 / PEAK_F32_ALU_TFLOPS, 4)
     pop.profile_enable(False)
     meta = meta_update_timing(M, pop, env, wl, pairs, args.fp_iters)
+    expand = expansion_timing(M, IO, W, pop, env, wl, 1000.0 * el / args.steps)
 
     ms_step = 1000.0 * el / args.steps
     value = frames / el
@@ -347,6 +386,7 @@ def main():
         "roofline": roof,
         "kernels": kern,
         "meta_update": meta,
+        "expansion": expand,
         "frames_per_step": frames // max(args.steps, 1),
     }
     if not args.no_cpu_baseline:
