@@ -239,6 +239,56 @@ def expansion_pairs(P, first_new, per_pair, team):
     return out
 
 
+def aggregate(M, sigma, br_row, br_col):
+    """Aggregate payoffs of a meta-strategy pair on the game M (the PSRO
+    convergence judgement of the example API's main loop, Appendix C.2):
+    x, y = the two weight rows of sigma (fp32) normalized in fp64; u = M y and
+    v = x^T M, each entry a sequential fp64 sum (products rounded, then
+    added); nash = x^T u (sequential).  Returns (nash payoff of the row side,
+    of the column side (= -nash, zero-sum), the row side's payoff of policy
+    br_row against y (u[br_row]), the column side's of br_col against x
+    (-v[br_col]), improvement = the larger gain of a best response over the
+    equilibrium payoff); a side with br = -1 is left out (NaN)."""
+    M = np.asarray(M, np.float64)
+    P = M.shape[0]
+    s = np.asarray(sigma, np.float32).reshape(2, P)
+    w0 = [float(a) for a in s[0]]
+    w1 = [float(a) for a in s[1]]
+    S0 = 0.0
+    S1 = 0.0
+    for a in w0:
+        S0 += a
+    for a in w1:
+        S1 += a
+    x = [a / S0 for a in w0]
+    y = [a / S1 for a in w1]
+    u = []
+    for i in range(P):
+        acc = 0.0
+        for j in range(P):
+            acc += float(M[i, j]) * y[j]
+        u.append(acc)
+    v = []
+    for j in range(P):
+        acc = 0.0
+        for i in range(P):
+            acc += x[i] * float(M[i, j])
+        v.append(acc)
+    nash = 0.0
+    for i in range(P):
+        nash += x[i] * u[i]
+    nan = float("nan")
+    w_row = u[br_row] if br_row >= 0 else nan
+    w_col = -v[br_col] if br_col >= 0 else nan
+    gains = []
+    if br_row >= 0:
+        gains.append(w_row - nash)
+    if br_col >= 0:
+        gains.append(w_col - (-nash))
+    improvement = max(gains) if gains else nan
+    return nash, -nash, w_row, w_col, improvement
+
+
 def payoff_matrix(mean):
     """The solver's game from a payoff table: the means, 0 where a cell has no
     simulations."""

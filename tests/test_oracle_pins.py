@@ -697,3 +697,46 @@ def test_expansion_merge_keeps_old_cells():
     new[:P0, :P0] = False
     assert (c1[new] == per_pair * 2 * 3).all()
     assert (c0[new] == 0).all()
+
+
+# ----------------------------------------------- aggregate / convergence
+
+def test_aggregate_matches_bilinear_forms():
+    """nash = x^T M y and the best-response payoffs (M y)[i], -(x^T M)[j],
+    against numpy's products (another summation order: 1e-13 relative)."""
+    rng = np.random.default_rng(12)
+    for P in (1, 3, 20, 200):
+        M = rng.normal(size=(P, P))
+        sig = (rng.random((2, P)) * 10).astype(np.float32)
+        sig[0, 0] += 1
+        sig[1, -1] += 1
+        x = sig[0].astype(np.float64) / sig[0].astype(np.float64).sum()
+        y = sig[1].astype(np.float64) / sig[1].astype(np.float64).sum()
+        for br in (0, P - 1):
+            nr, nc, wr, wc, imp = oracle.aggregate(M, sig, br, P - 1 - br)
+            tol = 1e-13 * max(1.0, np.abs(M).max())
+            assert abs(nr - x @ M @ y) <= tol and nc == -nr
+            assert abs(wr - (M @ y)[br]) <= tol
+            assert abs(wc + (x @ M)[P - 1 - br]) <= tol
+            assert imp == max(wr - nr, wc - nc)
+
+
+def test_aggregate_equilibria_and_a_hand_case():
+    # rock-paper-scissors at the uniform equilibrium: every payoff is 0
+    R = np.array([[0, -1, 1], [1, 0, -1], [-1, 1, 0]], np.float64)
+    for br in range(3):
+        out = oracle.aggregate(R, np.ones((2, 3), np.float32), br, br)
+        assert out[0] == 0.0 and out[2] == 0.0 and out[3] == 0.0 and out[4] == 0.0
+    # a 2x2 game with the mixed equilibrium x = (3/4, 1/4), y = (1/2, 1/2),
+    # value 1/2: no pure deviation gains
+    G = np.array([[1.0, 0.0], [-1.0, 2.0]])
+    out = oracle.aggregate(G, np.array([[3, 1], [1, 1]], np.float32), 1, 0)
+    assert abs(out[0] - 0.5) < 1e-15 and abs(out[4]) < 1e-15
+    # pure profile (0, 0) of [[1, 0], [0, 2]]: nash 1; the row side's policy 1
+    # earns 0 (gain -1), the column side's policy 1 pays 0 instead of 1 (gain 1)
+    H = np.array([[1.0, 0.0], [0.0, 2.0]])
+    nr, nc, wr, wc, imp = oracle.aggregate(H, np.array([[1, 0], [1, 0]], np.float32), 1, 1)
+    assert (nr, nc, wr, wc, imp) == (1.0, -1.0, 0.0, 0.0, 1.0)
+    # one side left out
+    out = oracle.aggregate(H, np.array([[1, 0], [1, 0]], np.float32), -1, 1)
+    assert np.isnan(out[2]) and out[4] == 1.0
