@@ -157,10 +157,11 @@ def cpu_baseline(wl, budget_s=12.0, max_s=30.0):
 
 def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
     """The meta-update after a fill, on the device: the table as a game
-    (malib_payoff_matrix), `iters` steps of fictitious play (malib_solve_fp)
-    and the next policy ids drawn from the play counts, row side's counts for
+    (malib_payoff_matrix), `iters` steps of fictitious play (malib_solve_fp),
+    the next policy ids drawn from the play counts, row side's counts for
     the row-side seats and the column side's for the others
-    (malib_meta_sample_device).  Each stage timed with HIP events on the
+    (malib_meta_sample_device), and the convergence figures of the last
+    policy against the averages (malib_aggregate).  Each stage timed with HIP events on the
     stream it runs on, averaged over `reps` calls, after one untimed fill that
     leaves the table full."""
     import torch
@@ -173,11 +174,13 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
     sigma = torch.empty((2, P), dtype=torch.float32, device="cuda")
     gap = torch.empty(1, dtype=torch.float64, device="cuda")
     ids = torch.empty((n, na), dtype=torch.int32, device="cuda")
+    agg = torch.empty(5, dtype=torch.float64, device="cuda")
     stages = {
         "payoff_matrix": lambda: pop.payoff_matrix(out=game),
         "solve_fp": lambda: M.solve_fp(game, iters, sigma=sigma, gap=gap),
         "meta_sample_device": lambda: M.meta_sample_device(sigma, P, n, na, wl.seed + 1,
                                                            seat_row=seat_row, out=ids),
+        "aggregate": lambda: M.aggregate(game, sigma, P - 1, P - 1, out=agg),
     }
     out = {"fp_iterations": iters, "policies": P, "envs": n}
     for name, fn in stages.items():
@@ -194,6 +197,7 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
     out["solve_fp_ns_per_iteration"] = round(1000.0 * out["solve_fp_us"] / iters, 1)
     out["total_us"] = round(sum(out[k + "_us"] for k in stages), 2)
     out["gap"] = float(gap.cpu()[0])
+    out["improvement_of_policy_P-1"] = float(agg.cpu()[4])
     pop.payoff(reset=True)
     return out
 

@@ -308,6 +308,28 @@ malib_status malib_solve_fp(const double* M, int32_t n_policies, int32_t iterati
                             float* sigma, double* gap, void* stream);
 
 /*
+ * Aggregate payoffs of a meta-strategy pair on a game, for the PSRO
+ * convergence judgement of the example API's main loop (Appendix C.2:
+ * aggregate(equilibrium) and aggregate(equilibrium, brs), then the
+ * evaluator's convergence test).
+ *  M:      device fp64 [P][P] (e.g. from malib_payoff_matrix).
+ *  sigma:  device fp32 [2][P] weight rows (e.g. malib_solve_fp's counts):
+ *          x = sigma[0] / sum, y = sigma[1] / sum, in fp64.
+ *  br_row, br_col: the sides' best-response (newly trained) policy ids, or
+ *          -1 to leave that side out.
+ *  out:    device fp64 [5]: {x^T M y (row side's equilibrium payoff),
+ *          -x^T M y (column side's), (M y)[br_row], -(x^T M)[br_col],
+ *          improvement = the larger of the sides' best-response gains over
+ *          their equilibrium payoffs}; NaN for a side left out.  Sums are
+ *          sequential in index order (u = M y row by row, then x^T u).
+ *          A converged meta-game has improvement <= a caller's tolerance.
+ * Weights are not checked: a row without positive finite mass gives NaN.
+ * Asynchronous on `stream`; one workgroup.
+ */
+malib_status malib_aggregate(const double* M, int32_t n_policies, const float* sigma,
+                             int32_t br_row, int32_t br_col, double* out, void* stream);
+
+/*
  * malib_meta_sample with the weights on the device (e.g. from malib_solve_fp),
  * same draws and the same fp64 thresholds.
  *  sigma:    device fp32 [n_sigma][n_policies] weight rows.

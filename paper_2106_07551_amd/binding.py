@@ -26,7 +26,7 @@ EXPORTS = [
     "malib_meta_sample", "malib_last_error", "malib_profile_enable", "malib_profile_read",
     "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
-    "malib_pop_extend", "malib_expansion_pairs",
+    "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate",
 ]
 
 
@@ -101,6 +101,8 @@ def lib():
         L.malib_solve_fp.restype = i32
         L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, vp, u64, i64, vp, vp]
         L.malib_meta_sample_device.restype = i32
+        L.malib_aggregate.argtypes = [vp, i32, vp, i32, i32, vp, vp]
+        L.malib_aggregate.restype = i32
         L.malib_pop_extend.argtypes = [vp, vp, vp]
         L.malib_pop_extend.restype = i32
         L.malib_expansion_pairs.argtypes = [i32, i32, i32, i32, vp, vp, vp]
@@ -311,6 +313,20 @@ def solve_fp(M, iterations: int, *, sigma=None, gap=None, stream=None):
     _check(lib().malib_solve_fp(_dptr(M), P, iterations, _dptr(sigma), _dptr(gap),
                                 _stream(stream)))
     return sigma, gap
+
+
+def aggregate(M, sigma, br_row: int = -1, br_col: int = -1, *, out=None, stream=None):
+    """malib_aggregate: device fp64 [5] = (nash payoff of the row side, of
+    the column side, best-response payoff of br_row, of br_col, improvement)."""
+    import torch
+    P = M.shape[0]
+    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
+    assert sigma.dtype == torch.float32 and sigma.is_contiguous() and sigma.numel() == 2 * P
+    if out is None:
+        out = torch.empty(5, dtype=torch.float64, device=M.device)
+    _check(lib().malib_aggregate(_dptr(M), P, _dptr(sigma), br_row, br_col, _dptr(out),
+                                 _stream(stream)))
+    return out
 
 
 def meta_sample_device(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *,

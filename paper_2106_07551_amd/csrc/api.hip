@@ -828,6 +828,19 @@ malib_status malib_solve_fp(const double* M, int32_t P, int32_t iterations, floa
     return MALIB_OK;
 }
 
+malib_status malib_aggregate(const double* M, int32_t P, const float* sigma, int32_t br_row,
+                             int32_t br_col, double* out, void* stream)
+{
+    if (!M || !sigma || !out)
+        return fail(MALIB_E_INVAL, "M, sigma and out must not be NULL");
+    if (P < 1 || P > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
+    if (br_row < -1 || br_row >= P || br_col < -1 || br_col >= P)
+        return fail(MALIB_E_INVAL, "best-response ids must be in [-1, n_policies)");
+    HIP_TRY(launch_aggregate(M, P, sigma, br_row, br_col, out, (hipStream_t)stream));
+    return MALIB_OK;
+}
+
 malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32_t P,
                                       int64_t n_envs, int32_t n_agents, const int32_t* seat_row,
                                       uint64_t seed, int64_t env_offset, int32_t* out,

@@ -91,6 +91,8 @@ hipError_t launch_solve_fp(const double* M, int P, int T, float* sigma, double* 
                            hipStream_t s);
 hipError_t launch_thresholds(const float* sigma, int n_sigma, int P, unsigned long long* thr,
                              hipStream_t s);
+hipError_t launch_aggregate(const double* M, int P, const float* sigma, int br_row, int br_col,
+                            double* out, hipStream_t s);
 
 // Incremental table expansion (k_expand.hip): the P0 x P0 accumulators copied
 // into a P x P table (new cells zero), and the policy ids of the batch that

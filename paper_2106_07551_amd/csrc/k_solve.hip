@@ -218,6 +218,76 @@ hipError_t launch_solve_fp(const double* M, int P, int T, float* sigma, double* 
     return hipGetLastError();
 }
 
+// Aggregate payoffs of a meta-strategy pair (the PSRO convergence judgement):
+// x, y = the weight rows sigma[0], sigma[1] normalized in fp64 (sequential
+// sums); u = M y and v = x^T M, each entry a sequential fp64 sum of rounded
+// products (thread k forms u[k] over row k and v[k] over column k); nash =
+// x^T u (sequential).  out = {nash, -nash, u[br_row], -v[br_col],
+// improvement}, where improvement is the larger best-response gain of the
+// sides whose br is >= 0 (a side with br = -1 gives NaN).
+__global__ __launch_bounds__(kMaxP) void aggregate_kernel(const double* __restrict__ M, int P,
+                                                          const float* __restrict__ sigma,
+                                                          int br_row, int br_col,
+                                                          double* __restrict__ out)
+{
+    __shared__ double x[kMaxP], y[kMaxP], u[kMaxP];
+    __shared__ double S[2], vbr;
+    const int k = threadIdx.x;
+    if (k == 0) {
+        double a = 0.0, b = 0.0;
+        for (int m = 0; m < P; ++m)
+            a += (double)sigma[m];
+        for (int m = 0; m < P; ++m)
+            b += (double)sigma[P + m];
+        S[0] = a;
+        S[1] = b;
+    }
+    __syncthreads();
+    if (k < P) {
+        x[k] = (double)sigma[k] / S[0];
+        y[k] = (double)sigma[P + k] / S[1];
+    }
+    __syncthreads();
+    if (k < P) {
+        double acc = 0.0;
+        for (int j = 0; j < P; ++j)
+            acc = acc + M[(size_t)k * P + j] * y[j];
+        u[k] = acc;
+        double accv = 0.0;
+        for (int i = 0; i < P; ++i)
+            accv = accv + x[i] * M[(size_t)i * P + k];
+        if (k == br_col)
+            vbr = accv;
+    }
+    __syncthreads();
+    if (k == 0) {
+        double nash = 0.0;
+        for (int i = 0; i < P; ++i)
+            nash = nash + x[i] * u[i];
+        const double wr = br_row >= 0 ? u[br_row] : (double)NAN;
+        const double wc = br_col >= 0 ? -vbr : (double)NAN;
+        double imp = (double)NAN;
+        if (br_row >= 0)
+            imp = wr - nash;
+        if (br_col >= 0) {
+            const double g = wc - (-nash);
+            imp = (br_row < 0 || g > imp) ? g : imp;
+        }
+        out[0] = nash;
+        out[1] = -nash;
+        out[2] = wr;
+        out[3] = wc;
+        out[4] = imp;
+    }
+}
+
+hipError_t launch_aggregate(const double* M, int P, const float* sigma, int br_row, int br_col,
+                            double* out, hipStream_t s)
+{
+    aggregate_kernel<<<1, kMaxP, 0, s>>>(M, P, sigma, br_row, br_col, out);
+    return hipGetLastError();
+}
+
 // Thresholds of meta-sampling from device weights, the same fp64 arithmetic as
 // the host path: T_m = floor(C_m / C_{P-1} * 2^32) from the sequential fp64
 // cumulative sum C of row r, T_{P-1} = 2^32.  A row with a negative or

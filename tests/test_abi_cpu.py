@@ -79,6 +79,16 @@ def test_validation_before_device_work():
     assert L.malib_solve_fp(dev, 257, 10, dev, None, None) == B.E_INVAL
     assert L.malib_solve_fp(None, 4, 10, dev, None, None) == B.E_INVAL
     assert L.malib_payoff_matrix(None, dev, None) == B.E_INVAL
+    assert L.malib_aggregate(dev, 4, dev, 4, 0, dev, None) == B.E_INVAL
+    assert L.malib_aggregate(dev, 4, dev, 0, -2, dev, None) == B.E_INVAL
+    assert L.malib_aggregate(dev, 0, dev, 0, 0, dev, None) == B.E_INVAL
+    assert L.malib_aggregate(None, 4, dev, 0, 0, dev, None) == B.E_INVAL
+    assert L.malib_expansion_pairs(4, 4, 1, 2, None, out, None) == B.E_INVAL
+    assert L.malib_expansion_pairs(4, 1, 0, 2, None, out, None) == B.E_INVAL
+    assert L.malib_expansion_pairs(4, 1, 1, 3, None, out, None) == B.E_INVAL
+    bad_team = np.array([1, 1], np.int8)
+    assert L.malib_expansion_pairs(4, 1, 1, 2, bad_team.ctypes.data, out, None) == B.E_INVAL
+    assert L.malib_pop_extend(None, None, None) == B.E_INVAL
     assert L.malib_profile_enable(None, 1, 1) == B.E_INVAL
     assert L.malib_debug_tanh_ref(None, None, 4, None) == B.E_INVAL
 

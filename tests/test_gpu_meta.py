@@ -255,3 +255,46 @@ def test_meta_update_loop_closed_on_device(c, iters, T):
         assert np.array_equal(ids.cpu().numpy(), o_ids), k
     assert pop.payoff()["status"] == 0
     pop.close()
+
+
+@pytest.mark.parametrize("P", [1, 2, 17, 128, 256])
+def test_aggregate_matches_oracle(P):
+    """Aggregate payoffs bit for bit (the same sequential fp64 sums on both
+    sides), on count-weighted and sparse meta-strategies."""
+    import paper_2106_07551_amd as M
+    rng = np.random.default_rng(300 + P)
+    Mx = rng.normal(size=(P, P))
+    sig = np.floor(rng.random((2, P)) * 40).astype(np.float32)
+    sig[0, 0] += 1
+    sig[1, P // 2] += 1
+    if P > 4:
+        sig[:, 1::3] = 0
+    Md = torch.from_numpy(Mx).cuda()
+    sd = torch.from_numpy(sig).cuda()
+    for br_row, br_col in ((0, P - 1), (P - 1, 0), (-1, P // 2), (P // 3, -1), (-1, -1)):
+        g = M.aggregate(Md, sd, br_row, br_col).cpu().numpy()
+        ref = np.array(oracle.aggregate(Mx, sig, br_row, br_col))
+        same = (g.view(np.uint64) == ref.view(np.uint64)) | (np.isnan(g) & np.isnan(ref))
+        assert same.all(), (br_row, br_col, g, ref)
+
+
+def test_psro_convergence_on_device():
+    """Rock-paper-scissors extended by one dominated policy: fictitious play
+    on the device, then the aggregate payoffs of its averages; the new
+    policy's gain is negative and the improvement shrinks with more steps."""
+    import paper_2106_07551_amd as M
+    R = np.array([[0, -1, 1, 2], [1, 0, -1, 2], [-1, 1, 0, 2], [-2, -2, -2, 0]], np.float64)
+    Md = torch.from_numpy(R).cuda()
+    worst = []
+    for T in (10, 100, 1000, 10000):
+        sig, gap = M.solve_fp(Md, T)
+        out = M.aggregate(Md, sig, 3, 3).cpu().numpy()
+        ref = oracle.aggregate(R, sig.cpu().numpy(), 3, 3)
+        assert np.array_equal(out.view(np.uint64), np.array(ref).view(np.uint64))
+        assert out[2] - out[0] < 0 and out[3] - out[1] < 0
+        # no single best response gains more than the exploitability of the
+        # averages (which adds both sides' best gains)
+        imp = max(float(M.aggregate(Md, sig, br, br).cpu()[4]) for br in range(4))
+        assert imp <= float(gap.cpu()[0]) + 1e-12
+        worst.append(imp)
+    assert worst[-1] < worst[0] and worst[-1] < 0.02
