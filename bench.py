@@ -155,6 +155,39 @@ def cpu_baseline(wl, budget_s=12.0, max_s=30.0):
             "cpu": platform.processor() or platform.machine()}
 
 
+def trajectory_timing(M, pop, env, wl, pairs, fill_ms, reps=2):
+    """Fills that also write every step's records (actions, reward, flags and
+    the compact observation) into a device ring holding the whole fill
+    (malib_rollout_batch_traj), timed like the fills, beside the fill time
+    without records."""
+    import torch
+    import workloads as W
+    n, na, H = wl.n_envs, wl.n_agents, wl.horizon
+    obs = {W.ITER_MATRIX: ((), torch.int16, 2), W.PURSUIT: ((2,), torch.uint8, 2),
+           W.FEATURE: ((wl.d,), torch.int16, 2 * wl.d)}.get(wl.env_kind, (None, None, 0))
+    cap = H * n
+    tr = M.Traj(cap, na, obs_shape=obs[0], obs_dtype=obs[1])
+    def fill():
+        if wl.pairs is None:
+            M.meta_sample(wl.sigma, wl.P, n, na, wl.seed, out=pairs)
+        pop.rollout_traj(env, n, pairs, wl.seed, H, tr)
+        return pop.payoff(reset=True)
+    fill()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fill()
+    torch.cuda.synchronize()
+    ms = 1000.0 * (time.perf_counter() - t0) / reps
+    rec_bytes = na + 4 + 1 + obs[2]
+    out = {"records": cap, "bytes_per_record": rec_bytes,
+           "ring_bytes": cap * rec_bytes, "fill_ms_with_records": round(ms, 3),
+           "fill_ms_without": round(fill_ms, 3),
+           "overhead_frac": round(ms / fill_ms - 1.0, 4)}
+    del tr
+    return out
+
+
 def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
     """The meta-update after a fill, on the device: the table as a game
     (malib_payoff_matrix), `iters` steps of fictitious play (malib_solve_fp),
@@ -345,6 +378,7 @@ def main():
                 kern[name]["fp32_TFLOPs"] = round(w["flops"] / t / 1e12, 2)
                 kern[name]["alu_frac"] = round(w["flops"] / t / 1e12 / PEAK_F32_ALU_TFLOPS, 4)
     pop.profile_enable(False)
+    traj = trajectory_timing(M, pop, env, wl, pairs, 1000.0 * el / args.steps)
     meta = meta_update_timing(M, pop, env, wl, pairs, args.fp_iters)
     expand = expansion_timing(M, IO, W, pop, env, wl, 1000.0 * el / args.steps)
 
@@ -389,6 +423,7 @@ def main():
         "config": describe(wl),
         "roofline": roof,
         "kernels": kern,
+        "trajectory": traj,
         "meta_update": meta,
         "expansion": expand,
         "frames_per_step": frames // max(args.steps, 1),

@@ -197,6 +197,49 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env,
                                  uint64_t seed, int64_t env_offset, int32_t horizon,
                                  float* returns, const malib_trace* trace, void* stream);
 
+/* ------------------------------------------------------ trajectory records */
+
+/*
+ * A device ring of per-step records for learners (the Actors' samples that
+ * the paper's offline dataset server stores, Sec. 3.1 and Sec. 3.2; the
+ * per-agent episode buffer of the example API, Appendix C.2).  One record per
+ * (step t, env e) of a batch, at index (cursor + t * n_envs + e) mod capacity;
+ * older records are overwritten once the ring wraps.  All buffers are
+ * caller-owned device memory:
+ *  actions:  uint8 [capacity][n_agents], each seat's action; 255 where the
+ *            env had already finished (no action).
+ *  rewards:  fp32 [capacity], the row side's (team +1) reward of the step;
+ *            the column side receives its negation.
+ *  flags:    uint8 [capacity]: bit 0 the episode terminated at this step
+ *            (pursuit capture), bit 1 the last step of the horizon, bit 2
+ *            the env had finished before this step.
+ *  obs:      NULL or the state every seat observed before the step, in
+ *            compact form: ITER_MATRIX uint16 [capacity] (the history as in
+ *            malib_trace's states), PURSUIT uint8 [capacity][2] (pursuer and
+ *            evader cell), FEATURE bf16 [capacity][d] (bf16_rne(s), exactly
+ *            the policy input), MATRIX nothing (not written).
+ *  cursor:   records written so far; malib_rollout_batch_traj advances it by
+ *            horizon * n_envs.
+ */
+typedef struct {
+    uint8_t* actions;
+    float* rewards;
+    uint8_t* flags;
+    void* obs;
+    int64_t capacity;
+    int64_t cursor;
+} malib_traj;
+
+/*
+ * malib_rollout_batch that also writes every step's records into `traj`
+ * (written by the env-step kernels as they step; nothing else changes: the
+ * same returns, table and random streams).
+ */
+malib_status malib_rollout_batch_traj(malib_pop_t pop, const malib_env_desc* env,
+                                      int64_t n_envs, const int32_t* pair_assign, uint64_t seed,
+                                      int64_t env_offset, int32_t horizon, float* returns,
+                                      malib_traj* traj, void* stream);
+
 /* ------------------------------------------------------------- payoff table */
 
 typedef struct {

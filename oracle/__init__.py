@@ -92,7 +92,7 @@ def lib():
         L.ora_rollout.restype = C.c_int
         L.ora_rollout.argtypes = [C.POINTER(Config), C.c_int64, C.c_void_p, C.c_void_p,
                                   C.c_void_p, C.c_double, C.c_void_p, C.c_void_p,
-                                  C.c_void_p, C.c_void_p, C.c_void_p]
+                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         L.ora_state_elems.restype = C.c_int64
         L.ora_state_elems.argtypes = [C.c_int32, C.c_int32]
         L.ora_obs_iter.argtypes = [C.c_void_p, C.c_int32, C.c_void_p]
@@ -354,7 +354,8 @@ def state_shape(wl, n):
 
 
 def rollout(wl, env_idx, pids, *, forced=None, tol=None, horizon=None, env_offset=0,
-            want_actions=False, want_logits=False, want_states=False, init_mode=None):
+            want_actions=False, want_logits=False, want_states=False, want_rewards=False,
+            init_mode=None):
     """Roll out the selected envs (local indices ``env_idx`` of a batch that
     starts at global env ``env_offset``) with per-env policy ids ``pids``
     [n_sel][n_agents].  ``forced`` is an action log [H][n_sel][n_agents] to
@@ -377,12 +378,15 @@ def rollout(wl, env_idx, pids, *, forced=None, tol=None, horizon=None, env_offse
         if shp is not None:
             states = np.zeros((H,) + shp, dt)
     stats = np.zeros(7, np.int64)
+    rews = np.zeros((H, n, wl.n_agents), np.float32) if want_rewards else None
     rc = lib().ora_rollout(C.byref(cfg.cfg), n, _ptr(idx), _ptr(p), _ptr(f), float(tol),
-                           _ptr(ret), _ptr(acts), _ptr(logits), _ptr(states), _ptr(stats))
+                           _ptr(ret), _ptr(acts), _ptr(logits), _ptr(states), _ptr(stats),
+                           _ptr(rews))
     if rc != 0:
         raise RuntimeError(f"ora_rollout failed ({rc})")
     return {
         "returns": ret, "actions": acts, "logits": logits, "states": states,
+        "rewards": rews,
         "near_ties": int(stats[0]), "flips": int(stats[1]), "fails": int(stats[2]),
         "live_frames": int(stats[3]),
         "first_fail": tuple(int(x) for x in stats[4:7]),

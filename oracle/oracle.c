@@ -699,7 +699,7 @@ int64_t ora_state_elems(int32_t env_kind, int32_t d)
 int ora_rollout(const ora_config* c, int64_t n_sel, const int64_t* env_idx,
                 const int32_t* pids, const uint8_t* forced, double tol,
                 float* returns, uint8_t* actions, float* logits, void* states,
-                int64_t* stats)
+                int64_t* stats, float* step_rewards)
 {
     int n = c->n_agents, A = c->n_actions, H = c->horizon;
     if (n <= 0 || A <= 0 || A > 64 || H < 0 || (c->pol_kind != POL_TABULAR && c->dims[c->n_layers] != A))
@@ -807,6 +807,9 @@ int ora_rollout(const ora_config* c, int64_t n_sel, const int64_t* env_idx,
             if (G)
                 for (int k = 0; k < n; ++k)
                     G[k] = G[k] + r[k];
+            if (step_rewards)
+                for (int k = 0; k < n; ++k)
+                    step_rewards[((size_t)t * n_sel + i) * n + k] = r[k];
         }
     }
     free(obs);

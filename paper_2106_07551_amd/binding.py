@@ -26,7 +26,7 @@ EXPORTS = [
     "malib_meta_sample", "malib_last_error", "malib_profile_enable", "malib_profile_read",
     "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
-    "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate",
+    "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate", "malib_rollout_batch_traj",
 ]
 
 
@@ -54,6 +54,11 @@ class TraceDesc(C.Structure):
     _fields_ = [("actions", C.c_void_p), ("n_snap", C.c_int32),
                 ("snap_steps", C.POINTER(C.c_int32)), ("logits", C.c_void_p),
                 ("states", C.c_void_p), ("perm", C.c_void_p), ("offsets", C.c_void_p)]
+
+
+class TrajDesc(C.Structure):
+    _fields_ = [("actions", C.c_void_p), ("rewards", C.c_void_p), ("flags", C.c_void_p),
+                ("obs", C.c_void_p), ("capacity", C.c_int64), ("cursor", C.c_int64)]
 
 
 class EvalStats(C.Structure):
@@ -101,6 +106,9 @@ def lib():
         L.malib_solve_fp.restype = i32
         L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, vp, u64, i64, vp, vp]
         L.malib_meta_sample_device.restype = i32
+        L.malib_rollout_batch_traj.argtypes = [vp, C.POINTER(EnvDesc), i64, vp, u64, i64, i32,
+                                               vp, C.POINTER(TrajDesc), vp]
+        L.malib_rollout_batch_traj.restype = i32
         L.malib_aggregate.argtypes = [vp, i32, vp, i32, i32, vp, vp]
         L.malib_aggregate.restype = i32
         L.malib_pop_extend.argtypes = [vp, vp, vp]
@@ -193,6 +201,14 @@ class Population:
             horizon, _dptr(returns), C.byref(tr) if tr is not None else None,
             _stream(stream)))
 
+    def rollout_traj(self, env: "Env", n_envs: int, pair_assign, seed: int, horizon: int,
+                     traj: Traj, *, env_offset: int = 0, returns=None, stream=None):
+        """malib_rollout_batch_traj: a rollout that also writes its per-step
+        records into `traj` (advancing its cursor)."""
+        _check(lib().malib_rollout_batch_traj(
+            self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
+            horizon, _dptr(returns), C.byref(traj.desc), _stream(stream)))
+
     def payoff_matrix(self, out=None, stream=None):
         """malib_payoff_matrix: the table's means as a device fp64 [P][P] game
         (0 for empty cells)."""
@@ -251,6 +267,30 @@ class Env:
         e.A, e.W, e.emb, e.u = _dptr(A), _dptr(W), _dptr(emb), _dptr(u)
         self.desc = e
         self.n_agents = n_agents
+
+
+class Traj:
+    """A device ring of per-step records (malib_traj): actions [cap][n_agents]
+    uint8, rewards [cap] fp32, flags [cap] uint8 and, optionally, obs in the
+    environment's compact form (see malib.h)."""
+
+    def __init__(self, capacity: int, n_agents: int, *, obs_shape=None, obs_dtype=None,
+                 device="cuda"):
+        import torch
+        self.capacity = capacity
+        self.actions = torch.empty((capacity, n_agents), dtype=torch.uint8, device=device)
+        self.rewards = torch.empty(capacity, dtype=torch.float32, device=device)
+        self.flags = torch.empty(capacity, dtype=torch.uint8, device=device)
+        self.obs = None
+        if obs_shape is not None:
+            self.obs = torch.empty((capacity,) + tuple(obs_shape), dtype=obs_dtype,
+                                   device=device)
+        self.desc = TrajDesc(_dptr(self.actions), _dptr(self.rewards), _dptr(self.flags),
+                             _dptr(self.obs), capacity, 0)
+
+    @property
+    def cursor(self) -> int:
+        return self.desc.cursor
 
 
 class Trace:

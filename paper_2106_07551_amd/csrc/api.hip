@@ -448,10 +448,10 @@ malib_status malib_expansion_pairs(int32_t n_policies, int32_t first_new, int32_
 
 // ------------------------------------------------------------------ rollout
 
-malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
+static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
                                  const int32_t* pair_assign, uint64_t seed, int64_t env_offset,
                                  int32_t horizon, float* returns, const malib_trace* trace,
-                                 void* stream)
+                                 const malib_traj* traj, void* stream)
 {
     if (!pop)
         return fail(MALIB_E_INVAL, "pop is NULL");
@@ -598,6 +598,15 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
     }
     ea.WT = (const float*)pop->wt.ptr;
     ea.obs = bf16_obs ? (uint16_t*)pop->obs.ptr : nullptr;
+    if (traj) {
+        ea.tr.act = traj->actions;
+        ea.tr.rew = traj->rewards;
+        ea.tr.flags = traj->flags;
+        ea.tr.obs = env->kind == MALIB_ENV_MATRIX ? nullptr : traj->obs;
+        ea.tr.base = traj->cursor % traj->capacity;
+        ea.tr.cap = traj->capacity;
+        ea.tr.horizon = horizon;
+    }
     float* ret = (float*)pop->ret.ptr;
     float* logits = (float*)pop->logits.ptr;
     uint8_t* done = env->kind == MALIB_ENV_PURSUIT ? (uint8_t*)pop->done.ptr : nullptr;
@@ -686,6 +695,33 @@ malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int
         pop->host_frames += ns * (int64_t)horizon;
     pop->envs += n_envs;
     return MALIB_OK;
+}
+
+malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
+                                 const int32_t* pair_assign, uint64_t seed, int64_t env_offset,
+                                 int32_t horizon, float* returns, const malib_trace* trace,
+                                 void* stream)
+{
+    return rollout_impl(pop, env, n_envs, pair_assign, seed, env_offset, horizon, returns, trace,
+                        nullptr, stream);
+}
+
+malib_status malib_rollout_batch_traj(malib_pop_t pop, const malib_env_desc* env,
+                                      int64_t n_envs, const int32_t* pair_assign, uint64_t seed,
+                                      int64_t env_offset, int32_t horizon, float* returns,
+                                      malib_traj* traj, void* stream)
+{
+    if (!traj)
+        return fail(MALIB_E_INVAL, "traj is NULL");
+    if (!traj->actions || !traj->rewards || !traj->flags)
+        return fail(MALIB_E_INVAL, "traj: actions, rewards and flags must not be NULL");
+    if (traj->capacity < 1 || traj->cursor < 0)
+        return fail(MALIB_E_INVAL, "traj: capacity must be >= 1 and cursor >= 0");
+    const malib_status st = rollout_impl(pop, env, n_envs, pair_assign, seed, env_offset,
+                                         horizon, returns, nullptr, traj, stream);
+    if (st == MALIB_OK)
+        traj->cursor += (int64_t)horizon * n_envs;
+    return st;
 }
 
 // ------------------------------------------------------------------- payoff

@@ -122,6 +122,18 @@ struct SampleArgs {
     int* flags;
 };
 
+// Trajectory records written by the env-step kernels (all null: none).
+// Record of step t of local env e: (base + t * n_envs + e) mod cap.
+struct TrajArgs {
+    uint8_t* act = nullptr;    // [cap][n_agents], 255 = no action (finished env)
+    float* rew = nullptr;      // [cap] the row side's reward of the step
+    uint8_t* flags = nullptr;  // [cap] bit 0 terminal, bit 1 last step, bit 2 finished before
+    void* obs = nullptr;       // [cap][...] the state before the step, compact (or null)
+    int64_t base = 0;
+    int64_t cap = 1;
+    int horizon = 0;
+};
+
 // Environment kernels.
 struct EnvArgs {
     int kind, n_agents, A, grid, d, init_mode;
@@ -136,6 +148,7 @@ struct EnvArgs {
     // [n_envs][d], written by reset and by each step next to the fp32 state
     // (the policy forward gathers these rows: half the bytes, no conversion)
     uint16_t* obs;
+    TrajArgs tr;
 };
 hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,
                         void* state, uint8_t* done, hipStream_t s);

@@ -12,6 +12,12 @@
 
 namespace malib {
 
+__device__ __forceinline__ int64_t traj_rec(const TrajArgs& tr, int t, int64_t n, int64_t e)
+{
+    return (tr.base + (int64_t)t * n + e) % tr.cap;
+}
+
+
 // ---------------------------------------------------------------- reset
 
 __global__ void reset_iter_kernel(uint16_t* __restrict__ hist, int64_t n)
@@ -131,7 +137,7 @@ __device__ __forceinline__ void sample_pair(const SampleArgs& sa, int A, int64_t
 // r0 = A[a0][a1], r1 = -r0; ITER also shifts the joint action into its history.
 template <int AMAX>
 __global__ void step_matrix_kernel(const float* __restrict__ Amat, int A, int iter, int64_t n,
-                                   SampleArgs sa, uint16_t* __restrict__ hist,
+                                   SampleArgs sa, TrajArgs tr, uint16_t* __restrict__ hist,
                                    float* __restrict__ ret)
 {
     int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -142,9 +148,17 @@ __global__ void step_matrix_kernel(const float* __restrict__ Amat, int A, int it
     float v = Amat[a0 * A + a1];
     ret[e] = ret[e] + v;
     ret[n + e] = ret[n + e] + (-v);
-    if (iter) {
-        uint32_t h = hist[e];
+    const uint32_t h = iter ? hist[e] : 0u;
+    if (iter)
         hist[e] = (uint16_t)(((h << 4) | (uint32_t)(a0 * 3 + a1)) & 0xFFFFu);
+    if (tr.act) {
+        const int64_t r = traj_rec(tr, sa.t, n, e);
+        tr.act[2 * r] = (uint8_t)a0;
+        tr.act[2 * r + 1] = (uint8_t)a1;
+        tr.rew[r] = v;
+        tr.flags[r] = sa.t == tr.horizon - 1 ? 2 : 0;
+        if (iter && tr.obs)
+            ((uint16_t*)tr.obs)[r] = (uint16_t)h;
     }
 }
 
@@ -169,8 +183,8 @@ __device__ __forceinline__ uint32_t torus_move(uint32_t cell, int a, int grid)
 // -1, env done.  Finished envs take no action (logged as 255).  Counts live
 // agent-frames (two per live env) with one atomic per workgroup.
 __global__ __launch_bounds__(256) void step_pursuit_kernel(
-    int grid, int64_t n, SampleArgs sa, uint8_t* __restrict__ pos, uint8_t* __restrict__ done,
-    float* __restrict__ ret, unsigned long long* frames)
+    int grid, int64_t n, SampleArgs sa, TrajArgs tr, uint8_t* __restrict__ pos,
+    uint8_t* __restrict__ done, float* __restrict__ ret, unsigned long long* frames)
 {
     __shared__ int live_s;
     if (threadIdx.x == 0)
@@ -192,15 +206,31 @@ __global__ __launch_bounds__(256) void step_pursuit_kernel(
         atomicOr(sa.flags, kErrNaN);
     if (valid && sa.log)
         sa.log[slot] = live ? (uint8_t)a : (uint8_t)255;
+    bool caught = false;
     if (live && seat == 0) {
         const uint32_t p1 = torus_move(p0, a, grid);
         const uint32_t q1 = torus_move(q0, a_other, grid);
         pos[e] = (uint8_t)p1;
         pos[n + e] = (uint8_t)q1;
         if (p1 == q1 || (p1 == q0 && q1 == p0)) {
+            caught = true;
             done[e] = 1;
             ret[e] = ret[e] + 1.0f;
             ret[n + e] = ret[n + e] + (-1.0f);
+        }
+    }
+    if (valid && tr.act) {
+        const int64_t r = traj_rec(tr, sa.t, n, e);
+        tr.act[2 * r + seat] = live ? (uint8_t)a : (uint8_t)255;
+        if (seat == 0) {
+            tr.rew[r] = caught ? 1.0f : 0.0f;
+            tr.flags[r] = (uint8_t)((caught ? 1 : 0) | (sa.t == tr.horizon - 1 ? 2 : 0) |
+                                    (dn ? 4 : 0));
+            if (tr.obs) {
+                uint8_t* o = (uint8_t*)tr.obs + 2 * r;
+                o[0] = (uint8_t)p0;
+                o[1] = (uint8_t)q0;
+            }
         }
     }
     const unsigned long long b = __ballot(live && seat == 0);
@@ -349,6 +379,8 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
                 atomicOr(sa.flags, kErrNaN);
             if (sa.log)
                 sa.log[slot] = (uint8_t)a;
+            if (ea.tr.act)
+                ea.tr.act[traj_rec(ea.tr, sa.t, n, e) * ea.n_agents + seat] = (uint8_t)a;
         }
         act_s[el * kMaxAgents + seat] = (uint8_t)a;
     }
@@ -367,6 +399,11 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
         for (int j = 0; j < NJ; ++j)
             acc[i][j] = 0.0f;
 
+    // trajectory observation of the step: bf16(s) of each env, written by the
+    // threads that stage the state chunks
+    uint16_t* obs_row = nullptr;
+    if (ea.tr.obs && s_owner && e_ld < n)
+        obs_row = (uint16_t*)ea.tr.obs + traj_rec(ea.tr, sa.t, n, e_ld) * D + cq_ld * 4;
     for (int c0 = 0; c0 < D; c0 += kFeatKC) {
         v4f* dst = reinterpret_cast<v4f*>(Ws);
 #pragma unroll
@@ -374,6 +411,9 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
             dst[q * kFeatThreads + tid] = wreg[q];
         if (e_ld >= n)
             sreg = v4f{0.f, 0.f, 0.f, 0.f};
+        if (obs_row)
+            *reinterpret_cast<uint2*>(obs_row + c0) =
+                make_uint2(pack_bf16x2(sreg.x, sreg.y), pack_bf16x2(sreg.z, sreg.w));
         if (s_owner) {
             Ss[(cq_ld * 4 + 0) * SSTR + el_ld] = sreg.x;
             Ss[(cq_ld * 4 + 1) * SSTR + el_ld] = sreg.y;
@@ -492,6 +532,11 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
         for (int q = 0; q < kMaxAgents; ++q)
             if (q < ea.n_agents)
                 ret[(int64_t)q * n + er] = rv[q] + (((ea.team_row >> q) & 1u) ? r : -r);
+        if (ea.tr.rew) {
+            const int64_t rec = traj_rec(ea.tr, sa.t, n, er);
+            ea.tr.rew[rec] = r;
+            ea.tr.flags[rec] = sa.t == ea.tr.horizon - 1 ? 2 : 0;
+        }
     }
 }
 
@@ -506,13 +551,13 @@ hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_env
         const int iter = e.kind == MALIB_ENV_ITER_MATRIX;
         uint16_t* hist = iter ? (uint16_t*)state_out : nullptr;
         if (e.A <= 8)
-            step_matrix_kernel<8><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+            step_matrix_kernel<8><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, e.tr, hist, ret);
         else if (e.A <= 16)
-            step_matrix_kernel<16><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+            step_matrix_kernel<16><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, e.tr, hist, ret);
         else if (e.A <= 24)
-            step_matrix_kernel<24><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+            step_matrix_kernel<24><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, e.tr, hist, ret);
         else if (e.A <= 32)
-            step_matrix_kernel<32><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, hist, ret);
+            step_matrix_kernel<32><<<blocks, 256, 0, s>>>(e.Amat, e.A, iter, n_envs, sa, e.tr, hist, ret);
         else
             return hipErrorInvalidValue;
         break;
@@ -522,7 +567,7 @@ hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_env
             return hipErrorInvalidValue;
         // one thread per slot
         step_pursuit_kernel<<<(int)((2 * n_envs + 255) / 256), 256, 0, s>>>(
-            e.grid, n_envs, sa, (uint8_t*)state_out, done, ret, frames);
+            e.grid, n_envs, sa, e.tr, (uint8_t*)state_out, done, ret, frames);
         break;
     case MALIB_ENV_FEATURE: {
         const float* si = (const float*)state_in;

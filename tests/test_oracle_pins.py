@@ -740,3 +740,38 @@ def test_aggregate_equilibria_and_a_hand_case():
     # one side left out
     out = oracle.aggregate(H, np.array([[1, 0], [1, 0]], np.float32), -1, 1)
     assert np.isnan(out[2]) and out[4] == 1.0
+
+
+# --------------------------------------------------------- per-step rewards
+
+@pytest.mark.parametrize("c", [1, 2, 3])
+def test_step_rewards_add_up_to_returns(c):
+    """The per-step rewards the oracle reports for trajectory records: summed
+    in step order (fp32) they are the returns bit for bit; the matrix games'
+    are the payoff entries of the actions taken, zero-sum per step; pursuit's
+    are +1 / -1 at the capture step only."""
+    if c == 1:
+        wl = W.make(1, per_pair=8)
+    elif c == 2:
+        wl = W.make(2, P=2, per_pair=4, horizon=7)
+    else:
+        wl = W.make(3, P=3, n_envs=1, horizon=40)
+    pairs = wl.pairs if wl.pairs is not None else W.blocked_pairs(3, 6)
+    n = len(pairs)
+    o = oracle.rollout(wl, np.arange(n), pairs, want_actions=True, want_rewards=True)
+    r = o["rewards"]
+    acc = np.zeros((n, 2), np.float32)
+    for t in range(r.shape[0]):
+        acc = acc + r[t]
+    assert np.array_equal(acc.view(np.uint32), o["returns"].view(np.uint32))
+    assert np.array_equal(r[:, :, 1], -r[:, :, 0])
+    a = o["actions"]
+    if c in (1, 2):
+        assert np.array_equal(r[:, :, 0], wl.A[a[:, :, 0], a[:, :, 1]])
+    else:
+        assert set(np.unique(r[:, :, 0])) <= {0.0, 1.0}
+        caught = r[:, :, 0] == 1.0
+        assert (caught.sum(axis=0) <= 1).all() and caught.any()
+        t_c = np.argmax(caught, axis=0)
+        for e in np.nonzero(caught.any(axis=0))[0]:
+            assert (a[t_c[e] + 1:, e] == 255).all()
