@@ -283,6 +283,10 @@ def main():
     ap.add_argument("--event-every", type=int, default=0, metavar="K",
                     help="time one grouped-forward launch in K with HIP events during the "
                          "timed fills (default: about 16 per fill, at least every 4th)")
+    ap.add_argument("--fill-only", action="store_true",
+                    help="skip the trajectory, meta-update and expansion timings after the "
+                         "fills (profiling runs: their small or extra launches would mix "
+                         "into the per-kernel statistics)")
     ap.add_argument("--fp-iters", type=int, default=1000, metavar="T",
                     help="fictitious-play iterations of the meta-update timed after the "
                          "fills (table -> game -> solver -> meta-sample)")
@@ -378,9 +382,11 @@ def main():
                 kern[name]["fp32_TFLOPs"] = round(w["flops"] / t / 1e12, 2)
                 kern[name]["alu_frac"] = round(w["flops"] / t / 1e12 / PEAK_F32_ALU_TFLOPS, 4)
     pop.profile_enable(False)
-    traj = trajectory_timing(M, pop, env, wl, pairs, 1000.0 * el / args.steps)
-    meta = meta_update_timing(M, pop, env, wl, pairs, args.fp_iters)
-    expand = expansion_timing(M, IO, W, pop, env, wl, 1000.0 * el / args.steps)
+    traj = meta = expand = None
+    if not args.fill_only:
+        traj = trajectory_timing(M, pop, env, wl, pairs, 1000.0 * el / args.steps)
+        meta = meta_update_timing(M, pop, env, wl, pairs, args.fp_iters)
+        expand = expansion_timing(M, IO, W, pop, env, wl, 1000.0 * el / args.steps)
 
     ms_step = 1000.0 * el / args.steps
     value = frames / el
