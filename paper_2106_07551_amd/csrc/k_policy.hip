@@ -4,11 +4,15 @@
 // wavefront (fp32) runs rows of a single policy with one set of weights.
 //
 //  tabular   logits = tab[pid]
-//  mlp_f32   fp32 MLP, one row per lane; the policy is wave-uniform, so the
-//            weights stream through the scalar cache as SGPR operands
-//  mlp_bf16  bf16 MLP on v_mfma_f32_32x32x16_bf16: a 128-row tile per
-//            workgroup; observations are built in LDS, hidden activations stay
-//            in LDS, weights come pre-packed in MFMA fragment order
+//  mlp_f32   fp32 MLP on v_mfma_f32_32x32x2_f32: one wavefront per 32-row
+//            tile, the hidden layer kept in registers (weights packed in the
+//            accumulators' k order)
+//  mlp_bf16  bf16 MLP on v_mfma_f32_32x32x16_bf16: a 64-row tile per
+//            workgroup (or, for wide feature observations, a persistent
+//            workgroup per CU over 128-row tiles); observations are built in
+//            LDS, the first hidden layer stays in LDS, the second feeds the
+//            output layer from the accumulators; weights come pre-packed in
+//            MFMA fragment order
 #include "device.hpp"
 #include "internal.hpp"
 
