@@ -89,6 +89,20 @@ def test_validation_before_device_work():
     bad_team = np.array([1, 1], np.int8)
     assert L.malib_expansion_pairs(4, 1, 1, 2, bad_team.ctypes.data, out, None) == B.E_INVAL
     assert L.malib_pop_extend(None, None, None) == B.E_INVAL
+    # trajectory rings: the descriptor is checked before the rollout's own checks
+    assert L.malib_rollout_batch_traj(None, None, 1, None, 0, 0, 1, None, None,
+                                      None) == B.E_INVAL
+    td = B.TrajDesc(16, 16, 16, None, 0, 0)             # capacity 0
+    assert L.malib_rollout_batch_traj(None, None, 1, None, 0, 0, 1, None, C.byref(td),
+                                      None) == B.E_INVAL
+    assert b"capacity" in L.malib_last_error()
+    td = B.TrajDesc(16, None, 16, None, 8, 0)           # no reward buffer
+    assert L.malib_rollout_batch_traj(None, None, 1, None, 0, 0, 1, None, C.byref(td),
+                                      None) == B.E_INVAL
+    td = B.TrajDesc(16, 16, 16, None, 8, 0)             # a valid ring, no population
+    assert L.malib_rollout_batch_traj(None, None, 1, None, 0, 0, 1, None, C.byref(td),
+                                      None) == B.E_INVAL
+    assert td.cursor == 0
     assert L.malib_profile_enable(None, 1, 1) == B.E_INVAL
     assert L.malib_debug_tanh_ref(None, None, 4, None) == B.E_INVAL
 
