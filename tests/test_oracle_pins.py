@@ -775,3 +775,17 @@ def test_step_rewards_add_up_to_returns(c):
         t_c = np.argmax(caught, axis=0)
         for e in np.nonzero(caught.any(axis=0))[0]:
             assert (a[t_c[e] + 1:, e] == 255).all()
+
+
+def test_payoff_matrix_is_the_means_with_empty_cells_zero():
+    """The solver's game from a table: a filled cell keeps its mean, an empty
+    one (NaN mean, count 0) becomes 0; built from the plain-loop table."""
+    rng = np.random.default_rng(21)
+    P = 4
+    pids = np.array([[0, 1], [0, 1], [2, 3], [1, 0]])
+    R = rng.standard_normal((4, 2)).astype(np.float32)
+    mean, cnt, s, _ = oracle.payoff(R, pids, np.array([1, -1], np.int8), P)
+    g = oracle.payoff_matrix(mean)
+    assert g[0, 1] == (float(R[0, 0]) + float(R[1, 0])) / 2
+    assert g[2, 3] == float(R[2, 0]) and g[1, 0] == float(R[3, 0])
+    assert (g[cnt == 0] == 0.0).all() and not np.isnan(g).any()
