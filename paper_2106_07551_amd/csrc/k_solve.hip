@@ -118,24 +118,25 @@ __global__ __launch_bounds__(64) void solve_fp_kernel(const double* __restrict__
     double v[K], w[K];
     int cx[K], cy[K];
     bool mine[K];
+    // slots past P start at -inf (v) and +inf (w) and keep adding finite
+    // entries, so they never win a reduction and need no masking
 #pragma unroll
     for (int q = 0; q < K; ++q) {
-        v[q] = 0.0;
-        w[q] = 0.0;
+        mine[q] = lane + 64 * q < P;
+        v[q] = mine[q] ? 0.0 : -INFINITY;
+        w[q] = mine[q] ? 0.0 : INFINITY;
         cx[q] = 0;
         cy[q] = 0;
-        mine[q] = lane + 64 * q < P;
     }
     // first index of the best value (row side: largest v; column side:
-    // smallest w); P - 1 when no lane matches, which only NaN can cause
+    // smallest w); P - 1 when no policy matches (only NaN or infinite
+    // entries can cause that, or a match past P)
     auto best = [&](int& i, int& j, double& vi, double& wj) {
-        double lv = -INFINITY, lw = INFINITY;
+        double lv = v[0], lw = w[0];
 #pragma unroll
-        for (int q = 0; q < K; ++q) {
-            if (mine[q]) {
-                lv = v[q] > lv ? v[q] : lv;
-                lw = w[q] < lw ? w[q] : lw;
-            }
+        for (int q = 1; q < K; ++q) {
+            lv = v[q] > lv ? v[q] : lv;
+            lw = w[q] < lw ? w[q] : lw;
         }
         wave_max_min(lv, lw);
         vi = lv;
@@ -145,8 +146,8 @@ __global__ __launch_bounds__(64) void solve_fp_kernel(const double* __restrict__
         bool fi = false, fj = false;
 #pragma unroll
         for (int q = 0; q < K; ++q) {
-            const unsigned long long bi = __ballot(mine[q] && v[q] == vi);
-            const unsigned long long bj = __ballot(mine[q] && w[q] == wj);
+            const unsigned long long bi = __ballot(v[q] == vi);
+            const unsigned long long bj = __ballot(w[q] == wj);
             if (!fi && bi) {
                 i = 64 * q + __ffsll(bi) - 1;
                 fi = true;
@@ -156,6 +157,8 @@ __global__ __launch_bounds__(64) void solve_fp_kernel(const double* __restrict__
                 fj = true;
             }
         }
+        i = i < P ? i : P - 1;
+        j = j < P ? j : P - 1;
     };
     for (int t = 0; t < T; ++t) {
         int i, j;
