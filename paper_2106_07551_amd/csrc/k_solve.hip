@@ -60,11 +60,14 @@ constexpr int kDppHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
 
 // The largest of x and the smallest of y over the wavefront, the same in
-// every lane (a NaN never replaces a number); the two reductions interleave.
+// every lane; the two reductions interleave.  IEEE maxNum / minNum (one
+// v_max_f64 / v_min_f64 each): a NaN never replaces a number, and which of
+// +0 and -0 survives does not matter (the callers compare with ==, and take
+// the winning policy's own sum afterwards).
 __device__ __forceinline__ void wave_max_min(double& x, double& y)
 {
-    auto hi = [](double a, double b) { return b > a ? b : a; };
-    auto lo = [](double a, double b) { return b < a ? b : a; };
+    auto hi = [](double a, double b) { return __builtin_fmax(a, b); };
+    auto lo = [](double a, double b) { return __builtin_fmin(a, b); };
     double dx = dpp_f64<kDppQuadSwap1>(x), dy = dpp_f64<kDppQuadSwap1>(y);
     x = hi(x, dx);
     y = lo(y, dy);
@@ -135,8 +138,8 @@ __global__ __launch_bounds__(64) void solve_fp_kernel(const double* __restrict__
         double lv = v[0], lw = w[0];
 #pragma unroll
         for (int q = 1; q < K; ++q) {
-            lv = v[q] > lv ? v[q] : lv;
-            lw = w[q] < lw ? w[q] : lw;
+            lv = __builtin_fmax(lv, v[q]);
+            lw = __builtin_fmin(lw, w[q]);
         }
         wave_max_min(lv, lw);
         vi = lv;
