@@ -86,6 +86,9 @@ def test_validation_before_device_work():
     assert L.malib_expansion_pairs(4, 4, 1, 2, None, out, None) == B.E_INVAL
     assert L.malib_expansion_pairs(4, 1, 0, 2, None, out, None) == B.E_INVAL
     assert L.malib_expansion_pairs(4, 1, 1, 3, None, out, None) == B.E_INVAL
+    # 256^2 cells x 1100 envs x 2 seats exceeds the 2^26-slot batch limit
+    assert L.malib_expansion_pairs(256, 0, 1100, 2, None, out, None) == B.E_INVAL
+    assert b"2^26" in L.malib_last_error()
     bad_team = np.array([1, 1], np.int8)
     assert L.malib_expansion_pairs(4, 1, 1, 2, bad_team.ctypes.data, out, None) == B.E_INVAL
     assert L.malib_pop_extend(None, None, None) == B.E_INVAL
