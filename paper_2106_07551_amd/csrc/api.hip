@@ -342,6 +342,9 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
                         "%s failed: %s", #expr, hipGetErrorString(e_));                   \
         }                                                                                 \
     } while (0)
+    // work queued on any stream may still update the table (or read the
+    // weights): let it finish before both are copied
+    TRY(hipDeviceSynchronize());
     if (pop->kind == MALIB_POLICY_TABULAR) {
         const size_t per = sizeof(float) * A;
         TRY(hipMalloc((void**)&tab, per * P));
@@ -382,7 +385,7 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
     TRY(hipMalloc((void**)&acc, acc_bytes));
     TRY(hipHostMalloc((void**)&host_acc, acc_bytes, hipHostMallocDefault));
     TRY(launch_remap_table(pop->acc, P0, acc, P, s));
-    // the old buffers may still be read by work queued on any stream
+    // the copies and the remap read the old buffers
     TRY(hipDeviceSynchronize());
 #undef TRY
     for (int l = 0; l < 3; ++l) {
