@@ -43,6 +43,18 @@ __device__ __forceinline__ double dpp_f64(double x)
     return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
 }
 
+// The same across rows: lanes of the rows in ROWS take the pattern's source,
+// the others keep their own value.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_f64_rows(double x)
+{
+    const long long b = __double_as_longlong(x);
+    const int lo = __builtin_amdgcn_update_dpp((int)b, (int)b, CTRL, ROWS, 0xF, false);
+    const int hi =
+        __builtin_amdgcn_update_dpp((int)(b >> 32), (int)(b >> 32), CTRL, ROWS, 0xF, false);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
 __device__ __forceinline__ double readlane_f64(double x, int l)
 {
     const long long b = __double_as_longlong(x);
@@ -53,11 +65,13 @@ __device__ __forceinline__ double readlane_f64(double x, int l)
 
 // DPP controls: swap neighbours, swap pairs in a quad, mirror each 8-lane
 // half row, mirror each 16-lane row.  After the four steps every lane holds
-// its row's result; the four rows are combined from lanes 0, 16, 32, 48.
+// its row's result; two row broadcasts then combine the rows into lane 63.
 constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1, 0, 3, 2]
 constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2, 3, 0, 1]
 constexpr int kDppHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowBcast15 = 0x142;   // lane 15 of each row to the next row
+constexpr int kDppRowBcast31 = 0x143;   // lane 31 to the rows above it
 
 // The largest of x and the smallest of y over the wavefront, the same in
 // every lane; the two reductions interleave.  IEEE maxNum / minNum (one
@@ -83,10 +97,18 @@ __device__ __forceinline__ void wave_max_min(double& x, double& y)
     dy = dpp_f64<kDppRowMirror>(y);
     x = hi(x, dx);
     y = lo(y, dy);
-    x = hi(hi(readlane_f64(x, 0), readlane_f64(x, 16)),
-           hi(readlane_f64(x, 32), readlane_f64(x, 48)));
-    y = lo(lo(readlane_f64(y, 0), readlane_f64(y, 16)),
-           lo(readlane_f64(y, 32), readlane_f64(y, 48)));
+    // rows: lane 15 of rows 0 and 2 into rows 1 and 3, then lane 31 into
+    // rows 2 and 3; lane 63 then holds the wavefront's result
+    dx = dpp_f64_rows<kDppRowBcast15, 0xA>(x);
+    dy = dpp_f64_rows<kDppRowBcast15, 0xA>(y);
+    x = hi(x, dx);
+    y = lo(y, dy);
+    dx = dpp_f64_rows<kDppRowBcast31, 0xC>(x);
+    dy = dpp_f64_rows<kDppRowBcast31, 0xC>(y);
+    x = hi(x, dx);
+    y = lo(y, dy);
+    x = readlane_f64(x, 63);
+    y = readlane_f64(y, 63);
 }
 
 // Simultaneous fictitious play on the zero-sum game with row payoff M
