@@ -263,8 +263,10 @@ __global__ __launch_bounds__(kMaxP) void aggregate_kernel(const double* __restri
     const int k = threadIdx.x;
     if (k == 0) {
         double a = 0.0, b = 0.0;
+#pragma unroll 16
         for (int m = 0; m < P; ++m)
             a += (double)sigma[m];
+#pragma unroll 16
         for (int m = 0; m < P; ++m)
             b += (double)sigma[P + m];
         S[0] = a;
@@ -277,11 +279,14 @@ __global__ __launch_bounds__(kMaxP) void aggregate_kernel(const double* __restri
     }
     __syncthreads();
     if (k < P) {
+        // (unrolled so that the loads run ahead of the dependent adds)
         double acc = 0.0;
+#pragma unroll 16
         for (int j = 0; j < P; ++j)
             acc = acc + M[(size_t)k * P + j] * y[j];
         u[k] = acc;
         double accv = 0.0;
+#pragma unroll 16
         for (int i = 0; i < P; ++i)
             accv = accv + x[i] * M[(size_t)i * P + k];
         if (k == br_col)
@@ -290,6 +295,7 @@ __global__ __launch_bounds__(kMaxP) void aggregate_kernel(const double* __restri
     __syncthreads();
     if (k == 0) {
         double nash = 0.0;
+#pragma unroll 16
         for (int i = 0; i < P; ++i)
             nash = nash + x[i] * u[i];
         const double wr = br_row >= 0 ? u[br_row] : (double)NAN;
