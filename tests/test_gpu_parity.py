@@ -441,3 +441,30 @@ def test_parity_matrix_many_actions(n_actions):
     wl.tab_logits = rng.normal(0.0, 1.0, (wl.P, n_actions)).astype(np.float32)
     g = run_gpu(wl, snaps=[0])
     check_parity(wl, g)
+
+
+# ------------------------------------------------------------ largest population
+
+def test_parity_max_population_pursuit():
+    """256 policies, the most the ABI takes (every bit of the bucketing's
+    8-bit policy id in use): bf16 pursuit with about two rows per policy, so
+    nearly every tile is a ragged one."""
+    wl = W.make(3, P=256, n_envs=300, horizon=20)
+    g = run_gpu(wl, snaps=[0, 19])
+    check_parity(wl, g)
+
+
+def test_parity_max_population_iter_sampled():
+    """256 fp32 policies, all 65536 ordered pairs once (one row per pair and
+    seat: 32-row tiles of about 16 rows), sampled envs in lockstep."""
+    wl = W.make(2, P=256, per_pair=1, horizon=4)
+    g = run_gpu(wl, snaps=[0, 3])
+    sel = np.concatenate([np.arange(0, wl.n_envs, 331), [wl.n_envs - 1]])
+    check_parity(wl, g, sel)
+
+
+def test_parity_max_population_matrix():
+    """256 tabular policies, every ordered pair twice (131072 envs), all envs."""
+    wl = W.make(1, P=256, per_pair=2)
+    g = run_gpu(wl, snaps=[0])
+    check_parity(wl, g)
