@@ -468,3 +468,21 @@ def test_parity_max_population_matrix():
     wl = W.make(1, P=256, per_pair=2)
     g = run_gpu(wl, snaps=[0])
     check_parity(wl, g)
+
+
+def test_parity_maximum_batch_32_actions_sampled():
+    """The largest batch the ABI takes (n_envs * n_agents = 2^26 slots) with
+    32 actions: logit offsets slot * A reach 2^31, past 32-bit indexing.
+    Sampled envs in lockstep (the first, the last, and across the range);
+    the table against the fp64 reduction of every env's returns."""
+    rng = np.random.default_rng([2106, 7551, 26])
+    wl = W.make(1, P=4, per_pair=1 << 21)
+    assert wl.n_envs * wl.n_agents == 1 << 26
+    a = rng.uniform(-1.0, 1.0, (32, 32)).astype(np.float32)
+    wl.A = np.triu(a, 1) - np.triu(a, 1).T
+    wl.n_actions = 32
+    wl.tab_logits = rng.normal(0.0, 1.0, (wl.P, 32)).astype(np.float32)
+    g = run_gpu(wl, snaps=())
+    sel = np.concatenate([[0], rng.choice(wl.n_envs, 254, replace=False), [wl.n_envs - 1]])
+    check_parity(wl, g, np.unique(sel))
+    assert g["table"]["counts"].sum() == wl.n_envs
