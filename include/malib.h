@@ -89,6 +89,12 @@ typedef struct {
                                      fp32 [P][dims[l+1]], or NULL (all zero);
                                      individual entries may be NULL (zero) */
     const float* tab_logits;      /* TABULAR: device fp32 [P][n_actions] */
+    const int64_t* policy_ids;    /* host [P] or NULL: the caller's ids of the policies
+                                     (the PolicyID keys of the example API's per-agent
+                                     distributions, Appendix C.2), distinct; NULL gives
+                                     0 .. P-1.  Rows and columns of every table and
+                                     every pair assignment use the index 0 .. P-1;
+                                     malib_pop_policy_ids maps indices back to ids */
 } malib_pop_desc;
 
 typedef struct malib_pop* malib_pop_t;
@@ -102,6 +108,17 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
 
 /* Free a handle (synchronizes the device first).  NULL is ignored. */
 void malib_pop_destroy(malib_pop_t pop);
+
+/*
+ * The caller's policy ids of a population (Sec. 3.1: agents draw policies from
+ * pools keyed by policy id; Appendix C.2: distributions Dict[PolicyID, float]),
+ * in index order: ids_out[i] is the id of the policy at row / column i of the
+ * payoff table and of pair-assignment value i.  *n_out receives P.  ids_out
+ * may be NULL (only the count is returned); otherwise it must hold
+ * `capacity` >= P entries (MALIB_E_INVAL if not).  Host-only, no device work.
+ */
+malib_status malib_pop_policy_ids(malib_pop_t pop, int64_t* ids_out, int32_t capacity,
+                                  int32_t* n_out);
 
 /* --------------------------------------------------------------- environment */
 
@@ -270,7 +287,9 @@ malib_status malib_payoff_eval(malib_pop_t pop, void* stream, int32_t reset,
  * Grow the population by add->n_policies policies (the auto-curriculum adds
  * policies to the pools, Sec. 3.1; extend_policy_pool of the example API,
  * Appendix C.2).  `add` describes only the new policies, with the kind, dims
- * and n_actions of the population; they take ids P0 .. P0 + k - 1.  The
+ * and n_actions of the population; they take indices P0 .. P0 + k - 1 and
+ * the caller ids add->policy_ids (NULL: ids P0 .. P0 + k - 1), which must be
+ * distinct from each other and from the ids already present.  The
  * payoff table grows to (P0 + k)^2 cells: the P0 x P0 cells keep their sums
  * and counts, the new cells start empty, the live-frame counter and the error
  * flags carry over.  Synchronizes the device (the old buffers are freed); on

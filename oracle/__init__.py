@@ -393,6 +393,39 @@ def rollout(wl, env_idx, pids, *, forced=None, tol=None, horizon=None, env_offse
     }
 
 
+def rollout_threads(wl, env_idx, pids, *, threads=None, forced=None, **kw):
+    """``rollout`` over shards of the selected envs in parallel threads (the C
+    oracle holds no shared state and ctypes releases the GIL during the call);
+    every env is still simulated by the same single-threaded code, so the
+    merged result equals one ``rollout`` over all of them."""
+    import concurrent.futures as cf
+    idx = np.ascontiguousarray(env_idx, dtype=np.int64)
+    n = idx.shape[0]
+    if threads is None:
+        threads = min(16, len(os.sched_getaffinity(0)))
+    k = max(1, min(threads, n))
+    bounds = np.linspace(0, n, k + 1).astype(int)
+    p = np.asarray(pids).reshape(n, wl.n_agents)
+
+    def one(i):
+        lo, hi = bounds[i], bounds[i + 1]
+        f = None if forced is None else np.asarray(forced)[:, lo:hi]
+        return rollout(wl, idx[lo:hi], p[lo:hi], forced=f, **kw)
+
+    with cf.ThreadPoolExecutor(max_workers=k) as ex:
+        parts = list(ex.map(one, range(k)))
+    out = {"returns": np.concatenate([q["returns"] for q in parts])}
+    for key in ("actions", "logits", "states", "rewards"):
+        out[key] = (None if parts[0][key] is None
+                    else np.concatenate([q[key] for q in parts], axis=1))
+    for key in ("near_ties", "flips", "fails", "live_frames"):
+        out[key] = sum(q[key] for q in parts)
+    out["first_fail"] = next(((q["first_fail"][0], q["first_fail"][1] + int(lo),
+                               q["first_fail"][2]) for q, lo in zip(parts, bounds)
+                              if q["fails"]), parts[0]["first_fail"])
+    return out
+
+
 def policy_logits(wl, p, obs):
     cfg = _Cfg(wl)
     o = np.ascontiguousarray(obs, dtype=np.float64)

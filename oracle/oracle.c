@@ -129,17 +129,18 @@ float ora_bf16_round(float x)
     return y;
 }
 
-/* Hidden-unit ReLU of the bf16 policies, applied to the rounded value: a bf16
- * with its sign bit set (negative, -0, -inf, negative NaN) becomes +0, any
- * other value is kept.  For every non-NaN x this is bf16(max(x, 0)). */
+/* Hidden-unit ReLU of the bf16 policies: max(x, 0) rounded to bf16.  A NaN
+ * (of either sign) stays NaN, so that it reaches the logits; zero and every
+ * negative value (including -0 and -inf) give +0; a positive value gives its
+ * bf16 rounding.  Rounding to nearest is monotone and keeps the sign, so this
+ * equals the ReLU of the rounded value. */
 float ora_bf16_relu(float x)
 {
-    uint32_t b = (uint32_t)ora_bf16_bits(x) << 16;
-    if (b & 0x80000000u)
-        b = 0;
-    float y;
-    memcpy(&y, &b, 4);
-    return y;
+    if (isnan(x))
+        return x;
+    if (!(x > 0.0f))
+        return 0.0f;
+    return ora_bf16_round(x);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -27,6 +27,7 @@ EXPORTS = [
     "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
     "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate", "malib_rollout_batch_traj",
+    "malib_pop_policy_ids",
 ]
 
 
@@ -40,7 +41,7 @@ class PopDesc(C.Structure):
     _fields_ = [("kind", C.c_int32), ("n_policies", C.c_int32), ("n_actions", C.c_int32),
                 ("n_layers", C.c_int32), ("dims", C.POINTER(C.c_int32)),
                 ("weights", C.POINTER(C.c_void_p)), ("biases", C.POINTER(C.c_void_p)),
-                ("tab_logits", C.c_void_p)]
+                ("tab_logits", C.c_void_p), ("policy_ids", C.POINTER(C.c_int64))]
 
 
 class EnvDesc(C.Structure):
@@ -115,6 +116,8 @@ def lib():
         L.malib_pop_extend.restype = i32
         L.malib_expansion_pairs.argtypes = [i32, i32, i32, i32, vp, vp, vp]
         L.malib_expansion_pairs.restype = i32
+        L.malib_pop_policy_ids.argtypes = [vp, vp, i32, C.POINTER(i32)]
+        L.malib_pop_policy_ids.restype = i32
         _lib = L
     return _lib
 
@@ -137,12 +140,18 @@ def _dptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
-def _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits):
+def _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits,
+              policy_ids=None):
     """A malib_pop_desc over device tensors, with the ctypes arrays it points
     into (keep them alive until the call returns)."""
     d = PopDesc()
     d.kind, d.n_policies, d.n_actions = kind, n_policies, n_actions
     keep = []
+    if policy_ids is not None:
+        ids = (C.c_int64 * n_policies)(*[int(x) for x in policy_ids])
+        assert len(policy_ids) == n_policies
+        keep.append(ids)
+        d.policy_ids = C.cast(ids, C.POINTER(C.c_int64))
     if kind == POLICY_TABULAR:
         d.n_layers = 0
         d.tab_logits = _dptr(tab_logits)
@@ -166,8 +175,9 @@ class Population:
 
     def __init__(self, kind: int, n_policies: int, n_actions: int, *, dims=None,
                  weights: Sequence = (), biases: Optional[Sequence] = None,
-                 tab_logits=None, stream=None):
-        d, keep = _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits)
+                 tab_logits=None, policy_ids: Optional[Sequence[int]] = None, stream=None):
+        d, keep = _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits,
+                            policy_ids)
         h = C.c_void_p()
         _check(lib().malib_pop_create(C.byref(d), _stream(stream), C.byref(h)))
         del keep
@@ -178,13 +188,23 @@ class Population:
         self.A = n_actions
 
     def extend(self, n_new: int, *, weights: Sequence = (), biases: Optional[Sequence] = None,
-               tab_logits=None, stream=None):
-        """malib_pop_extend: append n_new policies (ids P .. P + n_new - 1); the
-        table keeps its cells and gains empty rows and columns."""
-        d, keep = _pop_desc(self.kind, n_new, self.A, self.dims, weights, biases, tab_logits)
+               tab_logits=None, policy_ids: Optional[Sequence[int]] = None, stream=None):
+        """malib_pop_extend: append n_new policies (indices P .. P + n_new - 1,
+        caller ids ``policy_ids``, default the indices); the table keeps its
+        cells and gains empty rows and columns."""
+        d, keep = _pop_desc(self.kind, n_new, self.A, self.dims, weights, biases, tab_logits,
+                            policy_ids)
         _check(lib().malib_pop_extend(self.handle, C.byref(d), _stream(stream)))
         del keep
         self.P += n_new
+
+    def policy_ids(self) -> np.ndarray:
+        """malib_pop_policy_ids: the caller id of each index 0 .. P-1."""
+        n = C.c_int32()
+        out = np.zeros(self.P, np.int64)
+        _check(lib().malib_pop_policy_ids(self.handle, out.ctypes.data, self.P, C.byref(n)))
+        assert n.value == self.P
+        return out
 
     def close(self):
         if getattr(self, "handle", None):

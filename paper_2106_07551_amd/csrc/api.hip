@@ -175,6 +175,25 @@ static malib_status check_desc(const malib_pop_desc* desc, int* in_dim, int* hid
     return MALIB_OK;
 }
 
+// The caller ids of the policies a description adds at indices first ..
+// first + P - 1 (desc->policy_ids, else the indices themselves), checked to be
+// distinct from each other and from `existing`.
+static malib_status read_ids(const malib_pop_desc* desc, int first,
+                             const std::vector<int64_t>& existing, std::vector<int64_t>& out)
+{
+    const int P = desc->n_policies;
+    out.clear();
+    for (int i = 0; i < P; ++i)
+        out.push_back(desc->policy_ids ? desc->policy_ids[i] : (int64_t)(first + i));
+    std::vector<int64_t> all(existing);
+    all.insert(all.end(), out.begin(), out.end());
+    std::sort(all.begin(), all.end());
+    for (size_t i = 1; i < all.size(); ++i)
+        if (all[i] == all[i - 1])
+            return fail(MALIB_E_INVAL, "policy id %lld appears twice", (long long)all[i]);
+    return MALIB_OK;
+}
+
 malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_pop_t* out)
 {
     if (!out)
@@ -190,10 +209,17 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
         if (st != MALIB_OK)
             return st;
     }
+    std::vector<int64_t> ids;
+    {
+        const malib_status st = read_ids(desc, 0, {}, ids);
+        if (st != MALIB_OK)
+            return st;
+    }
 
     malib_pop* p = new (std::nothrow) malib_pop();
     if (!p)
         return fail(MALIB_E_NOMEM, "host allocation failed");
+    p->ids = std::move(ids);
     auto cleanup = [&](malib_status st) {
         malib_pop_destroy(p);
         return st;
@@ -310,6 +336,12 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
     const int P0 = pop->P, k = add->n_policies, P = P0 + k, A = pop->A;
     if (P > kMaxP)
         return fail(MALIB_E_INVAL, "%d + %d policies exceed %d", P0, k, kMaxP);
+    std::vector<int64_t> new_ids;
+    {
+        const malib_status st = read_ids(add, P0, pop->ids, new_ids);
+        if (st != MALIB_OK)
+            return st;
+    }
     hipStream_t s = (hipStream_t)stream;
     // Everything new is built before the handle changes: on failure the
     // population is left as it was.
@@ -412,6 +444,22 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
     pop->dev_frames = acc + 3 * PP;
     pop->dev_flags = reinterpret_cast<int*>(acc + 3 * PP + 1);
     pop->P = P;
+    pop->ids.insert(pop->ids.end(), new_ids.begin(), new_ids.end());
+    return MALIB_OK;
+}
+
+malib_status malib_pop_policy_ids(malib_pop_t pop, int64_t* ids_out, int32_t capacity,
+                                  int32_t* n_out)
+{
+    if (!pop)
+        return fail(MALIB_E_INVAL, "pop is NULL");
+    if (ids_out && capacity < pop->P)
+        return fail(MALIB_E_INVAL, "capacity %d is below the population size %d", capacity,
+                    pop->P);
+    if (n_out)
+        *n_out = pop->P;
+    if (ids_out)
+        std::copy(pop->ids.begin(), pop->ids.end(), ids_out);
     return MALIB_OK;
 }
 

@@ -52,6 +52,7 @@ struct Pop {
     void* w[3] = {nullptr, nullptr, nullptr};
     float* b[3] = {nullptr, nullptr, nullptr};  // fp32 [P][out] (zero-filled when absent)
     float* tab = nullptr;                       // fp32 [P][A]
+    std::vector<int64_t> ids;                   // caller's policy id of each index
     // payoff accumulators, one allocation acc[3 P*P + 2] so that the table
     // comes back in one copy: sum, sumsq, cnt ([P*P] each), the live-frame
     // counter and the device error flags (the low half of the last word)

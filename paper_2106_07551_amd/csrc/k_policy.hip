@@ -149,6 +149,13 @@ struct MlpF32Args {
 // with a relative tolerance.
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
+// Hidden ReLU of the fp32 policies: the IEEE 754-2019 maximum with +0, so a
+// NaN of either sign propagates to the logits (and raises the NaN flag).
+__device__ __forceinline__ float relu_f32(float x)
+{
+    return __builtin_elementwise_maximum(x, 0.0f);
+}
+
 template <int HID, int AMAX>
 __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
 {
@@ -227,7 +234,7 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                acc[nt][rt][r] = acc[nt][rt][r] > 0.0f ? acc[nt][rt][r] : 0.0f;
+                acc[nt][rt][r] = relu_f32(acc[nt][rt][r]);
     // ---- layer 2 (k-step s2 = 16 nt + r takes register r of n-tile nt); the
     // weights stream through a ring DEPTH k-steps ahead
 #pragma unroll
@@ -294,7 +301,7 @@ __global__ __launch_bounds__(256) void mlp_f32_kernel(MlpF32Args a)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         const float v = acc2[nt][rt][r];
-                        part = __builtin_fmaf(w3[nt][r], v > 0.0f ? v : 0.0f, part);
+                        part = __builtin_fmaf(w3[nt][r], relu_f32(v), part);
                     }
                 const float tot = part + __shfl_xor(part, 32);
                 if (h == 0 && valid[rt])
@@ -571,16 +578,14 @@ __device__ __forceinline__ void mfma_layer_1b(WRing<NT, DEPTH>& ring, Frags frag
     }
 }
 
-// Hidden-unit ReLU on two accumulators: round both to bf16 (one
-// v_cvt_pk_bf16_f32), then clear every half whose sign bit is set with one
-// signed 16-bit max against 0.  For non-NaN inputs this is bf16(max(x, 0));
-// a negative NaN becomes +0 and a positive NaN stays NaN.
-typedef short short2_t __attribute__((ext_vector_type(2)));
+// Hidden-unit ReLU on two accumulators: the IEEE 754-2019 maximum with +0
+// (v_maximum3_f32: a NaN of either sign stays NaN, -0 becomes +0), then both
+// rounded to bf16 with one v_cvt_pk_bf16_f32.  For non-NaN inputs this is
+// bf16(max(x, 0)) = max(bf16(x), 0); a NaN reaches the next layer, so every
+// logit of the row is NaN and the sampler raises the NaN flag.
 __device__ __forceinline__ uint32_t relu_pack(float lo, float hi)
 {
-    short2_t v = __builtin_bit_cast(short2_t, pack_bf16x2(lo, hi));
-    v = __builtin_elementwise_max(v, short2_t{0, 0});
-    return __builtin_bit_cast(uint32_t, v);
+    return pack_bf16x2(relu_f32(lo), relu_f32(hi));
 }
 
 // ReLU + bf16, written back as the next layer's input rows.

@@ -23,8 +23,11 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_gpu(wl, *, horizon=None, snaps=(0,), pairs=None, env_offset=0, trace=True):
-    """One rollout batch on the GPU with a full trace; returns host arrays."""
+def run_gpu(wl, *, horizon=None, snaps=(0,), pairs=None, env_offset=0, trace=True,
+            check=True):
+    """One rollout batch on the GPU with a full trace; returns host arrays.
+    ``check=False`` returns the table even when the device flagged bad data
+    (its status and flags are in the table dict)."""
     import torch
     import paper_2106_07551_amd as M
     from paper_2106_07551_amd import workload_io as IO
@@ -56,7 +59,7 @@ def run_gpu(wl, *, horizon=None, snaps=(0,), pairs=None, env_offset=0, trace=Tru
             bufs["offsets"] = torch.empty(wl.P + 1, dtype=torch.int32, device="cuda")
         tr = M.Trace(snap_steps=snaps, **bufs)
     pop.rollout(env, n, pairs_t, wl.seed, H, env_offset=env_offset, returns=ret, trace=tr)
-    tab = pop.payoff()
+    tab = pop.payoff(check=check)
     torch.cuda.synchronize()
     out = {"returns": ret.cpu().numpy().T.copy(), "pairs": pairs_t.cpu().numpy(),
            "table": tab, "snaps": list(snaps), "H": H}
@@ -77,9 +80,9 @@ def check_parity(wl, g, sel=None, *, env_offset=0, check_table_vs_oracle=None):
     tol = TOL[wl.pol_kind]
     acts = g["actions"].reshape(H, n, na)[:, sel, :]
     say(f"[oracle] workload={wl.name} envs={len(sel)} H={H}")
-    o = oracle.rollout(wl, sel, g["pairs"][sel], forced=acts, tol=tol, horizon=H,
-                       env_offset=env_offset, want_actions=True, want_logits=True,
-                       want_states=True)
+    o = oracle.rollout_threads(wl, sel, g["pairs"][sel], forced=acts, tol=tol, horizon=H,
+                               env_offset=env_offset, want_actions=True, want_logits=True,
+                               want_states=True)
     rep = {"near_ties": o["near_ties"], "flips": o["flips"], "fails": o["fails"],
            "first_fail": o["first_fail"]}
     assert o["fails"] == 0, rep
@@ -124,12 +127,28 @@ def check_parity(wl, g, sel=None, *, env_offset=0, check_table_vs_oracle=None):
     tab = g["table"]
     full = len(sel) == n
     ref_ret = o["returns"] if full else g["returns"]
-    mean, cnt, _, _ = oracle.payoff(ref_ret, g["pairs"], wl.team, wl.P)
+    mean, cnt, s1, s2 = oracle.payoff(ref_ret, g["pairs"], wl.team, wl.P)
     assert np.array_equal(tab["counts"], cnt)
     assert np.array_equal(np.isnan(tab["mean"]), cnt == 0)
     m = cnt > 0
     rep["payoff_max_abs"] = float(np.abs(tab["mean"][m] - mean[m]).max()) if m.any() else 0.0
     assert rep["payoff_max_abs"] <= (1e-3 if full else 1e-9), rep
+    # standard error of the mean, sqrt(sample variance / n), NaN below two
+    # simulations; the table keeps squares in 2^-20 fixed point, so its sum of
+    # squares is within n * 2^-21 of the exact one and its variance within
+    # 2^-21 * n / (n - 1) (+ fp64 cancellation); since |sqrt(a) - sqrt(b)| <=
+    # sqrt(|a - b|), the SE is within sqrt(2^-20 / (n - 1) + 1e-13 * s2 / n^2)
+    se_gpu = tab["stderr"]
+    assert np.array_equal(np.isnan(se_gpu), cnt < 2)
+    k = cnt >= 2
+    if k.any():
+        n = cnt[k].astype(np.float64)
+        var = np.maximum(s2[k] - s1[k] * s1[k] / n, 0.0) / (n - 1.0)
+        se_ora = np.sqrt(var / n)
+        tol_se = np.sqrt(2.0 ** -20 / (n - 1.0) + 1e-13 * s2[k] / (n * n))
+        err = np.abs(se_gpu[k] - se_ora)
+        rep["stderr_max_abs"] = float(err.max())
+        assert np.all(err <= tol_se), (rep, float((err / tol_se).max()))
     if full:
         assert tab["live_frames"] == o["live_frames"]
     say(f"[parity] {wl.name}: {rep}")

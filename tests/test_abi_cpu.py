@@ -125,3 +125,23 @@ def test_product_never_imports_oracle():
             if f.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
                 src = open(os.path.join(dp, f)).read()
                 assert "oracle" not in src.replace("Oracle", ""), f
+
+
+def test_policy_ids_validated_before_device_work():
+    """Policy ids are the caller's keys (Sec. 3.1 pools, Appendix C.2
+    Dict[PolicyID, float]): duplicates are rejected on the host before any
+    device work; the getter rejects a NULL handle and a short buffer."""
+    import paper_2106_07551_amd as M
+    L = M.lib()
+    B = M.binding
+    h = C.c_void_p()
+    d = B.PopDesc()
+    d.kind, d.n_policies, d.n_actions = B.POLICY_TABULAR, 3, 3
+    d.tab_logits = 16      # never dereferenced: validation fails first
+    ids = (C.c_int64 * 3)(5, 7, 5)
+    d.policy_ids = C.cast(ids, C.POINTER(C.c_int64))
+    assert L.malib_pop_create(C.byref(d), None, C.byref(h)) == B.E_INVAL
+    assert b"appears twice" in L.malib_last_error()
+    assert not h.value
+    n = C.c_int32()
+    assert L.malib_pop_policy_ids(None, None, 0, C.byref(n)) == B.E_INVAL

@@ -175,3 +175,39 @@ def test_extend_rejects_mismatch_and_keeps_population():
     pop.extend(1, **_policies(wl, 4, 5))
     assert pop.payoff()["counts"].shape == (5, 5)
     pop.close()
+
+
+def test_policy_ids_echoed_and_extended():
+    """The caller's policy ids (Sec. 3.1 pools keyed by policy id; Appendix
+    C.2 distributions Dict[PolicyID, float]) come back in index order, default
+    to the indices, grow with malib_pop_extend; a colliding id is rejected and
+    leaves the population, its ids and its table unchanged."""
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(1, P=4, per_pair=16)
+    ids = [1001, -7, 42, 2 ** 40]
+    pop = M.Population(M.POLICY_TABULAR, 3, 3, policy_ids=ids[:3],
+                       **_policies(wl, 0, 3))
+    assert pop.policy_ids().tolist() == ids[:3]
+    pairs = wl.pairs[(wl.pairs < 3).all(axis=1)]
+    env = IO.make_env(wl)
+    pop.rollout(env, len(pairs), torch.from_numpy(pairs).cuda(), wl.seed, 1)
+    before = pop.payoff()
+    with pytest.raises(M.MalibError) as e:
+        pop.extend(1, policy_ids=[42], **_policies(wl, 3, 4))
+    assert e.value.status == M.binding.E_INVAL
+    assert pop.P == 3 and pop.policy_ids().tolist() == ids[:3]
+    after = pop.payoff()
+    assert np.array_equal(after["counts"], before["counts"])
+    pop.extend(1, policy_ids=ids[3:], **_policies(wl, 3, 4))
+    assert pop.policy_ids().tolist() == ids
+    t = pop.payoff()
+    assert np.array_equal(t["counts"][:3, :3], before["counts"])
+    pop.close()
+    dflt = M.Population(M.POLICY_TABULAR, 3, 3, **_policies(wl, 0, 3))
+    assert dflt.policy_ids().tolist() == [0, 1, 2]
+    dflt.extend(1, **_policies(wl, 3, 4))
+    assert dflt.policy_ids().tolist() == [0, 1, 2, 3]
+    with pytest.raises(M.MalibError):
+        M.Population(M.POLICY_TABULAR, 3, 3, policy_ids=[9, 9, 1], **_policies(wl, 0, 3))
+    dflt.close()

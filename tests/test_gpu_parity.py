@@ -347,6 +347,38 @@ def test_nan_logits_are_flagged_bf16(c, n_envs):
     pop.close()
 
 
+@pytest.mark.parametrize("bits", [0x7FC00000, 0xFFC00000], ids=["pos_nan", "neg_nan"])
+@pytest.mark.parametrize("layer", [0, 1])
+@pytest.mark.parametrize("c", [2, 3, 4, 5], ids=["iter_f32", "pursuit", "feature_persist",
+                                                 "team"])
+def test_nan_hidden_weights_are_flagged(c, layer, bits):
+    """A NaN weight of either sign in the first or second layer of policy 1
+    reaches every logit of that policy (the hidden ReLU keeps a NaN of either
+    sign) and raises the NaN flag on the device, in the fp32 kernel, the 64-row
+    bf16 kernel and the persistent one; the oracle stops with a NaN logit on an
+    env that plays policy 1, and envs that play only policy 0 still match it."""
+    import paper_2106_07551_amd as M
+    if c == 2:
+        wl = W.make(2, P=2, per_pair=64, horizon=3)
+    elif c == 4:
+        wl = W.make(4, P=2, per_pair=80, horizon=3)    # 640 slots: persistent kernel
+    else:
+        wl = W.make(c, P=2, n_envs=96 if c == 3 else 40, horizon=3)
+    wl.weights = [w.copy() for w in wl.weights]
+    wl.weights[layer][1, 3, 5] = np.frombuffer(np.uint32(bits).tobytes(), np.float32)[0]
+    g = run_gpu(wl, snaps=[0, 2], check=False)
+    t = g["table"]
+    assert t["status"] == M.binding.E_DEVICE and t["device_flags"] & 2, t["device_flags"]
+    uses1 = (g["pairs"] == 1).any(axis=1)
+    e1 = int(np.nonzero(uses1)[0][0])
+    with pytest.raises(RuntimeError, match=r"\(-2\)"):
+        oracle.rollout(wl, [e1], g["pairs"][[e1]], horizon=3)
+    clean = np.nonzero(~uses1)[0]
+    say(f"[nan-hidden] c={c} layer={layer} bits={bits:#x}: {len(clean)} clean envs")
+    if len(clean):
+        check_parity(wl, g, clean)
+
+
 def test_host_validation_errors():
     import paper_2106_07551_amd as M
     from paper_2106_07551_amd import workload_io as IO

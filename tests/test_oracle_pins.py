@@ -235,14 +235,25 @@ def test_meta_sample_shard_invariant():
 
 # -------------------------------------------------------------------- policies
 
-def _torch_mlp_f32(Ws, p, x):
+def _torch_mlp_f32(Ws, bs, p, x):
+    """fp64 torch reference of an fp32 MLP: linear layers with bias, ReLU on
+    the hidden ones."""
     h = torch.from_numpy(np.asarray(x, np.float64))
     L = len(Ws)
     for l in range(L):
-        h = torch.nn.functional.linear(h, torch.from_numpy(Ws[l][p].astype(np.float64)))
+        b = None if bs is None else torch.from_numpy(bs[l][p].astype(np.float64))
+        h = torch.nn.functional.linear(h, torch.from_numpy(Ws[l][p].astype(np.float64)), b)
         if l + 1 < L:
             h = torch.relu(h)
     return h.numpy()
+
+
+def _random_biases(wl, seed, scale=0.3):
+    """Distinct nonzero fp32 biases for every policy and layer (the generated
+    populations have zero biases)."""
+    rng = np.random.default_rng([2106, 7551, 90, seed])
+    wl.biases = [rng.normal(0.0, scale, b.shape).astype(np.float32) for b in wl.biases]
+    return wl
 
 
 def test_mlp_f32_matches_torch():
@@ -251,15 +262,30 @@ def test_mlp_f32_matches_torch():
     for p in range(4):
         x = rng.standard_normal(24)
         got = oracle.policy_logits(wl, p, x)
-        ref = _torch_mlp_f32(wl.weights, p, x)
+        ref = _torch_mlp_f32(wl.weights, None, p, x)
         assert np.allclose(got, ref, rtol=1e-6, atol=1e-6)
+
+
+def test_mlp_f32_biases_match_torch():
+    """fp32 MLP with distinct nonzero biases per policy and layer against torch
+    fp64 linear(x, W, b): the bias enters each unit before its ReLU, from the
+    row of the policy that runs (another policy's biases give other logits)."""
+    wl = _random_biases(W.make(2, P=4, per_pair=1), 1)
+    rng = np.random.default_rng(17)
+    for p in range(4):
+        for _ in range(4):
+            x = rng.standard_normal(24)
+            got = oracle.policy_logits(wl, p, x)
+            ref = _torch_mlp_f32(wl.weights, wl.biases, p, x)
+            assert np.allclose(got, ref, rtol=1e-6, atol=1e-6), p
+            other = _torch_mlp_f32(wl.weights, [np.roll(b, 1, axis=0) for b in wl.biases], p, x)
+            assert not np.allclose(got, other, rtol=1e-6, atol=1e-6)
 
 
 def test_bf16_relu_is_relu_of_the_rounded_value():
     """ReLU of a hidden unit: bf16(max(x, 0)) (torch) for every non-NaN x,
     including -0 (-> +0), tiny negatives, values that round up to a power of
-    two and infinities; a NaN keeps its sign rule (negative NaN -> +0,
-    positive NaN stays NaN)."""
+    two and infinities; a NaN of either sign stays NaN (torch.relu keeps NaN)."""
     xs = [0.0, -0.0, 1e-40, -1e-40, 1.0, -1.0, 3.0e38, -3.0e38, np.inf, -np.inf,
           1.00390625, 1.0039062500001, -2.9e-39, 65504.0, -7.5]
     rng = np.random.default_rng(3)
@@ -269,10 +295,26 @@ def test_bf16_relu_is_relu_of_the_rounded_value():
     ref = np.where(ref == 0, np.float32(0), ref)     # max(-0, 0) is taken as +0
     got = np.array([oracle.bf16_relu(x) for x in xs], np.float32)
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
-    pos_nan = np.frombuffer(np.uint32(0x7FC01234).tobytes(), np.float32)[0]
-    neg_nan = np.frombuffer(np.uint32(0xFFC01234).tobytes(), np.float32)[0]
-    assert np.isnan(oracle.bf16_relu(pos_nan))
-    assert np.float32(oracle.bf16_relu(neg_nan)).view(np.uint32) == 0
+    for bits in (0x7FC01234, 0xFFC01234, 0x7F800001, 0xFF800001):
+        nan = np.frombuffer(np.uint32(bits).tobytes(), np.float32)[0]
+        assert np.isnan(torch.relu(torch.tensor([nan])).item())
+        assert np.isnan(oracle.bf16_relu(nan))
+
+
+def _torch_mlp_bf16(wl, p, x):
+    """torch emulation of a bf16 policy: bf16 input, weights and hidden
+    activations; exact products summed in fp64 and rounded to the fp32
+    accumulator; the fp32 bias added in fp32 to that accumulator, before the
+    hidden ReLU; logits fp32."""
+    bf = lambda t: t.to(torch.bfloat16).to(torch.float64)
+    h = bf(torch.from_numpy(np.asarray(x, np.float64)).float())
+    for l in range(3):
+        w = bf(torch.from_numpy(wl.weights[l][p]))
+        acc = torch.nn.functional.linear(h, w).float()
+        if wl.biases is not None:
+            acc = acc + torch.from_numpy(wl.biases[l][p])
+        h = bf(torch.relu(acc)) if l < 2 else acc.double()
+    return h.numpy()
 
 
 def test_mlp_bf16_matches_torch_emulation():
@@ -280,16 +322,71 @@ def test_mlp_bf16_matches_torch_emulation():
     accumulator; emulated with torch's bf16 conversion and fp64 linear."""
     wl = W.make(3, P=3, n_envs=1)
     rng = np.random.default_rng(8)
-    bf = lambda t: t.to(torch.bfloat16).to(torch.float64)
     for p in range(3):
         x = rng.standard_normal(75)
-        h = bf(torch.from_numpy(x).float())
-        for l in range(3):
-            w = bf(torch.from_numpy(wl.weights[l][p]))
-            acc = torch.nn.functional.linear(h, w).float()
-            h = bf(torch.relu(acc)) if l < 2 else acc.double()
         got = oracle.policy_logits(wl, p, x)
-        assert np.allclose(got, h.numpy(), rtol=1e-5, atol=1e-5)
+        assert np.allclose(got, _torch_mlp_bf16(wl, p, x), rtol=1e-5, atol=1e-5)
+
+
+def test_mlp_bf16_biases_match_torch_emulation():
+    """bf16 policy with distinct nonzero fp32 biases per policy and layer: the
+    bias is added in fp32 after the layer sum is rounded to fp32 and before
+    the ReLU and bf16 rounding of the hidden units (the torch emulation
+    follows that order); another policy's biases give other logits."""
+    wl = _random_biases(W.make(3, P=3, n_envs=1), 2)
+    rng = np.random.default_rng(18)
+    for p in range(3):
+        for _ in range(4):
+            x = rng.standard_normal(75)
+            got = oracle.policy_logits(wl, p, x)
+            assert np.allclose(got, _torch_mlp_bf16(wl, p, x), rtol=1e-5, atol=1e-5), p
+            swapped = W.Workload(**{**wl.__dict__,
+                                    "biases": [np.roll(b, 1, axis=0) for b in wl.biases]})
+            assert not np.allclose(got, _torch_mlp_bf16(swapped, p, x), rtol=1e-5, atol=1e-5)
+
+
+def _tiny_bf16(dims, Ws, bs):
+    wl = W.make(3, P=1, n_envs=1)
+    wl.dims = list(dims)
+    wl.n_actions = dims[-1]
+    wl.weights = [np.asarray(w, np.float32)[None] for w in Ws]
+    wl.biases = [np.asarray(b, np.float32)[None] for b in bs]
+    return wl
+
+
+def test_mlp_bf16_bias_order_hand_values():
+    """Hand-computed bf16 policies that fix where the bias enters.
+    (a) Output unit with inputs h = [1, 2^-30] (exact in bf16), weights [1, 1]
+    and bias 2^-24: the sum 1 + 2^-30 rounds to the fp32 accumulator 1, and
+    1 + 2^-24 is a tie that rounds to even, so the logit is exactly 1.0; adding
+    the bias before the fp32 rounding would give 1 + 2^-23.
+    (b) Hidden unit with pre-activation -1 and bias 0.5: ReLU(-0.5) = 0, so the
+    logit is 0; a bias added after the ReLU would give 0.5."""
+    eye = np.eye(2)
+    wl = _tiny_bf16([2, 2, 2, 1], [eye, eye, [[1.0, 1.0]]],
+                    [[0, 0], [0, 0], [2.0 ** -24]])
+    got = oracle.policy_logits(wl, 0, np.array([1.0, 2.0 ** -30]))
+    assert got[0] == np.float32(1.0), got[0]
+    wl = _tiny_bf16([2, 2, 2, 1], [[[-1.0, 0.0], [0.0, 0.0]], eye, [[1.0, 0.0]]],
+                    [[0.5, 0.0], [0, 0], [0.0]])
+    got = oracle.policy_logits(wl, 0, np.array([1.0, 0.0]))
+    assert got[0] == np.float32(0.0), got[0]
+
+
+def test_mlp_hidden_nan_reaches_the_logits():
+    """A NaN weight (either sign) in a hidden layer of a policy makes all of its
+    logits NaN in both policy kinds, so the rollout stops on it; the other
+    policies are unaffected."""
+    for c, n_in in ((2, 24), (3, 75)):
+        for layer in (0, 1):
+            for bits in (0x7FC00000, 0xFFC00000):
+                wl = W.make(c, P=2, per_pair=1) if c == 2 else W.make(c, P=2, n_envs=1)
+                wl.weights = [w.copy() for w in wl.weights]
+                wl.weights[layer][1, 3, 5] = np.frombuffer(np.uint32(bits).tobytes(),
+                                                           np.float32)[0]
+                x = np.random.default_rng(c).standard_normal(n_in)
+                assert np.isnan(oracle.policy_logits(wl, 1, x)).all(), (c, layer, hex(bits))
+                assert np.isfinite(oracle.policy_logits(wl, 0, x)).all()
 
 
 # ---------------------------------------------------------- matrix game (C1)
@@ -789,3 +886,19 @@ def test_payoff_matrix_is_the_means_with_empty_cells_zero():
     assert g[0, 1] == (float(R[0, 0]) + float(R[1, 0])) / 2
     assert g[2, 3] == float(R[2, 0]) and g[1, 0] == float(R[3, 0])
     assert (g[cnt == 0] == 0.0).all() and not np.isnan(g).any()
+
+
+def test_threaded_oracle_equals_single_thread():
+    """The parity tests split the oracle's envs over threads: the merged
+    result equals one single-threaded rollout of the same envs, element by
+    element (returns, actions, logits, states, counters)."""
+    wl = W.make(5, P=8, n_envs=24, horizon=6)
+    pairs = oracle.meta_sample(wl.sigma, wl.P, wl.n_envs, wl.n_agents, wl.seed)
+    idx = np.arange(3, 24)
+    kw = dict(want_actions=True, want_logits=True, want_states=True, want_rewards=True)
+    a = oracle.rollout(wl, idx, pairs[idx], **kw)
+    b = oracle.rollout_threads(wl, idx, pairs[idx], threads=5, **kw)
+    for k in ("returns", "actions", "logits", "states", "rewards"):
+        assert np.array_equal(a[k], b[k]), k
+    for k in ("near_ties", "flips", "fails", "live_frames"):
+        assert a[k] == b[k], k
