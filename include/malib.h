@@ -348,7 +348,7 @@ malib_status malib_payoff_matrix(malib_pop_t pop, double* M, void* stream);
 /*
  * Fictitious play on the table (the meta-update Comb_{t+1} ~ G(Eval) of
  * Sec. 3.1 with the fictitious-play meta-solver of the PSRO experiments,
- * Sec. 5; get_equilibrium of the example API, Appendix C.2).  The game is
+ * Sec. 4.2; get_equilibrium of the example API, Appendix C.2).  The game is
  * two-player zero-sum: the row side receives M[i][j], the column side
  * -M[i][j].  Each of `iterations` (1 .. 2^24) simultaneous steps plays the
  * first best response of each side to the other's empirical play so far:

@@ -300,7 +300,7 @@ int ora_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, int64_t n_en
 /* ------------------------------------------------------------------------ */
 /* Meta-solver on the payoff table: the meta-update Comb_{t+1} ~ G(...) of    */
 /* Sec. 3.1 with a fictitious-play solver (the FP meta-solver of the PSRO     */
-/* experiments, Sec. 5; get_equilibrium of the example API, Appendix C.2).    */
+/* experiments, Sec. 4.2; get_equilibrium of the example API, Appendix C.2).  */
 /* The table is a two-player zero-sum game: the row side receives M[i][j],   */
 /* the column side -M[i][j].  Simultaneous fictitious play: at iteration t   */
 /* each side best-responds to the other's empirical play so far,             */

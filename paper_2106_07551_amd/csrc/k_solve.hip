@@ -1,6 +1,6 @@
 // Meta-solver on the payoff table and meta-strategy sampling from device
 // weights: the meta-update Comb_{t+1} ~ G(...) of Sec. 3.1 with the
-// fictitious-play solver of the PSRO experiments (Sec. 5), closed on the GPU
+// fictitious-play solver of the PSRO experiments (Sec. 4.2), closed on the GPU
 // (table -> game -> fictitious play -> sigma -> meta-sample -> next rollout).
 #include "device.hpp"
 #include "internal.hpp"

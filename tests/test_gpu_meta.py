@@ -1,7 +1,7 @@
 """GPU parity of the meta-update closed on the device: payoff table -> game
 matrix -> fictitious play -> play counts -> meta-sampling from device weights
 -> next rollout (Sec. 3.1 meta-update with the fictitious-play solver of the
-PSRO experiments, Sec. 5), each step against the oracle through the C ABI.
+PSRO experiments, Sec. 4.2), each step against the oracle through the C ABI.
 
 Bars: play counts and policy ids bit for bit; the game matrix and the gap bit
 for bit (the same fp64 arithmetic on both sides, in the same order); the
