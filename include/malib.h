@@ -257,6 +257,30 @@ malib_status malib_rollout_batch_traj(malib_pop_t pop, const malib_env_desc* env
                                       int64_t env_offset, int32_t horizon, float* returns,
                                       malib_traj* traj, void* stream);
 
+/* ------------------------------------------------------- no allocation */
+
+/*
+ * malib_rollout_batch for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same batch, same kernels, same results bit for bit as
+ * malib_rollout_batch with trace = NULL, but the batch's scratch (logits,
+ * returns, environment state, bucketing tables) lives in one static device
+ * array of the library, 64 MiB (67108864 bytes) per GPU, held from the first
+ * malib_pop_create on that GPU until the process ends; the call makes no
+ * hipMalloc / hipFree and records no HIP-event timing.  The caller still
+ * passes the handle, inputs and outputs.  A batch whose scratch (each buffer
+ * rounded up to 256 bytes) exceeds the array returns MALIB_E_INVAL before any
+ * device work: e.g. the 4v4 game of 16384 envs x 8 seats at d = 256 needs
+ * about 54 MB, the d = 512 feature game of 65536 envs does not fit.
+ * Every call on one GPU shares that GPU's array and overwrites it (the
+ * returns are cleared by the call itself): calls that overlap on one GPU, on
+ * any streams or handles, race and must be serialized by the caller.
+ */
+malib_status malib_rollout_batch_noalloc(malib_pop_t pop, const malib_env_desc* env,
+                                         int64_t n_envs, const int32_t* pair_assign,
+                                         uint64_t seed, int64_t env_offset, int32_t horizon,
+                                         float* returns, void* stream);
+
 /* ------------------------------------------------------------- payoff table */
 
 typedef struct {

@@ -27,7 +27,7 @@ EXPORTS = [
     "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
     "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate", "malib_rollout_batch_traj",
-    "malib_pop_policy_ids",
+    "malib_pop_policy_ids", "malib_rollout_batch_noalloc",
 ]
 
 
@@ -116,6 +116,9 @@ def lib():
         L.malib_pop_extend.restype = i32
         L.malib_expansion_pairs.argtypes = [i32, i32, i32, i32, vp, vp, vp]
         L.malib_expansion_pairs.restype = i32
+        L.malib_rollout_batch_noalloc.argtypes = [vp, C.POINTER(EnvDesc), i64, vp, u64, i64,
+                                                  i32, vp, vp]
+        L.malib_rollout_batch_noalloc.restype = i32
         L.malib_pop_policy_ids.argtypes = [vp, vp, i32, C.POINTER(i32)]
         L.malib_pop_policy_ids.restype = i32
         _lib = L
@@ -220,6 +223,14 @@ class Population:
             self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
             horizon, _dptr(returns), C.byref(tr) if tr is not None else None,
             _stream(stream)))
+
+    def rollout_noalloc(self, env: "Env", n_envs: int, pair_assign, seed: int, horizon: int,
+                        *, env_offset: int = 0, returns=None, stream=None):
+        """malib_rollout_batch_noalloc: the same batch on the library's static
+        scratch (no device allocation; calls on one GPU must not overlap)."""
+        _check(lib().malib_rollout_batch_noalloc(
+            self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
+            horizon, _dptr(returns), _stream(stream)))
 
     def rollout_traj(self, env: "Env", n_envs: int, pair_assign, seed: int, horizon: int,
                      traj: Traj, *, env_offset: int = 0, returns=None, stream=None):

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -17,18 +18,53 @@ using namespace malib;
 
 struct malib_pop : public Pop {};
 
+// Scratch of malib_rollout_batch_noalloc: one static device array per GPU the
+// library runs on (held until the process ends).  Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in for the symbol):
+// its device address is looked up once per device with hipGetSymbolAddress
+// and kept in g_scratch_addr.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+}  // namespace
+
+// The current device's address of `scratch` (looked up on the first call for
+// that device, with the device current).  Null on failure (*err says why).
+static void* scratch_address(int device, hipError_t* err)
+{
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (device < 0 || device >= kMaxDevices) {
+        *err = hipErrorInvalidDevice;
+        return nullptr;
+    }
+    if (!g_scratch_addr[device] && g_scratch_err[device] == hipSuccess) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e == hipSuccess && ptr)
+            g_scratch_addr[device] = ptr;
+        else
+            g_scratch_err[device] = e == hipSuccess ? hipErrorInvalidSymbol : e;
+    }
+    *err = g_scratch_err[device];
+    return g_scratch_addr[device];
+}
+
 namespace {
 
-thread_local std::string g_last_error;
+// fixed-size, so that reporting an error allocates nothing
+thread_local char g_last_error[512];
 
 malib_status fail(malib_status code, const char* fmt, ...)
 {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
     va_end(ap);
-    g_last_error = buf;
     return code;
 }
 
@@ -120,7 +156,7 @@ int64_t snap_bytes_per_env(int kind, int d)
 
 extern "C" {
 
-const char* malib_last_error(void) { return g_last_error.c_str(); }
+const char* malib_last_error(void) { return g_last_error; }
 
 // ------------------------------------------------------------------- create
 
@@ -233,6 +269,11 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
     } while (0)
     TRY(hipGetDevice(&p->device));
     TRY(hipDeviceGetAttribute(&p->n_cus, hipDeviceAttributeMultiprocessorCount, p->device));
+    {
+        // set-up of the no-allocation entry point on this device
+        hipError_t e = hipSuccess;
+        p->scratch = scratch_address(p->device, &e);
+    }
     p->kind = desc->kind;
     p->P = P;
     p->A = A;
@@ -499,10 +540,36 @@ malib_status malib_expansion_pairs(int32_t n_policies, int32_t first_new, int32_
 
 // ------------------------------------------------------------------ rollout
 
-static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
-                                 const int32_t* pair_assign, uint64_t seed, int64_t env_offset,
-                                 int32_t horizon, float* returns, const malib_trace* trace,
-                                 const malib_traj* traj, void* stream)
+// Everything a rollout batch needs besides its device buffers: the validated
+// environment arguments and the shapes of the buffers.
+struct RolloutPlan {
+    EnvArgs ea{};
+    int8_t team[kMaxAgents];
+    int64_t ns = 0;               // agent slots
+    bool mlp = false, persist = false, bf16_obs = false;
+    int tile_rows = 0, max_tiles = 0, n_chunks = 0;
+    int64_t state_bytes = 0;      // one state buffer (FEATURE has two)
+};
+
+// Device buffers of one rollout batch (from the handle, or carved from the
+// no-allocation scratch).
+struct RolloutBufs {
+    float* logits = nullptr;
+    float* ret = nullptr;
+    void* state0 = nullptr;
+    void* state1 = nullptr;
+    uint8_t* done = nullptr;
+    float* wt = nullptr;
+    uint16_t* obs = nullptr;
+    int32_t *perm = nullptr, *perm_env = nullptr, *hist = nullptr, *base = nullptr,
+            *offsets = nullptr, *tile_off = nullptr;
+    int4* tile_info = nullptr;
+};
+
+// Host-side validation of a batch (no device work) and its plan.
+static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
+                                 const int32_t* pair_assign, int64_t env_offset, int32_t horizon,
+                                 RolloutPlan& plan)
 {
     if (!pop)
         return fail(MALIB_E_INVAL, "pop is NULL");
@@ -510,7 +577,6 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
         return fail(MALIB_E_INVAL, "env is NULL");
     if (!pair_assign)
         return fail(MALIB_E_INVAL, "pair_assign is NULL");
-    hipStream_t s = (hipStream_t)stream;
     const int n_agents = env->n_agents;
     if (n_agents < 1 || n_agents > kMaxAgents)
         return fail(MALIB_E_INVAL, "n_agents must be in [1, %d]", kMaxAgents);
@@ -527,7 +593,7 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
         return fail(MALIB_E_INVAL, "env_offset must be >= 0");
     if (env->init_mode != MALIB_INIT_PER_ENV && env->init_mode != MALIB_INIT_SHARED)
         return fail(MALIB_E_INVAL, "unknown init_mode %d", env->init_mode);
-    int8_t team[kMaxAgents];
+    int8_t* team = plan.team;
     if (env->team) {
         for (int k = 0; k < n_agents; ++k) {
             team[k] = env->team[k];
@@ -540,7 +606,7 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
         team[0] = 1;
         team[1] = -1;
     }
-    EnvArgs ea{};
+    EnvArgs& ea = plan.ea;
     ea.kind = env->kind;
     ea.n_agents = n_agents;
     ea.A = env->n_actions;
@@ -596,59 +662,105 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
     }
     if (ea.team_row == 0 || ea.team_col == 0)
         return fail(MALIB_E_INVAL, "both sides need at least one seat");
-    std::vector<int> snap_of(horizon, -1);
-    if (trace && trace->n_snap > 0) {
-        if (!trace->snap_steps)
-            return fail(MALIB_E_INVAL, "trace: snap_steps is NULL");
-        for (int i = 0; i < trace->n_snap; ++i) {
-            int st = trace->snap_steps[i];
-            if (st < 0 || st >= horizon)
-                return fail(MALIB_E_INVAL, "trace: snapshot step %d outside [0, %d)", st,
-                            horizon);
-            snap_of[st] = i;
-        }
-    }
-
-    // ---- buffers
     const int64_t ns = n_envs * n_agents;
-    const bool mlp = pop->kind != MALIB_POLICY_TABULAR;
-    const bool persist = pop->kind == MALIB_POLICY_MLP_BF16 &&
-                         use_persist_kernel(env->kind, pop->in_pad, ns, pop->P);
-    const int tile_rows = pop->kind == MALIB_POLICY_MLP_BF16
-                              ? (persist ? kPersistRows : kBf16TileRows)
-                              : kF32TileRows;
-    const int max_tiles = max_tiles_for(ns, pop->P, tile_rows);
-    const int n_chunks = (int)((ns + kBucketChunk - 1) / kBucketChunk);
-    HIP_TRY(ensure(pop->logits, sizeof(float) * ns * pop->A));
-    HIP_TRY(ensure(pop->ret, sizeof(float) * ns));
-    int64_t sb = state_bytes_per_env(env->kind, env->d) * n_envs;
-    if (sb > 0) {
-        HIP_TRY(ensure(pop->state0, sb));
-        if (env->kind == MALIB_ENV_FEATURE)
-            HIP_TRY(ensure(pop->state1, sb));
-    }
-    if (env->kind == MALIB_ENV_PURSUIT)
-        HIP_TRY(ensure(pop->done, n_envs));
-    if (env->kind == MALIB_ENV_FEATURE)
-        HIP_TRY(ensure(pop->wt, sizeof(float) * env->d * env->d));
+    plan.ns = ns;
+    plan.mlp = pop->kind != MALIB_POLICY_TABULAR;
+    plan.persist = pop->kind == MALIB_POLICY_MLP_BF16 &&
+                   use_persist_kernel(env->kind, pop->in_pad, ns, pop->P);
+    plan.tile_rows = pop->kind == MALIB_POLICY_MLP_BF16
+                         ? (plan.persist ? kPersistRows : kBf16TileRows)
+                         : kF32TileRows;
+    plan.max_tiles = max_tiles_for(ns, pop->P, plan.tile_rows);
+    plan.n_chunks = (int)((ns + kBucketChunk - 1) / kBucketChunk);
+    plan.state_bytes = state_bytes_per_env(env->kind, env->d) * n_envs;
     // bf16 observation rows for the 64-row policy kernel (its gather reads half
     // the bytes); the persistent kernel converts the fp32 state itself, since
     // at d = 512 the extra rows cost the env step more than they save
-    const bool bf16_obs =
-        env->kind == MALIB_ENV_FEATURE && pop->kind == MALIB_POLICY_MLP_BF16 && !persist;
-    if (bf16_obs)
-        HIP_TRY(ensure(pop->obs, sizeof(uint16_t) * env->d * n_envs));
-    if (mlp) {
-        HIP_TRY(ensure(pop->perm, sizeof(int32_t) * ns));
-        HIP_TRY(ensure(pop->perm_env, sizeof(int32_t) * ns));
-        HIP_TRY(ensure(pop->tile_info, sizeof(int4) * (size_t)max_tiles));
-        HIP_TRY(ensure(pop->hist, sizeof(int32_t) * (size_t)pop->P * n_chunks));
-        HIP_TRY(ensure(pop->base, sizeof(int32_t) * (size_t)pop->P * n_chunks));
-        HIP_TRY(ensure(pop->offsets, sizeof(int32_t) * (pop->P + 1)));
-        HIP_TRY(ensure(pop->tile_off, sizeof(int32_t) * (pop->P + 1)));
+    plan.bf16_obs =
+        env->kind == MALIB_ENV_FEATURE && pop->kind == MALIB_POLICY_MLP_BF16 && !plan.persist;
+    return MALIB_OK;
+}
+
+// Byte sizes of the batch's buffers, in the order of RolloutBufs (0 = unused).
+static void buffer_sizes(const Pop& pop, const malib_env_desc* env, int64_t n_envs,
+                         const RolloutPlan& plan, size_t (&sz)[14])
+{
+    const int64_t ns = plan.ns;
+    const bool feat = env->kind == MALIB_ENV_FEATURE;
+    sz[0] = sizeof(float) * ns * pop.A;                                  // logits
+    sz[1] = sizeof(float) * ns;                                          // ret
+    sz[2] = plan.state_bytes;                                            // state0
+    sz[3] = feat ? plan.state_bytes : 0;                                 // state1
+    sz[4] = env->kind == MALIB_ENV_PURSUIT ? n_envs : 0;                 // done
+    sz[5] = feat ? sizeof(float) * env->d * env->d : 0;                  // wt
+    sz[6] = plan.bf16_obs ? sizeof(uint16_t) * env->d * n_envs : 0;     // obs
+    const size_t pc = (size_t)pop.P * plan.n_chunks;
+    sz[7] = plan.mlp ? sizeof(int32_t) * ns : 0;                         // perm
+    sz[8] = plan.mlp ? sizeof(int32_t) * ns : 0;                         // perm_env
+    sz[9] = plan.mlp ? sizeof(int32_t) * pc : 0;                         // hist
+    sz[10] = plan.mlp ? sizeof(int32_t) * pc : 0;                        // base
+    sz[11] = plan.mlp ? sizeof(int32_t) * (pop.P + 1) : 0;               // offsets
+    sz[12] = plan.mlp ? sizeof(int32_t) * (pop.P + 1) : 0;               // tile_off
+    sz[13] = plan.mlp ? sizeof(int4) * (size_t)plan.max_tiles : 0;       // tile_info
+}
+
+static void assign_bufs(void* const (&ptr)[14], RolloutBufs& b)
+{
+    b.logits = (float*)ptr[0];
+    b.ret = (float*)ptr[1];
+    b.state0 = ptr[2];
+    b.state1 = ptr[3];
+    b.done = (uint8_t*)ptr[4];
+    b.wt = (float*)ptr[5];
+    b.obs = (uint16_t*)ptr[6];
+    b.perm = (int32_t*)ptr[7];
+    b.perm_env = (int32_t*)ptr[8];
+    b.hist = (int32_t*)ptr[9];
+    b.base = (int32_t*)ptr[10];
+    b.offsets = (int32_t*)ptr[11];
+    b.tile_off = (int32_t*)ptr[12];
+    b.tile_info = (int4*)ptr[13];
+}
+
+// The handle's growable buffers, enlarged as needed (may call hipMalloc).
+static malib_status handle_bufs(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
+                                const RolloutPlan& plan, RolloutBufs& b)
+{
+    size_t sz[14];
+    buffer_sizes(*pop, env, n_envs, plan, sz);
+    DevBuf* db[14] = {&pop->logits, &pop->ret, &pop->state0, &pop->state1, &pop->done,
+                      &pop->wt, &pop->obs, &pop->perm, &pop->perm_env, &pop->hist,
+                      &pop->base, &pop->offsets, &pop->tile_off, &pop->tile_info};
+    void* ptr[14];
+    for (int i = 0; i < 14; ++i) {
+        ptr[i] = nullptr;
+        if (sz[i]) {
+            HIP_TRY(ensure(*db[i], sz[i]));
+            ptr[i] = db[i]->ptr;
+        }
     }
-    ea.WT = (const float*)pop->wt.ptr;
-    ea.obs = bf16_obs ? (uint16_t*)pop->obs.ptr : nullptr;
+    assign_bufs(ptr, b);
+    return MALIB_OK;
+}
+
+// The launch sequence of one batch on buffers `b`: set-up (returns cleared,
+// bucketing, reset), `horizon` steps of policy forward -> env step (sampling
+// inside), then the payoff reduction into the handle's table.  `snap_of`
+// (host, [horizon], or NULL) maps a step to its trace snapshot; `prof`
+// enables the handle's HIP-event timing.
+static malib_status launch_rollout(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
+                                   const int32_t* pair_assign, uint64_t seed,
+                                   int64_t env_offset, int32_t horizon, float* returns,
+                                   const malib_trace* trace, const int* snap_of,
+                                   const malib_traj* traj, RolloutPlan& plan,
+                                   const RolloutBufs& b, bool prof, hipStream_t s)
+{
+    EnvArgs& ea = plan.ea;
+    const int n_agents = env->n_agents;
+    const int64_t ns = plan.ns;
+    const bool mlp = plan.mlp, persist = plan.persist;
+    ea.WT = b.wt;
+    ea.obs = plan.bf16_obs ? b.obs : nullptr;
     if (traj) {
         ea.tr.act = traj->actions;
         ea.tr.rew = traj->rewards;
@@ -658,40 +770,41 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
         ea.tr.cap = traj->capacity;
         ea.tr.horizon = horizon;
     }
-    float* ret = (float*)pop->ret.ptr;
-    float* logits = (float*)pop->logits.ptr;
-    uint8_t* done = env->kind == MALIB_ENV_PURSUIT ? (uint8_t*)pop->done.ptr : nullptr;
-    void* cur = pop->state0.ptr;
-    void* nxt = env->kind == MALIB_ENV_FEATURE ? pop->state1.ptr : pop->state0.ptr;
-    int32_t* perm = (int32_t*)pop->perm.ptr;
-    int32_t* offsets = (int32_t*)pop->offsets.ptr;
-    int32_t* tile_off = (int32_t*)pop->tile_off.ptr;
+    float* ret = b.ret;
+    float* logits = b.logits;
+    uint8_t* done = env->kind == MALIB_ENV_PURSUIT ? b.done : nullptr;
+    void* cur = b.state0;
+    void* nxt = env->kind == MALIB_ENV_FEATURE ? b.state1 : b.state0;
+    auto pbeg = [&](int kind) { return prof ? prof_begin(*pop, kind, s) : -1; };
+    auto pend = [&](int i) {
+        if (prof)
+            prof_end(*pop, i, s);
+    };
 
-    // ---- set-up: bucketing, reset, returns
-    int pi = prof_begin(*pop, MALIB_K_SETUP, s);
-    HIP_TRY(hipMemsetAsync(ret, 0, sizeof(float) * ns, s));
+    // ---- set-up: returns cleared (a fill kernel, no memset), bucketing, reset
+    int pi = pbeg(MALIB_K_SETUP);
+    HIP_TRY(launch_zero_f32(ret, ns, s));
     if (mlp)
-        HIP_TRY(launch_bucket(pair_assign, ns, n_agents, pop->P, tile_rows, max_tiles,
-                              (int32_t*)pop->hist.ptr, (int32_t*)pop->base.ptr, perm,
-                              (int32_t*)pop->perm_env.ptr, offsets, tile_off,
-                              (int4*)pop->tile_info.ptr, pop->dev_flags, s));
+        HIP_TRY(launch_bucket(pair_assign, ns, n_agents, pop->P, plan.tile_rows, plan.max_tiles,
+                              b.hist, b.base, b.perm, b.perm_env, b.offsets, b.tile_off,
+                              b.tile_info, pop->dev_flags, s));
     HIP_TRY(launch_reset(ea, n_envs, seed, env_offset, cur, done, s));
     if (env->kind == MALIB_ENV_FEATURE)
-        HIP_TRY(launch_transpose(env->W, (float*)pop->wt.ptr, env->d, s));
-    prof_end(*pop, pi, s);
+        HIP_TRY(launch_transpose(env->W, b.wt, env->d, s));
+    pend(pi);
     if (trace && mlp) {
         if (trace->perm)
-            HIP_TRY(hipMemcpyAsync(trace->perm, perm, sizeof(int32_t) * ns,
+            HIP_TRY(hipMemcpyAsync(trace->perm, b.perm, sizeof(int32_t) * ns,
                                    hipMemcpyDeviceToDevice, s));
         if (trace->offsets)
-            HIP_TRY(hipMemcpyAsync(trace->offsets, offsets, sizeof(int32_t) * (pop->P + 1),
+            HIP_TRY(hipMemcpyAsync(trace->offsets, b.offsets, sizeof(int32_t) * (pop->P + 1),
                                    hipMemcpyDeviceToDevice, s));
     }
 
     // ---- the step loop
     const int64_t snap_b = snap_bytes_per_env(env->kind, env->d) * n_envs;
     for (int t = 0; t < horizon; ++t) {
-        int si = snap_of[t];
+        const int si = snap_of ? snap_of[t] : -1;
         if (si >= 0 && trace->states && snap_b > 0) {
             uint8_t* dst = (uint8_t*)trace->states + (int64_t)si * snap_b;
             if (env->kind == MALIB_ENV_PURSUIT)
@@ -699,23 +812,20 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
             else
                 HIP_TRY(hipMemcpyAsync(dst, cur, snap_b, hipMemcpyDeviceToDevice, s));
         }
-        pi = prof_begin(*pop, MALIB_K_POLICY, s);
+        pi = pbeg(MALIB_K_POLICY);
         if (pop->kind == MALIB_POLICY_TABULAR)
             HIP_TRY(launch_tabular(pop->tab, pair_assign, ns, pop->A, pop->P, pop->dev_flags,
                                    logits, s));
         else if (pop->kind == MALIB_POLICY_MLP_F32)
-            HIP_TRY(launch_mlp_f32(*pop, perm, (const int4*)pop->tile_info.ptr, ns, n_agents,
-                                   cur, logits, s));
+            HIP_TRY(launch_mlp_f32(*pop, b.perm, b.tile_info, ns, n_agents, cur, logits, s));
         else if (persist)
-            HIP_TRY(launch_mlp_bf16_persist(*pop, perm, (const int32_t*)pop->perm_env.ptr,
-                                            (const int4*)pop->tile_info.ptr, tile_off, ns,
-                                            n_agents, cur, logits, s));
+            HIP_TRY(launch_mlp_bf16_persist(*pop, b.perm, b.perm_env, b.tile_info, b.tile_off,
+                                            ns, n_agents, cur, logits, s));
         else
-            HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d, tile_rows,
-                                    perm, (const int32_t*)pop->perm_env.ptr,
-                                    (const int4*)pop->tile_info.ptr, ns,
-                                    bf16_obs ? (const void*)ea.obs : cur, logits, s));
-        prof_end(*pop, pi, s);
+            HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d,
+                                    plan.tile_rows, b.perm, b.perm_env, b.tile_info, ns,
+                                    plan.bf16_obs ? (const void*)ea.obs : cur, logits, s));
+        pend(pi);
         if (si >= 0 && trace->logits)
             HIP_TRY(hipMemcpyAsync(trace->logits + (int64_t)si * ns * pop->A, logits,
                                    sizeof(float) * ns * pop->A, hipMemcpyDeviceToDevice, s));
@@ -727,25 +837,61 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
         sa.t = t;
         sa.log = (trace && trace->actions) ? trace->actions + (int64_t)t * ns : nullptr;
         sa.flags = pop->dev_flags;
-        pi = prof_begin(*pop, MALIB_K_ENV, s);
+        pi = pbeg(MALIB_K_ENV);
         HIP_TRY(launch_env_step(ea, sa, n_envs, cur, nxt, done, ret, pop->dev_frames, s));
-        prof_end(*pop, pi, s);
+        pend(pi);
         std::swap(cur, nxt);
         if (env->kind != MALIB_ENV_FEATURE)
             nxt = cur;
     }
 
     // ---- payoff reduction
-    pi = prof_begin(*pop, MALIB_K_PAYOFF, s);
-    HIP_TRY(launch_payoff(ret, pair_assign, n_envs, n_agents, team, pop->P, pop->sum,
+    pi = pbeg(MALIB_K_PAYOFF);
+    HIP_TRY(launch_payoff(ret, pair_assign, n_envs, n_agents, plan.team, pop->P, pop->sum,
                           pop->sumsq, pop->cnt, s));
-    prof_end(*pop, pi, s);
+    pend(pi);
     if (returns)
         HIP_TRY(hipMemcpyAsync(returns, ret, sizeof(float) * ns, hipMemcpyDeviceToDevice, s));
     if (env->kind != MALIB_ENV_PURSUIT)
         pop->host_frames += ns * (int64_t)horizon;
     pop->envs += n_envs;
     return MALIB_OK;
+}
+
+static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
+                                 const int32_t* pair_assign, uint64_t seed, int64_t env_offset,
+                                 int32_t horizon, float* returns, const malib_trace* trace,
+                                 const malib_traj* traj, void* stream)
+{
+    RolloutPlan plan;
+    {
+        const malib_status st =
+            plan_rollout(pop, env, n_envs, pair_assign, env_offset, horizon, plan);
+        if (st != MALIB_OK)
+            return st;
+    }
+    std::vector<int> snap_of;
+    if (trace && trace->n_snap > 0) {
+        if (!trace->snap_steps)
+            return fail(MALIB_E_INVAL, "trace: snap_steps is NULL");
+        snap_of.assign(horizon, -1);
+        for (int i = 0; i < trace->n_snap; ++i) {
+            int st = trace->snap_steps[i];
+            if (st < 0 || st >= horizon)
+                return fail(MALIB_E_INVAL, "trace: snapshot step %d outside [0, %d)", st,
+                            horizon);
+            snap_of[st] = i;
+        }
+    }
+    RolloutBufs b;
+    {
+        const malib_status st = handle_bufs(pop, env, n_envs, plan, b);
+        if (st != MALIB_OK)
+            return st;
+    }
+    return launch_rollout(pop, env, n_envs, pair_assign, seed, env_offset, horizon, returns,
+                          trace, snap_of.empty() ? nullptr : snap_of.data(), traj, plan, b,
+                          true, (hipStream_t)stream);
 }
 
 malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
@@ -773,6 +919,48 @@ malib_status malib_rollout_batch_traj(malib_pop_t pop, const malib_env_desc* env
     if (st == MALIB_OK)
         traj->cursor += (int64_t)horizon * n_envs;
     return st;
+}
+
+// -------------------------------------------------------- no allocation
+
+malib_status malib_rollout_batch_noalloc(malib_pop_t pop, const malib_env_desc* env,
+                                         int64_t n_envs, const int32_t* pair_assign,
+                                         uint64_t seed, int64_t env_offset, int32_t horizon,
+                                         float* returns, void* stream)
+{
+    RolloutPlan plan;
+    {
+        const malib_status st =
+            plan_rollout(pop, env, n_envs, pair_assign, env_offset, horizon, plan);
+        if (st != MALIB_OK)
+            return st;
+    }
+    if (!pop->scratch) {
+        hipError_t e = hipSuccess;
+        (void)scratch_address(pop->device, &e);
+        return fail(MALIB_E_HIP, "the no-allocation scratch has no device address: %s",
+                    hipGetErrorString(e));
+    }
+    size_t sz[14];
+    buffer_sizes(*pop, env, n_envs, plan, sz);
+    void* ptr[14];
+    size_t off = 0;
+    for (int i = 0; i < 14; ++i) {
+        ptr[i] = nullptr;
+        if (sz[i]) {
+            ptr[i] = (unsigned char*)pop->scratch + off;
+            off += (sz[i] + 255) / 256 * 256;
+        }
+    }
+    if (off > kNoAllocScratchBytes)
+        return fail(MALIB_E_INVAL,
+                    "the batch needs %zu bytes of scratch, above the %zu bytes of "
+                    "malib_rollout_batch_noalloc (use malib_rollout_batch)",
+                    off, kNoAllocScratchBytes);
+    RolloutBufs b;
+    assign_bufs(ptr, b);
+    return launch_rollout(pop, env, n_envs, pair_assign, seed, env_offset, horizon, returns,
+                          nullptr, nullptr, nullptr, plan, b, false, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------- payoff

@@ -68,6 +68,9 @@ struct Pop {
     // scratch, grown on demand
     DevBuf perm, perm_env, tile_info, hist, base, offsets, tile_off, logits, ret, state0,
         state1, obs, wt, done, thresholds;
+    // device address of the library's static no-allocation scratch on this
+    // handle's device (resolved at creation; null if that failed)
+    void* scratch = nullptr;
     Profile prof;
 };
 
@@ -151,6 +154,7 @@ struct EnvArgs {
     uint16_t* obs;
     TrajArgs tr;
 };
+hipError_t launch_zero_f32(float* x, int64_t n, hipStream_t s);
 hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,
                         void* state, uint8_t* done, hipStream_t s);
 hipError_t launch_transpose(const float* W, float* WT, int d, hipStream_t s);

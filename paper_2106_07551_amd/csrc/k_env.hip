@@ -20,6 +20,22 @@ __device__ __forceinline__ int64_t traj_rec(const TrajArgs& tr, int t, int64_t n
 
 // ---------------------------------------------------------------- reset
 
+// x[0..n) = 0 with a kernel rather than a memset node, so that a caller may
+// capture the launch sequence in a HIP graph.
+__global__ void zero_f32_kernel(float* __restrict__ x, int64_t n)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        x[i] = 0.0f;
+}
+
+hipError_t launch_zero_f32(float* x, int64_t n, hipStream_t s)
+{
+    if (n > 0)
+        zero_f32_kernel<<<(int)((n + 255) / 256), 256, 0, s>>>(x, n);
+    return hipGetLastError();
+}
+
 __global__ void reset_iter_kernel(uint16_t* __restrict__ hist, int64_t n)
 {
     int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

@@ -1,0 +1,93 @@
+"""The no-allocation rollout (malib_rollout_batch_noalloc) against
+malib_rollout_batch: the same batches through the C ABI on two handles built
+from the same population, one per entry point, two calls in a row (the second
+with fewer envs, so the static scratch still holds the first call's larger
+contents); returns and the whole table must be equal bit for bit.  A batch
+whose scratch exceeds the static array is rejected before any device work.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from gpu_helpers import say
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+SCRATCH_BYTES = 64 << 20      # the array size stated in include/malib.h
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _batch(pop, env, wl, pairs, n, offset, noalloc):
+    ret = torch.empty((wl.n_agents, n), dtype=torch.float32, device="cuda")
+    pt = torch.from_numpy(np.ascontiguousarray(pairs[:n], dtype=np.int32)).cuda()
+    f = pop.rollout_noalloc if noalloc else pop.rollout
+    f(env, n, pt, wl.seed, wl.horizon, env_offset=offset, returns=ret)
+    tab = pop.payoff(reset=True)
+    return ret.cpu().numpy(), tab
+
+
+def _pairs(wl):
+    import oracle
+    if wl.pairs is not None:
+        return wl.pairs
+    return oracle.meta_sample(wl.sigma, wl.P, wl.n_envs, wl.n_agents, wl.seed)
+
+
+CASES = {
+    "team_full": lambda: W.make(5),                                   # 16384 x 8, d = 256
+    "feature_d512_persistent": lambda: W.make(4, P=4, per_pair=40, horizon=20),
+    "pursuit": lambda: W.make(3, n_envs=4000, horizon=60),
+    "iter": lambda: W.make(2, P=8, per_pair=64),
+    "matrix": lambda: W.make(1, per_pair=512),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_noalloc_matches_rollout_batch(name):
+    from paper_2106_07551_amd import workload_io as IO
+    wl = CASES[name]()
+    pairs = _pairs(wl)
+    env = IO.make_env(wl)
+    pa, pb = IO.make_population(wl), IO.make_population(wl)
+    n1, n2 = wl.n_envs, max(1, wl.n_envs // 3 + 7)
+    for n, offset in ((n1, 0), (n2, 12345)):
+        say(f"[noalloc] {name}: n_envs={n} offset={offset}")
+        ra, ta = _batch(pa, env, wl, pairs, n, offset, noalloc=False)
+        rb, tb = _batch(pb, env, wl, pairs, n, offset, noalloc=True)
+        assert np.array_equal(ra.view(np.uint32), rb.view(np.uint32)), name
+        assert np.array_equal(ta["counts"], tb["counts"])
+        for k in ("mean", "stderr"):
+            assert np.array_equal(np.isnan(ta[k]), np.isnan(tb[k]))
+            m = ~np.isnan(ta[k])
+            assert np.array_equal(ta[k][m].view(np.uint64), tb[k][m].view(np.uint64)), k
+        assert ta["live_frames"] == tb["live_frames"] and ta["envs"] == tb["envs"] == n
+        assert tb["status"] == 0
+    pa.close()
+    pb.close()
+
+
+def test_noalloc_rejects_batches_beyond_the_scratch():
+    """The d = 512 feature game at full size (65536 envs: 268 MB of state) does
+    not fit the 64 MiB array: MALIB_E_INVAL before any device work, the table
+    untouched; the same handle then runs a batch that fits."""
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(4, P=4, per_pair=4096, horizon=2)
+    assert wl.n_envs * wl.d * 4 * 2 > SCRATCH_BYTES
+    pop = IO.make_population(wl)
+    env = IO.make_env(wl)
+    pt = torch.from_numpy(wl.pairs).cuda()
+    with pytest.raises(M.MalibError) as e:
+        pop.rollout_noalloc(env, wl.n_envs, pt, wl.seed, 2)
+    assert e.value.status == M.binding.E_INVAL and "scratch" in str(e.value)
+    t = pop.payoff()
+    assert t["counts"].sum() == 0 and t["envs"] == 0
+    pop.rollout_noalloc(env, 256, pt, wl.seed, 2)
+    assert pop.payoff()["counts"].sum() == 256
+    pop.close()
