@@ -223,6 +223,30 @@ def test_parity_team_2v2_large_buckets_hidden_widths(hid):
     check_parity(wl, g)
 
 
+@pytest.mark.parametrize("P", [8, 64])
+def test_parity_team_many_tiles_sampled(P):
+    """4v4 d=256 game with the 256-512-512-18 policies: 6000 envs x 8 seats =
+    48000 slots, 750+ 64-row tiles (more than one round of workgroups, ragged
+    policy ends); the oracle replays a sample of envs whose slots fall in most
+    tiles."""
+    wl = W.team_variant(8, P=P, n_envs=6000, horizon=3, dims=[256, 512, 512, 18])
+    g = run_gpu(wl, snaps=[0, 2])
+    rng = np.random.default_rng(P)
+    sel = np.unique(np.concatenate([[0, 1, wl.n_envs - 1],
+                                    rng.choice(wl.n_envs, 250, replace=False)]))
+    check_parity(wl, g, sel)
+
+
+def test_parity_team_large_buckets_biases():
+    """4v4 d=256 game, 256-512-512-18 policies with nonzero biases, 4
+    policies, 300 envs (2400 slots, several full tiles per policy), every env
+    against the oracle."""
+    wl = _with_biases(W.team_variant(8, d=256, P=4, n_envs=300, horizon=3,
+                                     dims=[256, 512, 512, 18]), 6)
+    g = run_gpu(wl, snaps=[0, 2])
+    check_parity(wl, g)
+
+
 @pytest.mark.parametrize("d", [256, 512])
 def test_parity_many_tiles_sampled(d):
     """80000 slots (more tiles than workgroups: 64-row tiles for d=256, several
