@@ -344,7 +344,7 @@ void malib_pop_destroy(malib_pop_t p)
         (void)hipHostFree(p->host_acc);
     for (DevBuf* b : {&p->perm, &p->perm_env, &p->tile_info, &p->hist, &p->base, &p->offsets, &p->tile_off, &p->logits,
                       &p->ret, &p->state0, &p->state1, &p->obs, &p->wt, &p->done,
-                      &p->thresholds})
+                      &p->thresholds, &p->actions})
         release(*b);
     for (auto& ev : p->prof.pool) {
         (void)hipEventDestroy(ev.start);
@@ -547,6 +547,7 @@ struct RolloutPlan {
     int8_t team[kMaxAgents];
     int64_t ns = 0;               // agent slots
     bool mlp = false, persist = false, bf16_obs = false;
+    bool kernel_sample = false;   // the 64-row policy kernel samples the actions
     int tile_rows = 0, max_tiles = 0, n_chunks = 0;
     int64_t state_bytes = 0;      // one state buffer (FEATURE has two)
 };
@@ -564,7 +565,10 @@ struct RolloutBufs {
     int32_t *perm = nullptr, *perm_env = nullptr, *hist = nullptr, *base = nullptr,
             *offsets = nullptr, *tile_off = nullptr;
     int4* tile_info = nullptr;
+    uint8_t* actions = nullptr;   // actions sampled by the policy kernel
 };
+
+constexpr int kNumBufs = 15;
 
 // Host-side validation of a batch (no device work) and its plan.
 static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
@@ -678,12 +682,16 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
     // at d = 512 the extra rows cost the env step more than they save
     plan.bf16_obs =
         env->kind == MALIB_ENV_FEATURE && pop->kind == MALIB_POLICY_MLP_BF16 && !plan.persist;
+    // feature games with the 64-row kernel: Gumbel-max sampling in the policy
+    // kernel (its noise is drawn while the observation rows are fetched), so
+    // the env step only reads one action byte per slot
+    plan.kernel_sample = plan.bf16_obs;
     return MALIB_OK;
 }
 
 // Byte sizes of the batch's buffers, in the order of RolloutBufs (0 = unused).
 static void buffer_sizes(const Pop& pop, const malib_env_desc* env, int64_t n_envs,
-                         const RolloutPlan& plan, size_t (&sz)[14])
+                         const RolloutPlan& plan, size_t (&sz)[kNumBufs])
 {
     const int64_t ns = plan.ns;
     const bool feat = env->kind == MALIB_ENV_FEATURE;
@@ -702,9 +710,10 @@ static void buffer_sizes(const Pop& pop, const malib_env_desc* env, int64_t n_en
     sz[11] = plan.mlp ? sizeof(int32_t) * (pop.P + 1) : 0;               // offsets
     sz[12] = plan.mlp ? sizeof(int32_t) * (pop.P + 1) : 0;               // tile_off
     sz[13] = plan.mlp ? sizeof(int4) * (size_t)plan.max_tiles : 0;       // tile_info
+    sz[14] = plan.kernel_sample ? (size_t)ns : 0;                        // actions
 }
 
-static void assign_bufs(void* const (&ptr)[14], RolloutBufs& b)
+static void assign_bufs(void* const (&ptr)[kNumBufs], RolloutBufs& b)
 {
     b.logits = (float*)ptr[0];
     b.ret = (float*)ptr[1];
@@ -720,19 +729,21 @@ static void assign_bufs(void* const (&ptr)[14], RolloutBufs& b)
     b.offsets = (int32_t*)ptr[11];
     b.tile_off = (int32_t*)ptr[12];
     b.tile_info = (int4*)ptr[13];
+    b.actions = (uint8_t*)ptr[14];
 }
 
 // The handle's growable buffers, enlarged as needed (may call hipMalloc).
 static malib_status handle_bufs(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
                                 const RolloutPlan& plan, RolloutBufs& b)
 {
-    size_t sz[14];
+    size_t sz[kNumBufs];
     buffer_sizes(*pop, env, n_envs, plan, sz);
-    DevBuf* db[14] = {&pop->logits, &pop->ret, &pop->state0, &pop->state1, &pop->done,
+    DevBuf* db[kNumBufs] = {&pop->logits, &pop->ret, &pop->state0, &pop->state1, &pop->done,
                       &pop->wt, &pop->obs, &pop->perm, &pop->perm_env, &pop->hist,
-                      &pop->base, &pop->offsets, &pop->tile_off, &pop->tile_info};
-    void* ptr[14];
-    for (int i = 0; i < 14; ++i) {
+                      &pop->base, &pop->offsets, &pop->tile_off, &pop->tile_info,
+                      &pop->actions};
+    void* ptr[kNumBufs];
+    for (int i = 0; i < kNumBufs; ++i) {
         ptr[i] = nullptr;
         if (sz[i]) {
             HIP_TRY(ensure(*db[i], sz[i]));
@@ -822,9 +833,15 @@ static malib_status launch_rollout(malib_pop_t pop, const malib_env_desc* env, i
             HIP_TRY(launch_mlp_bf16_persist(*pop, b.perm, b.perm_env, b.tile_info, b.tile_off,
                                             ns, n_agents, cur, logits, s));
         else
+        {
+            KernelSample ks{b.actions, pop->dev_flags, seed, env_offset, t};
+            // the logits are written only when a trace snapshot reads them
+            float* lg = plan.kernel_sample && !(si >= 0 && trace->logits) ? nullptr : logits;
             HIP_TRY(launch_mlp_bf16(*pop, env->kind, n_agents, env->grid, env->d,
                                     plan.tile_rows, b.perm, b.perm_env, b.tile_info, ns,
-                                    plan.bf16_obs ? (const void*)ea.obs : cur, logits, s));
+                                    plan.bf16_obs ? (const void*)ea.obs : cur, lg,
+                                    plan.kernel_sample ? &ks : nullptr, s));
+        }
         pend(pi);
         if (si >= 0 && trace->logits)
             HIP_TRY(hipMemcpyAsync(trace->logits + (int64_t)si * ns * pop->A, logits,
@@ -837,6 +854,7 @@ static malib_status launch_rollout(malib_pop_t pop, const malib_env_desc* env, i
         sa.t = t;
         sa.log = (trace && trace->actions) ? trace->actions + (int64_t)t * ns : nullptr;
         sa.flags = pop->dev_flags;
+        sa.actions = plan.kernel_sample ? b.actions : nullptr;
         pi = pbeg(MALIB_K_ENV);
         HIP_TRY(launch_env_step(ea, sa, n_envs, cur, nxt, done, ret, pop->dev_frames, s));
         pend(pi);
@@ -941,11 +959,11 @@ malib_status malib_rollout_batch_noalloc(malib_pop_t pop, const malib_env_desc* 
         return fail(MALIB_E_HIP, "the no-allocation scratch has no device address: %s",
                     hipGetErrorString(e));
     }
-    size_t sz[14];
+    size_t sz[kNumBufs];
     buffer_sizes(*pop, env, n_envs, plan, sz);
-    void* ptr[14];
+    void* ptr[kNumBufs];
     size_t off = 0;
-    for (int i = 0; i < 14; ++i) {
+    for (int i = 0; i < kNumBufs; ++i) {
         ptr[i] = nullptr;
         if (sz[i]) {
             ptr[i] = (unsigned char*)pop->scratch + off;

@@ -67,7 +67,7 @@ struct Pop {
     int64_t envs = 0;
     // scratch, grown on demand
     DevBuf perm, perm_env, tile_info, hist, base, offsets, tile_off, logits, ret, state0,
-        state1, obs, wt, done, thresholds;
+        state1, obs, wt, done, thresholds, actions;
     // device address of the library's static no-allocation scratch on this
     // handle's device (resolved at creation; null if that failed)
     void* scratch = nullptr;
@@ -124,6 +124,9 @@ struct SampleArgs {
     int t;
     uint8_t* log;
     int* flags;
+    // FEATURE: the actions the policy kernel already sampled [n_slots] (it
+    // also raised the NaN flag), or null to sample here from the logits
+    const uint8_t* actions = nullptr;
 };
 
 // Trajectory records written by the env-step kernels (all null: none).
@@ -189,10 +192,22 @@ constexpr int kBf16TileRows = 64;
 // measured 29.5 -> 23.7 us against four) for hidden widths >= 128; four below,
 // where eight would leave a wavefront no whole tile.
 constexpr int bf16_tile_threads(int hid) { return hid >= 128 ? 512 : 256; }
+// Gumbel-max sampling done by the 64-row policy kernel itself (feature
+// observations: no env finishes early): the sampled actions [n_slots], the
+// error flags, the Philox key and the counter parts of the step.
+struct KernelSample {
+    uint8_t* actions;
+    int* flags;
+    uint64_t seed;
+    int64_t env_offset;
+    int t;
+};
+// ks: null = only the logits (the env step samples); logits may be null when
+// ks is given and no one reads them.
 hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid, int d,
                            int tile_rows, const int32_t* perm, const int32_t* perm_env,
                            const int4* tile_info, int64_t n_slots, const void* state,
-                           float* logits, hipStream_t s);
+                           float* logits, const KernelSample* ks, hipStream_t s);
 // Feature observations of d = 512 with >= 256 slots per policy on average:
 // persistent kernel over 128-row tiles (one eight-wave workgroup per CU, output
 // layer fed from the layer-2 accumulators).  For narrower observations the

@@ -379,8 +379,9 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     sreg = *reinterpret_cast<const v4f*>(ssrc);
 
     // the actions of the workgroup's slots while the first chunk loads are in
-    // flight: one thread per slot, Gumbel-max over its logits (envs past the
-    // end take action 0 and are never stored)
+    // flight: one thread per slot, Gumbel-max over its logits, or the action
+    // the policy kernel sampled (envs past the end take action 0 and are never
+    // stored)
     __shared__ __attribute__((aligned(8))) uint8_t act_s[kFeatEnvs * kMaxAgents];
     if (tid < kFeatEnvs * ea.n_agents) {
         const int el = tid / ea.n_agents, seat = tid - el * ea.n_agents;
@@ -388,11 +389,15 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
         int a = 0;
         if (e < n) {
             const int64_t slot = e * ea.n_agents + seat;
-            bool nan;
-            a = gumbel_action<kMaxActions>(sa.logits + slot * ea.A, ea.A, sa.seed,
-                                            (uint64_t)(sa.env_offset + e), sa.t, seat, nan);
-            if (nan)
-                atomicOr(sa.flags, kErrNaN);
+            if (sa.actions) {
+                a = sa.actions[slot];   // sampled by the policy kernel
+            } else {
+                bool nan;
+                a = gumbel_action<kMaxActions>(sa.logits + slot * ea.A, ea.A, sa.seed,
+                                                (uint64_t)(sa.env_offset + e), sa.t, seat, nan);
+                if (nan)
+                    atomicOr(sa.flags, kErrNaN);
+            }
             if (sa.log)
                 sa.log[slot] = (uint8_t)a;
             if (ea.tr.act)

@@ -413,6 +413,14 @@ struct MlpBf16Args {
     int n_blocks;                   // launched workgroups (a multiple of 8)
     int max_tiles;                  // entries of tile_info
     const int32_t* tile_off;        // persistent kernel: tile_off[P] = number of tiles
+    // Gumbel-max sampling inside the 64-row kernel (feature observations):
+    // actions [n_slots] (null: the env step samples from the logits), the
+    // Philox key, global env offset and step, and the device error flags
+    uint8_t* actions;
+    int* flags;
+    uint64_t seed;
+    int64_t env_offset;
+    int t;
 };
 
 // Weight fragments of one layer of one policy, read through a buffer resource:
@@ -691,6 +699,58 @@ __device__ __forceinline__ void out_reduce(const float* red, int row, int slot, 
     }
 }
 
+// out_reduce that also samples the row's action (the four threads of a row,
+// lanes 4r..4r+3, share it): z_u = logit_u + g_u with the Gumbel noise g of
+// the row's slot staged in LDS (gz[row][u]), the first index of the largest z
+// wins (each thread scans its own u in order, then the four bests are combined
+// by two shuffles preferring the larger z, on equal z the lower index), as in
+// gumbel_action.  A NaN logit raises kErrNaN and gives action 0.  Every lane
+// takes part in the shuffles; padding rows (slot < 0) write nothing.  Logits
+// are written when `logits` is not null.
+template <int NG, int RTILES, int G4 = 16>
+__device__ __forceinline__ void out_reduce_sample(const float* red, const float* gz, int row,
+                                                  int slot, int u0, int A, const float* b3,
+                                                  float* __restrict__ logits,
+                                                  uint8_t* __restrict__ actions, int* flags)
+{
+    float zbest = -__builtin_inff();
+    int best = -1;
+    bool bad = false;
+    const bool live = slot >= 0;
+    for (int u = u0; u < A; u += 4) {
+        const int lr = (row & 31) + 32 * ((u >> 2) & 1);
+        const int reg = (u >> 3) * 4 + (u & 3);
+        float v = 0.0f;
+#pragma unroll
+        for (int gq = 0; gq < NG; ++gq)
+            v += red[((gq * RTILES + (row >> 5)) * G4 + reg) * 64 + lr];
+        const float l = v + b3[u];
+        if (live && logits)
+            logits[(int64_t)slot * A + u] = l;
+        bad |= __builtin_isnan(l);
+        const float z = l + gz[row * kMaxActions + u];
+        if (best < 0 || z > zbest) {
+            zbest = z;
+            best = u;
+        }
+    }
+#pragma unroll
+    for (int m = 1; m <= 2; m <<= 1) {
+        const float zo = __shfl_xor(zbest, m, 64);
+        const int bo = __shfl_xor(best, m, 64);
+        if (bo >= 0 && (best < 0 || zo > zbest || (zo == zbest && bo < best))) {
+            zbest = zo;
+            best = bo;
+        }
+        bad |= __shfl_xor((int)bad, m, 64) != 0;
+    }
+    if (live && u0 == 0) {
+        actions[slot] = (uint8_t)(bad ? 0 : best);
+        if (bad)
+            atomicOr(flags, kErrNaN);
+    }
+}
+
 // Wavefront grid of a HID-wide layer: WAVES wavefronts over (HID/32 n-tiles) x
 // (RTILES row-tiles of 32); each wave owns NT n-tiles x RT row-tiles.
 template <int HID, int WAVES, int RTILES>
@@ -827,6 +887,10 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     __shared__ __attribute__((aligned(16))) uint16_t buf[BUF];
     __shared__ int row_slot[MR];
     __shared__ int row_env[MR];
+    // Gumbel noise of the rows' slots when the kernel samples the actions
+    // (feature observations), [MR][kMaxActions]
+    constexpr int GZ = OBS == kObsFeature ? MR * kMaxActions : 1;
+    __shared__ float gz[GZ];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -858,6 +922,29 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
         row_env[tid] = tid < nrows ? a.perm_env[r0 + tid] : -1;
     }
     __syncthreads();
+    if constexpr (OBS == kObsFeature) {
+        // the rows' Gumbel noise while the observation rows are fetched: one
+        // thread per (row, Philox block of 8 actions), the same stream and
+        // transform as gumbel_action
+        if (a.actions) {
+            const int nb = (a.A + 7) >> 3;
+            for (int i = tid; i < MR * nb; i += THREADS) {
+                const int row = i / nb, blk = i - row * nb;
+                const int slot = row_slot[row];
+                if (slot >= 0) {
+                    const int env = slot / a.n_agents, seat = slot - env * a.n_agents;
+                    const u64x4 pb = stream_block(a.seed, (uint64_t)(a.env_offset + env),
+                                                  (uint64_t)a.t, kPurposeAction,
+                                                  (uint32_t)seat, (uint64_t)blk);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if (blk * 8 + j < a.A)
+                            gz[row * kMaxActions + blk * 8 + j] =
+                                gumbel01(uniform01(block_lane(pb, j)));
+                }
+            }
+        }
+    }
     build_obs<OBS, KIN, MR, THREADS, LDW>(a, row_slot, row_env, buf, tid);
     __syncthreads();
 
@@ -883,9 +970,18 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     __syncthreads();
     {
         const int row = tid >> 2;
-        out_reduce<S::NGROUPS, RTILES, G4>(red, row,
-                                           row < nrows && row < MR ? row_slot[row] : -1, tid & 3,
-                                           a.A, a.b3 + p * a.A, a.logits);
+        const int slot = row < nrows && row < MR ? row_slot[row] : -1;
+        if constexpr (OBS == kObsFeature) {
+            if (a.actions) {
+                if (row < MR)
+                    out_reduce_sample<S::NGROUPS, RTILES, G4>(red, gz, row, slot, tid & 3, a.A,
+                                                              a.b3 + p * a.A, a.logits,
+                                                              a.actions, a.flags);
+                return;
+            }
+        }
+        out_reduce<S::NGROUPS, RTILES, G4>(red, row, slot, tid & 3, a.A, a.b3 + p * a.A,
+                                           a.logits);
     }
 }
 
@@ -1145,9 +1241,18 @@ static hipError_t launch_hid(const MlpBf16Args& a, int obs, int in_pad, int rows
 hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid, int d,
                            int tile_rows, const int32_t* perm, const int32_t* perm_env,
                            const int4* tile_info, int64_t n_slots, const void* state,
-                           float* logits, hipStream_t s)
+                           float* logits, const KernelSample* ks, hipStream_t s)
 {
-    MlpBf16Args a;
+    MlpBf16Args a = {};
+    if (ks) {
+        if (env_kind != MALIB_ENV_FEATURE)
+            return hipErrorInvalidValue;
+        a.actions = ks->actions;
+        a.flags = ks->flags;
+        a.seed = ks->seed;
+        a.env_offset = ks->env_offset;
+        a.t = ks->t;
+    }
     a.w1 = (const uint4*)pop.w[0];
     a.w2 = (const uint4*)pop.w[1];
     a.w3 = (const uint4*)pop.w[2];
