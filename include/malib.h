@@ -438,6 +438,28 @@ malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32
 /* Message for the last non-OK status returned on this thread. */
 const char* malib_last_error(void);
 
+/* ------------------------------------------------------------- graph mode */
+
+/*
+ * Graph mode of a handle (enable != 0; off at creation).  The paper names the
+ * per-step overheads of its rollout workers (environment resets, data
+ * concatenation, locks) as the main source of throughput noise (Sec. 4.1);
+ * here the per-step cost outside the kernels is one launch per kernel, which
+ * matters for small batches.  In graph mode, malib_rollout_batch and
+ * malib_rollout_batch_traj record the batch's whole launch sequence (set-up,
+ * `horizon` x (policy forward, env step), payoff reduction) into a HIP graph
+ * and replay it with one launch; the handle keeps one executable graph and
+ * updates it in place for the next batch with the same launch structure
+ * (same population, environment kind, sizes and horizon), so repeated batches
+ * pay the instantiation once.  Results are identical to the direct launches.
+ * Calls with a parity trace, calls on a stream that is being captured by the
+ * caller (the launches then join the caller's graph; the handle's host-side
+ * counts of envs and of fixed-length frames count the capture, not the
+ * replays) and malib_rollout_batch_noalloc launch directly.  HIP-event timing
+ * (malib_profile_enable) does not see launches made in graph mode.
+ */
+malib_status malib_pop_set_graph(malib_pop_t pop, int32_t enable);
+
 /* ---------------------------------------------------------------- profiling */
 
 enum {

@@ -27,7 +27,7 @@ EXPORTS = [
     "malib_debug_tanh_ref", "malib_debug_bf16", "malib_debug_philox",
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
     "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate", "malib_rollout_batch_traj",
-    "malib_pop_policy_ids", "malib_rollout_batch_noalloc",
+    "malib_pop_policy_ids", "malib_rollout_batch_noalloc", "malib_pop_set_graph",
 ]
 
 
@@ -119,6 +119,8 @@ def lib():
         L.malib_rollout_batch_noalloc.argtypes = [vp, C.POINTER(EnvDesc), i64, vp, u64, i64,
                                                   i32, vp, vp]
         L.malib_rollout_batch_noalloc.restype = i32
+        L.malib_pop_set_graph.argtypes = [vp, i32]
+        L.malib_pop_set_graph.restype = i32
         L.malib_pop_policy_ids.argtypes = [vp, vp, i32, C.POINTER(i32)]
         L.malib_pop_policy_ids.restype = i32
         _lib = L
@@ -200,6 +202,10 @@ class Population:
         _check(lib().malib_pop_extend(self.handle, C.byref(d), _stream(stream)))
         del keep
         self.P += n_new
+
+    def set_graph(self, enable: bool = True):
+        """malib_pop_set_graph: replay each batch's launch sequence as one HIP graph."""
+        _check(lib().malib_pop_set_graph(self.handle, int(bool(enable))))
 
     def policy_ids(self) -> np.ndarray:
         """malib_pop_policy_ids: the caller id of each index 0 .. P-1."""

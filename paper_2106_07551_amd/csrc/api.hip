@@ -346,6 +346,12 @@ void malib_pop_destroy(malib_pop_t p)
                       &p->ret, &p->state0, &p->state1, &p->obs, &p->wt, &p->done,
                       &p->thresholds, &p->actions})
         release(*b);
+    if (p->graph_exec)
+        (void)hipGraphExecDestroy(p->graph_exec);
+    if (p->graph_done)
+        (void)hipEventDestroy(p->graph_done);
+    if (p->graph_rec)
+        (void)hipStreamDestroy(p->graph_rec);
     for (auto& ev : p->prof.pool) {
         (void)hipEventDestroy(ev.start);
         (void)hipEventDestroy(ev.stop);
@@ -865,8 +871,13 @@ static malib_status launch_rollout(malib_pop_t pop, const malib_env_desc* env, i
 
     // ---- payoff reduction
     pi = pbeg(MALIB_K_PAYOFF);
-    HIP_TRY(launch_payoff(ret, pair_assign, n_envs, n_agents, plan.team, pop->P, pop->sum,
-                          pop->sumsq, pop->cnt, s));
+    if (mlp)
+        HIP_TRY(launch_payoff_bucketed(ret, pair_assign, b.perm, b.offsets, n_envs, n_agents,
+                                       ea.team_row, ea.team_col, pop->P, pop->sum, pop->sumsq,
+                                       pop->cnt, s));
+    else
+        HIP_TRY(launch_payoff(ret, pair_assign, n_envs, n_agents, plan.team, pop->P, pop->sum,
+                              pop->sumsq, pop->cnt, s));
     pend(pi);
     if (returns)
         HIP_TRY(hipMemcpyAsync(returns, ret, sizeof(float) * ns, hipMemcpyDeviceToDevice, s));
@@ -907,9 +918,61 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
         if (st != MALIB_OK)
             return st;
     }
-    return launch_rollout(pop, env, n_envs, pair_assign, seed, env_offset, horizon, returns,
-                          trace, snap_of.empty() ? nullptr : snap_of.data(), traj, plan, b,
-                          true, (hipStream_t)stream);
+    hipStream_t s = (hipStream_t)stream;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    HIP_TRY(hipStreamIsCapturing(s, &cap));
+    if (!pop->graph_mode || trace || cap != hipStreamCaptureStatusNone)
+        return launch_rollout(pop, env, n_envs, pair_assign, seed, env_offset, horizon, returns,
+                              trace, snap_of.empty() ? nullptr : snap_of.data(), traj, plan, b,
+                              true, s);
+    // graph mode: record the batch (no HIP-event timing inside) on the
+    // handle's own stream (recording runs nothing, and the caller's stream may
+    // be the null stream, which cannot be captured), then replay it on the
+    // caller's stream through the handle's executable graph, updated in place
+    // when the batch has the same launch structure as the previous one
+    if (!pop->graph_rec)
+        HIP_TRY(hipStreamCreateWithFlags(&pop->graph_rec, hipStreamNonBlocking));
+    HIP_TRY(hipStreamBeginCapture(pop->graph_rec, hipStreamCaptureModeThreadLocal));
+    const malib_status st = launch_rollout(pop, env, n_envs, pair_assign, seed, env_offset,
+                                           horizon, returns, nullptr, nullptr, traj, plan, b,
+                                           false, pop->graph_rec);
+    hipGraph_t graph = nullptr;
+    const hipError_t ec = hipStreamEndCapture(pop->graph_rec, &graph);
+    if (st != MALIB_OK) {
+        if (graph)
+            (void)hipGraphDestroy(graph);
+        return st;
+    }
+    HIP_TRY(ec);
+    bool updated = false;
+    if (pop->graph_exec) {
+        // an update rewrites the executable graph's kernel arguments: the
+        // previous replay must have finished reading them
+        if (pop->graph_done)
+            HIP_TRY(hipEventSynchronize(pop->graph_done));
+        hipGraphNode_t err_node = nullptr;
+        hipGraphExecUpdateResult res;
+        updated = hipGraphExecUpdate(pop->graph_exec, graph, &err_node, &res) == hipSuccess &&
+                  res == hipGraphExecUpdateSuccess;
+        if (!updated) {
+            (void)hipGetLastError();
+            (void)hipGraphExecDestroy(pop->graph_exec);
+            pop->graph_exec = nullptr;
+        }
+    }
+    hipError_t e = hipSuccess;
+    if (!updated)
+        e = hipGraphInstantiate(&pop->graph_exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (e != hipSuccess) {
+        pop->graph_exec = nullptr;
+        return fail(MALIB_E_HIP, "hipGraphInstantiate failed: %s", hipGetErrorString(e));
+    }
+    HIP_TRY(hipGraphLaunch(pop->graph_exec, s));
+    if (!pop->graph_done)
+        HIP_TRY(hipEventCreateWithFlags(&pop->graph_done, hipEventDisableTiming));
+    HIP_TRY(hipEventRecord(pop->graph_done, s));
+    return MALIB_OK;
 }
 
 malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env, int64_t n_envs,
@@ -1174,6 +1237,14 @@ malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32
 }
 
 // ---------------------------------------------------------------- profiling
+
+malib_status malib_pop_set_graph(malib_pop_t pop, int32_t enable)
+{
+    if (!pop)
+        return fail(MALIB_E_INVAL, "pop is NULL");
+    pop->graph_mode = enable != 0;
+    return MALIB_OK;
+}
 
 malib_status malib_profile_enable(malib_pop_t pop, int32_t mask, int32_t every)
 {

@@ -72,6 +72,13 @@ struct Pop {
     // handle's device (resolved at creation; null if that failed)
     void* scratch = nullptr;
     Profile prof;
+    // graph mode: malib_rollout_batch records each batch's launch sequence
+    // into a HIP graph and replays it through one executable graph, updated
+    // in place for the next batch of the same shape
+    int graph_mode = 0;
+    hipGraphExec_t graph_exec = nullptr;
+    hipEvent_t graph_done = nullptr;     // recorded after each replay
+    hipStream_t graph_rec = nullptr;     // the (default-priority) stream recorded on
 };
 
 // Bucketing of slots by policy id (stable counting sort) + tile table:
@@ -167,10 +174,17 @@ hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_env
 hipError_t launch_snapshot_pursuit(const void* state, const uint8_t* done, int64_t n_envs,
                                    uint8_t* out, hipStream_t s);
 
-// Payoff reduction (once per batch).
+// Payoff reduction (once per batch): per env (global atomics, wave-combined
+// where a wavefront shares a cell), or from the policy bucketing (LDS rows,
+// one set of global atomics per touched cell).
 hipError_t launch_payoff(const float* ret, const int32_t* pids, int64_t n_envs, int n_agents,
                          const int8_t* team, int P, unsigned long long* sum,
                          unsigned long long* sumsq, unsigned long long* cnt, hipStream_t s);
+hipError_t launch_payoff_bucketed(const float* ret, const int32_t* pids, const int32_t* perm,
+                                  const int32_t* offsets, int64_t n_envs, int n_agents,
+                                  uint32_t team_row, uint32_t team_col, int P,
+                                  unsigned long long* sum, unsigned long long* sumsq,
+                                  unsigned long long* cnt, hipStream_t s);
 
 // Policy forwards.
 hipError_t launch_pack_bf16(const float* w, int P, int out, int in, int out_pad, int in_pad,

@@ -698,6 +698,78 @@ __global__ __launch_bounds__(256) void payoff_kernel(
     }
 }
 
+// The same reduction from the slots sorted by policy id (the bucketing of the
+// policy forward): workgroup (p, k) walks part k of row policy p's bucket
+// (gridDim.y parts, so that small populations still fill the GPU); each of
+// its row-side slots adds its env's incidences (p, pid of each column-side
+// seat) into a row of P cells in LDS (64-bit integer LDS atomics: exact and
+// order-independent), and the workgroup then adds each touched cell to the
+// table with one set of global atomics.  Slots whose id is out of range (the
+// bucketing files them under policy 0) are skipped, as above.
+constexpr int kPayoffThreads = 256;
+
+__global__ __launch_bounds__(kPayoffThreads) void payoff_bucketed_kernel(
+    const float* __restrict__ ret, const int32_t* __restrict__ pids,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets, int64_t n,
+    int n_agents, uint32_t team_row, uint32_t team_col, int P,
+    unsigned long long* __restrict__ sum, unsigned long long* __restrict__ sumsq,
+    unsigned long long* __restrict__ cnt)
+{
+    __shared__ unsigned long long s_sum[kMaxP], s_sq[kMaxP];
+    __shared__ unsigned int s_cnt[kMaxP];
+    const int p = blockIdx.x;
+    for (int c = threadIdx.x; c < P; c += kPayoffThreads) {
+        s_sum[c] = 0;
+        s_sq[c] = 0;
+        s_cnt[c] = 0;
+    }
+    __syncthreads();
+    const int b0 = offsets[p], len = offsets[p + 1] - b0;
+    const int r0 = b0 + (int)((int64_t)len * blockIdx.y / gridDim.y);
+    const int r1 = b0 + (int)((int64_t)len * (blockIdx.y + 1) / gridDim.y);
+    for (int r = r0 + threadIdx.x; r < r1; r += kPayoffThreads) {
+        const int slot = perm[r];
+        const int e = slot / n_agents, a = slot - e * n_agents;
+        if (!((team_row >> a) & 1u) || pids[slot] != p)
+            continue;
+        const double g = (double)ret[(int64_t)a * n + e];
+        const long long fx = __double2ll_rn(g * 4294967296.0);
+        const long long fsq = __double2ll_rn(g * g * 1048576.0);
+        for (int b = 0; b < n_agents; ++b) {
+            if (!((team_col >> b) & 1u))
+                continue;
+            const int pb = pids[(int64_t)e * n_agents + b];
+            if (pb < 0 || pb >= P)
+                continue;
+            atomicAdd(&s_sum[pb], (unsigned long long)fx);
+            atomicAdd(&s_sq[pb], (unsigned long long)fsq);
+            atomicAdd(&s_cnt[pb], 1u);
+        }
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < P; c += kPayoffThreads) {
+        const unsigned int k = s_cnt[c];
+        if (k) {
+            const int64_t cell = (int64_t)p * P + c;
+            atomicAdd(&sum[cell], s_sum[c]);
+            atomicAdd(&sumsq[cell], s_sq[c]);
+            atomicAdd(&cnt[cell], (unsigned long long)k);
+        }
+    }
+}
+
+hipError_t launch_payoff_bucketed(const float* ret, const int32_t* pids, const int32_t* perm,
+                                  const int32_t* offsets, int64_t n_envs, int n_agents,
+                                  uint32_t team_row, uint32_t team_col, int P,
+                                  unsigned long long* sum, unsigned long long* sumsq,
+                                  unsigned long long* cnt, hipStream_t s)
+{
+    const int parts = std::max(1, std::min(64, 1024 / P));
+    payoff_bucketed_kernel<<<dim3(P, parts), kPayoffThreads, 0, s>>>(
+        ret, pids, perm, offsets, n_envs, n_agents, team_row, team_col, P, sum, sumsq, cnt);
+    return hipGetLastError();
+}
+
 hipError_t launch_payoff(const float* ret, const int32_t* pids, int64_t n_envs, int n_agents,
                          const int8_t* team, int P, unsigned long long* sum,
                          unsigned long long* sumsq, unsigned long long* cnt, hipStream_t s)

@@ -1,0 +1,157 @@
+"""Graph mode (malib_pop_set_graph) against direct launches.
+
+Two handles built from the same population run the same batches through the C
+ABI, one launching directly, one recording each batch into a HIP graph and
+replaying it.  Three batches in a row on each: the first instantiates the
+executable graph, the second (another seed and env offset, same sizes) updates
+it in place, the third (fewer envs) has another launch structure.  Returns,
+per-step records and the whole table must be equal bit for bit.  A caller's
+own capture (torch.cuda.graph) of a direct-mode batch is replayed several
+times, with eager batches between the replays, and every replay checked
+against the eager result.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from gpu_helpers import say
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _pairs(wl):
+    import oracle
+    if wl.pairs is not None:
+        return wl.pairs
+    return oracle.meta_sample(wl.sigma, wl.P, wl.n_envs, wl.n_agents, wl.seed)
+
+
+def _same_table(ta, tb):
+    assert np.array_equal(ta["counts"], tb["counts"])
+    for k in ("mean", "stderr"):
+        assert np.array_equal(np.isnan(ta[k]), np.isnan(tb[k]))
+        m = ~np.isnan(ta[k])
+        assert np.array_equal(ta[k][m].view(np.uint64), tb[k][m].view(np.uint64)), k
+    assert ta["live_frames"] == tb["live_frames"] and ta["envs"] == tb["envs"]
+    assert ta["status"] == tb["status"] == 0
+
+
+CASES = {
+    "team_full": lambda: W.make(5),                                   # 16384 x 8, d = 256
+    "feature_d512_persistent": lambda: W.make(4, P=4, per_pair=40, horizon=20),
+    "feature_1v1_d256": lambda: W.team_variant(2, P=6, n_envs=600, horizon=12),
+    "pursuit": lambda: W.make(3, n_envs=4000, horizon=60),
+    "iter": lambda: W.make(2, P=8, per_pair=64),
+    "matrix": lambda: W.make(1, per_pair=512),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_graph_mode_matches_direct(name):
+    from paper_2106_07551_amd import workload_io as IO
+    wl = CASES[name]()
+    pairs = _pairs(wl)
+    env = IO.make_env(wl)
+    pa, pb = IO.make_population(wl), IO.make_population(wl)
+    pb.set_graph(True)
+    n1, n2 = wl.n_envs, max(1, wl.n_envs // 3 + 5)
+    for n, seed, offset in ((n1, wl.seed, 0), (n1, wl.seed + 1, 777), (n2, wl.seed, 12345)):
+        say(f"[graph] {name}: n_envs={n} seed={seed} offset={offset}")
+        pt = torch.from_numpy(np.ascontiguousarray(pairs[:n], dtype=np.int32)).cuda()
+        out = []
+        for pop in (pa, pb):
+            ret = torch.empty((wl.n_agents, n), dtype=torch.float32, device="cuda")
+            pop.rollout(env, n, pt, seed, wl.horizon, env_offset=offset, returns=ret)
+            out.append((ret.cpu().numpy(), pop.payoff(reset=True)))
+        (ra, ta), (rb, tb) = out
+        assert np.array_equal(ra.view(np.uint32), rb.view(np.uint32)), name
+        _same_table(ta, tb)
+        assert tb["envs"] == n
+    pa.close()
+    pb.close()
+
+
+def test_graph_mode_trajectory_records():
+    """malib_rollout_batch_traj in graph mode: the same records and table as
+    direct launches, and the ring cursor advanced the same way over two
+    batches (the second wraps the ring)."""
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(3, n_envs=500, horizon=40)
+    env = IO.make_env(wl)
+    pt = torch.from_numpy(np.ascontiguousarray(_pairs(wl), dtype=np.int32)).cuda()
+    cap = wl.n_envs * wl.horizon + 3000
+    res = []
+    for graph in (False, True):
+        pop = IO.make_population(wl)
+        pop.set_graph(graph)
+        tr = M.Traj(cap, wl.n_agents, obs_shape=(2,), obs_dtype=torch.uint8)
+        tabs = []
+        for b in range(2):
+            say(f"[graph] traj graph={graph} batch={b}")
+            pop.rollout_traj(env, wl.n_envs, pt, wl.seed + b, wl.horizon, tr,
+                             env_offset=b * wl.n_envs)
+            tabs.append(pop.payoff(reset=True))
+        torch.cuda.synchronize()
+        res.append((tabs, tr.cursor, {k: getattr(tr, k).cpu().numpy()
+                                      for k in ("actions", "rewards", "flags", "obs")}))
+        pop.close()
+    (ta, ca, ra), (tb, cb, rb) = res
+    assert ca == cb == 2 * wl.n_envs * wl.horizon
+    for x, y in zip(ta, tb):
+        _same_table(x, y)
+    for k in ra:
+        assert np.array_equal(ra[k].view(np.uint8), rb[k].view(np.uint8)), k
+
+
+def test_caller_capture_replays():
+    """A direct-mode batch captured by the caller (torch.cuda.graph) joins
+    that graph: each replay adds one batch to the table, identical to an
+    eager batch, with eager batches and synchronisations between replays."""
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.make(5, n_envs=2048)
+    env = IO.make_env(wl)
+    pt = torch.from_numpy(np.ascontiguousarray(_pairs(wl), dtype=np.int32)).cuda()
+    eager = IO.make_population(wl)
+    ref_ret = torch.empty((wl.n_agents, wl.n_envs), dtype=torch.float32, device="cuda")
+    eager.rollout(env, wl.n_envs, pt, wl.seed, wl.horizon, returns=ref_ret)
+    ref_tab = eager.payoff(reset=True)
+    ref_ret = ref_ret.cpu().numpy()
+
+    pop = IO.make_population(wl)
+    ret = torch.empty((wl.n_agents, wl.n_envs), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        # one eager batch first: the handle's buffers exist before the capture
+        pop.rollout(env, wl.n_envs, pt, wl.seed, wl.horizon, returns=ret, stream=s)
+        pop.payoff(reset=True, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pop.rollout(env, wl.n_envs, pt, wl.seed, wl.horizon, returns=ret)
+    torch.cuda.synchronize()
+    assert pop.payoff(reset=True)["envs"] == wl.n_envs    # host-side count of the capture
+    for rep in range(3):
+        say(f"[graph] caller capture replay {rep}")
+        ret.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(ret.cpu().numpy().view(np.uint32), ref_ret.view(np.uint32))
+        tab = pop.payoff(reset=True)
+        assert np.array_equal(tab["counts"], ref_tab["counts"])
+        m = ~np.isnan(ref_tab["mean"])
+        assert np.array_equal(tab["mean"][m].view(np.uint64), ref_tab["mean"][m].view(np.uint64))
+        # eager work between replays
+        eager.rollout(env, wl.n_envs, pt, wl.seed + rep, wl.horizon)
+        eager.payoff(reset=True)
+    eager.close()
+    pop.close()
