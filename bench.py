@@ -65,8 +65,12 @@ def algorithmic_work(wl):
     n, na, A = wl.n_envs, wl.n_agents, wl.n_actions
     ns = n * na
     out = {}
-    # the env step also samples the actions: the step's logits are read once
-    sample = ns * 4 * A
+    # feature games on the 64-row bf16 kernel sample inside the policy kernel,
+    # which hands the env step one action byte per slot; elsewhere the env
+    # step samples and reads the step's logits once
+    ksample = wl.env_kind == W.FEATURE and wl.pol_kind == W.MLP_BF16 and \
+        policy_kernel(wl) == "mlp_bf16_kernel"
+    sample = ns if ksample else ns * 4 * A
     if wl.env_kind == W.FEATURE:
         d = wl.d
         # state in and out, returns read-modify-write, W and the embedding
@@ -90,10 +94,15 @@ def algorithmic_work(wl):
         obs = 0
         if wl.env_kind == W.FEATURE:
             obs = n * wl.d * (4 if policy_kernel(wl) == "mlp_bf16_persist_kernel" else 2)
-        out["policy"] = {"bytes": wbytes + obs + ns * 4 * A,
+        out["policy"] = {"bytes": wbytes + obs + sample,
                          "flops": policy_flops_per_frame(wl.dims) * ns}
     else:
         out["policy"] = {"bytes": wl.P * A * 4 + ns * 4 * A}
+    # payoff reduction, once per fill: every seat's int32 policy id and each
+    # row-side seat's fp32 return read once, the table's three accumulators
+    # (sum, sum of squares: int64; count: uint32) updated once per cell
+    n_row = int((wl.team > 0).sum())
+    out["payoff"] = {"bytes": ns * 4 + n * n_row * 4 + wl.P * wl.P * 20}
     return out
 
 
@@ -324,13 +333,105 @@ def expansion_timing(M, IO, W, pop, env, wl, fill_ms):
     pop.rollout(env, n_new, pairs, wl.seed, wl.horizon, env_offset=n)
     tab = pop.payoff(reset=True)
     t2 = time.perf_counter()
+    # the same new cells again in graph mode: the first fill records and
+    # instantiates the graph, the second updates it in place (another seed)
+    graph_ms = []
+    pop.set_graph(True)
+    for k in range(2):
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        pop.rollout(env, n_new, pairs, wl.seed + 1 + k, wl.horizon, env_offset=n)
+        pop.payoff(reset=True)
+        graph_ms.append(round(1000.0 * (time.perf_counter() - ta), 3))
+    pop.set_graph(False)
     cells = (P + 1) ** 2 - P * P
     return {"policies": f"{P} -> {P + 1}", "cells": cells, "per_pair": per_pair,
             "envs": n_new, "extend_ms": round(1000.0 * (t1 - t0), 3),
             "fill_ms": round(1000.0 * (t2 - t1), 3),
+            "fill_ms_graph_first": graph_ms[0], "fill_ms_graph_updated": graph_ms[1],
             "agent_frames_per_s": round(tab["live_frames"] / (t2 - t1), 1),
             "full_refill_cells": (P + 1) ** 2,
             "full_fill_ms_at_P": round(fill_ms, 3)}
+
+
+def graph_timing(pop, one_step, steps, direct_ms):
+    """The same fills with the handle in graph mode: each fill's launches
+    (set-up, H x (forward, env step), payoff) recorded into a HIP graph and
+    replayed with one launch; the executable graph is instantiated on the
+    first (untimed) fill and updated in place on the timed ones."""
+    import torch
+    pop.set_graph(True)
+    t0 = time.perf_counter()
+    one_step()
+    first = time.perf_counter() - t0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one_step()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    pop.set_graph(False)
+    ms = 1000.0 * el / steps
+    return {"fill_ms": round(ms, 3), "first_fill_ms": round(1000.0 * first, 3),
+            "direct_fill_ms": round(direct_ms, 3), "speedup": round(direct_ms / ms, 3),
+            "steps": steps}
+
+
+SWEEP_BASE = {"matrix": ("per_pair", 1024), "iter": ("per_pair", 4096),
+              "pursuit": ("n_envs", 16384), "team": ("n_envs", 16384)}
+
+
+def bandwidth_sweep(factors, horizon):
+    """Bandwidth sweep of the streaming kernels: the env step (K2; the
+    4v4 game's K3, which is fp32-ALU-bound, for comparison) and the payoff
+    reduction (K4), with the env count of each workload scaled by each factor
+    and every launch timed with HIP events.  One JSON line per point, labelled
+    "bandwidth_sweep"; not the bench metric."""
+    import torch
+    import workloads as W
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    torch.cuda.set_device(0)
+    for name, (key, base) in SWEEP_BASE.items():
+        c = NAME_TO_C[name]
+        for f in factors:
+            h = 1 if name == "matrix" else horizon
+            wl = W.make(c, horizon=h, **{key: base * f})
+            if wl.n_envs * wl.n_agents > (1 << 26):       # the batch limit of the library
+                print(json.dumps({"bandwidth_sweep": name, "scale": f, "skipped":
+                                  "more than 2^26 slots in one batch"}), flush=True)
+                continue
+            n, na = wl.n_envs, wl.n_agents
+            pop = IO.make_population(wl)
+            env = IO.make_env(wl)
+            if wl.pairs is not None:
+                pairs = IO.make_pairs(wl)
+            else:
+                pairs = torch.empty((n, na), dtype=torch.int32, device="cuda")
+                M.meta_sample(wl.sigma, wl.P, n, na, wl.seed, out=pairs)
+            pop.rollout(env, n, pairs, wl.seed, h)           # warm-up (buffers, caches)
+            pop.payoff(reset=True)
+            pop.profile_enable(True)
+            pop.rollout(env, n, pairs, wl.seed + 1, h)
+            pop.payoff(reset=True)
+            work = algorithmic_work(wl)
+            for kname, k in (("env", M.K_ENV), ("payoff", M.K_PAYOFF)):
+                ms, cnt = pop.profile_read(k)
+                avg_us = 1000.0 * ms / max(cnt, 1)
+                b = work[kname]["bytes"]
+                gbs = b / (avg_us * 1e-6) / 1e9
+                row = {"bandwidth_sweep": name, "kernel": kname, "scale": f, "n_envs": n,
+                       "slots": n * na, "launches": cnt, "avg_us": round(avg_us, 3),
+                       "alg_bytes": b, "GBps": round(gbs, 1),
+                       "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+                if kname == "env" and "flops" in work["env"]:
+                    tf = work["env"]["flops"] / (avg_us * 1e-6) / 1e12
+                    row["fp32_TFLOPs"] = round(tf, 2)
+                    row["alu_frac"] = round(tf / PEAK_F32_ALU_TFLOPS, 4)
+                print(json.dumps(row), flush=True)
+            pop.close()
+            del pairs
+            torch.cuda.empty_cache()
 
 
 def main():
@@ -353,7 +454,14 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the "
                          "reference kernel for scaling HBM byte counters) and exit")
+    ap.add_argument("--sweep", default="", metavar="F1,F2,...",
+                    help="only run the bandwidth sweep of the env step and the payoff "
+                         "reduction at these env-count factors (e.g. 1,8,16,32,64) and exit")
+    ap.add_argument("--sweep-horizon", type=int, default=8)
     args = ap.parse_args()
+    if args.sweep:
+        bandwidth_sweep([int(x) for x in args.sweep.split(",")], args.sweep_horizon)
+        return
     if args.copy_calibration:
         import torch
         nbytes = args.copy_calibration << 20
@@ -445,8 +553,9 @@ def main():
                 kern[name]["fp32_TFLOPs"] = round(w["flops"] / t / 1e12, 2)
                 kern[name]["alu_frac"] = round(w["flops"] / t / 1e12 / PEAK_F32_ALU_TFLOPS, 4)
     pop.profile_enable(False)
-    traj = meta = expand = None
+    traj = meta = expand = graph = None
     if not args.fill_only:
+        graph = graph_timing(pop, one_step, args.steps, 1000.0 * el / args.steps)
         traj = trajectory_timing(M, pop, env, wl, pairs, 1000.0 * el / args.steps)
         meta = meta_update_timing(M, pop, env, wl, pairs, args.fp_iters)
         expand = expansion_timing(M, IO, W, pop, env, wl, 1000.0 * el / args.steps)
@@ -495,6 +604,7 @@ def main():
         "trajectory": traj,
         "meta_update": meta,
         "expansion": expand,
+        "graph_mode": graph,
         "frames_per_step": frames // max(args.steps, 1),
     }
     if not args.no_cpu_baseline:

@@ -871,10 +871,14 @@ static malib_status launch_rollout(malib_pop_t pop, const malib_env_desc* env, i
 
     // ---- payoff reduction
     pi = pbeg(MALIB_K_PAYOFF);
-    if (mlp)
+    if (payoff_stream_fits(pop->P))
+        HIP_TRY(launch_payoff_stream(ret, pair_assign, n_envs, n_agents, ea.team_row,
+                                     ea.team_col, pop->P, pop->n_cus, pop->sum, pop->sumsq,
+                                     pop->cnt, s));
+    else if (mlp)
         HIP_TRY(launch_payoff_bucketed(ret, pair_assign, b.perm, b.offsets, n_envs, n_agents,
-                                       ea.team_row, ea.team_col, pop->P, pop->sum, pop->sumsq,
-                                       pop->cnt, s));
+                                       ea.team_row, ea.team_col, pop->P, pop->n_cus, pop->sum,
+                                       pop->sumsq, pop->cnt, s));
     else
         HIP_TRY(launch_payoff(ret, pair_assign, n_envs, n_agents, plan.team, pop->P, pop->sum,
                               pop->sumsq, pop->cnt, s));

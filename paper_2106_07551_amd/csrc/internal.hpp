@@ -174,15 +174,23 @@ hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_env
 hipError_t launch_snapshot_pursuit(const void* state, const uint8_t* done, int64_t n_envs,
                                    uint8_t* out, hipStream_t s);
 
-// Payoff reduction (once per batch): per env (global atomics, wave-combined
-// where a wavefront shares a cell), or from the policy bucketing (LDS rows,
-// one set of global atomics per touched cell).
+// Payoff reduction (once per batch): for P*P <= kPayoffStreamMaxCells a
+// private LDS copy of the whole table per workgroup over env ranges;
+// otherwise from the policy bucketing (LDS rows, one set of global atomics per
+// touched cell), or per env (global atomics, wave-combined where a wavefront
+// shares a cell) when there is no bucketing (tabular policies).
+constexpr int kPayoffStreamMaxCells = 4096;     // P <= 64: 80 KB of LDS
+bool payoff_stream_fits(int P);
+hipError_t launch_payoff_stream(const float* ret, const int32_t* pids, int64_t n_envs,
+                                int n_agents, uint32_t team_row, uint32_t team_col, int P,
+                                int n_cus, unsigned long long* sum, unsigned long long* sumsq,
+                                unsigned long long* cnt, hipStream_t s);
 hipError_t launch_payoff(const float* ret, const int32_t* pids, int64_t n_envs, int n_agents,
                          const int8_t* team, int P, unsigned long long* sum,
                          unsigned long long* sumsq, unsigned long long* cnt, hipStream_t s);
 hipError_t launch_payoff_bucketed(const float* ret, const int32_t* pids, const int32_t* perm,
                                   const int32_t* offsets, int64_t n_envs, int n_agents,
-                                  uint32_t team_row, uint32_t team_col, int P,
+                                  uint32_t team_row, uint32_t team_col, int P, int n_cus,
                                   unsigned long long* sum, unsigned long long* sumsq,
                                   unsigned long long* cnt, hipStream_t s);
 

@@ -698,75 +698,301 @@ __global__ __launch_bounds__(256) void payoff_kernel(
     }
 }
 
-// The same reduction from the slots sorted by policy id (the bucketing of the
-// policy forward): workgroup (p, k) walks part k of row policy p's bucket
-// (gridDim.y parts, so that small populations still fill the GPU); each of
-// its row-side slots adds its env's incidences (p, pid of each column-side
-// seat) into a row of P cells in LDS (64-bit integer LDS atomics: exact and
-// order-independent), and the workgroup then adds each touched cell to the
-// table with one set of global atomics.  Slots whose id is out of range (the
-// bucketing files them under policy 0) are skipped, as above.
-constexpr int kPayoffThreads = 256;
-
-__global__ __launch_bounds__(kPayoffThreads) void payoff_bucketed_kernel(
-    const float* __restrict__ ret, const int32_t* __restrict__ pids,
-    const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets, int64_t n,
-    int n_agents, uint32_t team_row, uint32_t team_col, int P,
-    unsigned long long* __restrict__ sum, unsigned long long* __restrict__ sumsq,
-    unsigned long long* __restrict__ cnt)
+// Small populations (P*P cells fit one workgroup's LDS): each workgroup walks
+// a contiguous range of envs in env order (coalesced reads of the returns and
+// ids) and reduces every incidence into a private copy of the whole table in
+// LDS: one LDS atomic per incidence, or, where a whole wavefront targets one
+// cell (blocked assignments), a shuffle reduction and one LDS atomic per
+// wavefront.  The workgroup then adds each touched cell to the table with one
+// set of global atomics.  64-bit integer atomics keep the sums exact and
+// independent of the order.
+__device__ __forceinline__ void lds_incidence(unsigned long long* s_sum,
+                                              unsigned long long* s_sq, unsigned int* s_cnt,
+                                              int cell, long long fx, long long fsq)
 {
-    __shared__ unsigned long long s_sum[kMaxP], s_sq[kMaxP];
-    __shared__ unsigned int s_cnt[kMaxP];
-    const int p = blockIdx.x;
-    for (int c = threadIdx.x; c < P; c += kPayoffThreads) {
+    const int c0 = __shfl(cell, 0, 64);
+    if (__ballot(cell != c0) == 0ull) {
+        if (c0 >= 0) {
+            const long long s1 = wave_sum_i64(fx), s2 = wave_sum_i64(fsq);
+            if ((threadIdx.x & 63) == 0) {
+                atomicAdd(&s_sum[c0], (unsigned long long)s1);
+                atomicAdd(&s_sq[c0], (unsigned long long)s2);
+                atomicAdd(&s_cnt[c0], 64u);
+            }
+        }
+    } else if (cell >= 0) {
+        atomicAdd(&s_sum[cell], (unsigned long long)fx);
+        atomicAdd(&s_sq[cell], (unsigned long long)fsq);
+        atomicAdd(&s_cnt[cell], 1u);
+    }
+}
+
+constexpr int kPayoffStreamThreads = 512;
+constexpr int kPayoffStreamBatch = 2;     // envs per thread per iteration (loads in flight)
+
+// The incidences of one env whose seats' returns and ids are in registers.
+template <int NA>
+__device__ __forceinline__ void stream_env(unsigned long long* s_sum, unsigned long long* s_sq,
+                                           unsigned int* s_cnt, const float (&g)[NA],
+                                           const int (&pid)[NA], uint32_t team_row,
+                                           uint32_t team_col, int P)
+{
+#pragma unroll
+    for (int a = 0; a < NA; ++a) {
+        if (!((team_row >> a) & 1u))
+            continue;
+        const double gd = (double)g[a];
+        const long long fx = __double2ll_rn(gd * 4294967296.0);
+        const long long fsq = __double2ll_rn(gd * gd * 1048576.0);
+#pragma unroll
+        for (int b = 0; b < NA; ++b) {
+            if (!((team_col >> b) & 1u))
+                continue;
+            // lanes past the range carry id -1, hence cell -1: a partial
+            // wavefront never takes the shuffle path with them
+            const int cell = (pid[a] >= 0 && pid[a] < P && pid[b] >= 0 && pid[b] < P)
+                                 ? pid[a] * P + pid[b]
+                                 : -1;
+            lds_incidence(s_sum, s_sq, s_cnt, cell, fx, fsq);
+        }
+    }
+}
+
+// NA: seats per env known at compile time (2), or 0 (any count, one env per
+// thread per iteration)
+template <int CELLS, int NA>
+__global__ __launch_bounds__(kPayoffStreamThreads) void payoff_stream_kernel(
+    const float* __restrict__ ret, const int32_t* __restrict__ pids, int64_t n, int n_agents,
+    uint32_t team_row, uint32_t team_col, int P, unsigned long long* __restrict__ sum,
+    unsigned long long* __restrict__ sumsq, unsigned long long* __restrict__ cnt)
+{
+    __shared__ unsigned long long s_sum[CELLS], s_sq[CELLS];
+    __shared__ unsigned int s_cnt[CELLS];
+    const int cells = P * P;
+    for (int c = threadIdx.x; c < cells; c += kPayoffStreamThreads) {
         s_sum[c] = 0;
         s_sq[c] = 0;
         s_cnt[c] = 0;
     }
     __syncthreads();
-    const int b0 = offsets[p], len = offsets[p + 1] - b0;
-    const int r0 = b0 + (int)((int64_t)len * blockIdx.y / gridDim.y);
-    const int r1 = b0 + (int)((int64_t)len * (blockIdx.y + 1) / gridDim.y);
-    for (int r = r0 + threadIdx.x; r < r1; r += kPayoffThreads) {
-        const int slot = perm[r];
-        const int e = slot / n_agents, a = slot - e * n_agents;
-        if (!((team_row >> a) & 1u) || pids[slot] != p)
-            continue;
-        const double g = (double)ret[(int64_t)a * n + e];
-        const long long fx = __double2ll_rn(g * 4294967296.0);
-        const long long fsq = __double2ll_rn(g * g * 1048576.0);
-        for (int b = 0; b < n_agents; ++b) {
-            if (!((team_col >> b) & 1u))
-                continue;
-            const int pb = pids[(int64_t)e * n_agents + b];
-            if (pb < 0 || pb >= P)
-                continue;
-            atomicAdd(&s_sum[pb], (unsigned long long)fx);
-            atomicAdd(&s_sq[pb], (unsigned long long)fsq);
-            atomicAdd(&s_cnt[pb], 1u);
+    const int64_t e0 = n * blockIdx.x / gridDim.x, e1 = n * (blockIdx.x + 1) / gridDim.x;
+    if constexpr (NA > 0) {
+        constexpr int kStep = kPayoffStreamThreads * kPayoffStreamBatch;
+        // the loop bound is uniform over the workgroup (shuffles inside)
+        for (int64_t base = e0; base < e1; base += kStep) {
+            // every seat's return and id of this thread's envs first (all
+            // loads in flight together), then the incidences
+            float g[kPayoffStreamBatch][NA];
+            int pid[kPayoffStreamBatch][NA];
+#pragma unroll
+            for (int k = 0; k < kPayoffStreamBatch; ++k) {
+                const int64_t e = base + k * kPayoffStreamThreads + threadIdx.x;
+                const bool valid = e < e1;
+#pragma unroll
+                for (int a = 0; a < NA; ++a) {
+                    pid[k][a] = valid ? pids[e * NA + a] : -1;
+                    g[k][a] = valid && ((team_row >> a) & 1u) ? ret[(int64_t)a * n + e] : 0.f;
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kPayoffStreamBatch; ++k)
+                stream_env<NA>(s_sum, s_sq, s_cnt, g[k], pid[k], team_row, team_col, P);
+        }
+    } else {
+        for (int64_t base = e0; base < e1; base += kPayoffStreamThreads) {
+            const int64_t e = base + threadIdx.x;
+            const bool valid = e < e1;
+            for (int a = 0; a < n_agents; ++a) {
+                if (!((team_row >> a) & 1u))
+                    continue;
+                long long fx = 0, fsq = 0;
+                int pa = -1;
+                if (valid) {
+                    const double gd = (double)ret[(int64_t)a * n + e];
+                    fx = __double2ll_rn(gd * 4294967296.0);
+                    fsq = __double2ll_rn(gd * gd * 1048576.0);
+                    pa = pids[e * n_agents + a];
+                }
+                for (int b = 0; b < n_agents; ++b) {
+                    if (!((team_col >> b) & 1u))
+                        continue;
+                    const int pb = valid ? pids[e * n_agents + b] : -1;
+                    const int cell =
+                        (pa >= 0 && pa < P && pb >= 0 && pb < P) ? pa * P + pb : -1;
+                    lds_incidence(s_sum, s_sq, s_cnt, cell, fx, fsq);
+                }
+            }
         }
     }
     __syncthreads();
-    for (int c = threadIdx.x; c < P; c += kPayoffThreads) {
+    for (int c = threadIdx.x; c < cells; c += kPayoffStreamThreads) {
         const unsigned int k = s_cnt[c];
         if (k) {
-            const int64_t cell = (int64_t)p * P + c;
-            atomicAdd(&sum[cell], s_sum[c]);
-            atomicAdd(&sumsq[cell], s_sq[c]);
-            atomicAdd(&cnt[cell], (unsigned long long)k);
+            atomicAdd(&sum[c], s_sum[c]);
+            atomicAdd(&sumsq[c], s_sq[c]);
+            atomicAdd(&cnt[c], (unsigned long long)k);
         }
+    }
+}
+
+// Larger populations: from the slots sorted by policy id (the bucketing of
+// the policy forward).  The sorted slot list is cut into equal ranges, one
+// per workgroup, so that a heavily played policy spreads over many
+// workgroups; a range holds one or a few policy segments.  For each segment
+// (row policy p) the row-side slots add their env's incidences (p, id of each
+// column-side seat) into one row of P cells in LDS, which is then added to the
+// table with one set of global atomics per touched cell.  Each thread keeps
+// kPayoffBatch slots' loads in flight.  Slots whose id is out of range (the
+// bucketing files them under policy 0) are skipped.
+constexpr int kPayoffThreads = 256;
+constexpr int kPayoffBatch = 4;
+
+__global__ __launch_bounds__(kPayoffThreads) void payoff_bucketed_kernel(
+    const float* __restrict__ ret, const int32_t* __restrict__ pids,
+    const int32_t* __restrict__ perm, const int32_t* __restrict__ offsets, int64_t n,
+    int n_agents, uint32_t team_row, uint32_t team_col, int P, int64_t rows_per_wg,
+    unsigned long long* __restrict__ sum, unsigned long long* __restrict__ sumsq,
+    unsigned long long* __restrict__ cnt)
+{
+    __shared__ unsigned long long s_sum[kMaxP], s_sq[kMaxP];
+    __shared__ unsigned int s_cnt[kMaxP];
+    __shared__ int s_off[kMaxP + 1];
+    const int64_t ns = n * n_agents;
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_wg;
+    const int64_t r1 = r0 + rows_per_wg < ns ? r0 + rows_per_wg : ns;
+    for (int c = threadIdx.x; c <= P; c += kPayoffThreads)
+        s_off[c] = offsets[c];
+    __syncthreads();
+    // first policy whose segment reaches past r0 (offsets is non-decreasing,
+    // offsets[0] = 0, offsets[P] = ns)
+    int p = 0;
+    {
+        int lo = 0, hi = P - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_off[mid] <= r0)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        p = lo;
+    }
+    for (; p < P && s_off[p] < r1; ++p) {
+        const int64_t s0 = s_off[p] > r0 ? s_off[p] : r0;
+        const int64_t s1 = s_off[p + 1] < r1 ? s_off[p + 1] : r1;
+        if (s0 >= s1)
+            continue;          // uniform over the workgroup
+        for (int c = threadIdx.x; c < P; c += kPayoffThreads) {
+            s_sum[c] = 0;
+            s_sq[c] = 0;
+            s_cnt[c] = 0;
+        }
+        __syncthreads();
+        for (int64_t r = s0 + threadIdx.x; r < s1; r += (int64_t)kPayoffThreads * kPayoffBatch) {
+            int slot[kPayoffBatch], pid[kPayoffBatch];
+            float g[kPayoffBatch];
+#pragma unroll
+            for (int k = 0; k < kPayoffBatch; ++k) {
+                const int64_t rk = r + (int64_t)k * kPayoffThreads;
+                slot[k] = rk < s1 ? perm[rk] : -1;
+            }
+#pragma unroll
+            for (int k = 0; k < kPayoffBatch; ++k) {
+                pid[k] = -1;
+                g[k] = 0.f;
+                if (slot[k] >= 0) {
+                    const int64_t e = slot[k] / n_agents, a = slot[k] - e * n_agents;
+                    if ((team_row >> a) & 1u) {
+                        pid[k] = pids[slot[k]];
+                        g[k] = ret[a * n + e];
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kPayoffBatch; ++k) {
+                if (pid[k] != p)
+                    continue;
+                const int64_t e = slot[k] / n_agents;
+                const double gd = (double)g[k];
+                const long long fx = __double2ll_rn(gd * 4294967296.0);
+                const long long fsq = __double2ll_rn(gd * gd * 1048576.0);
+                for (int b = 0; b < n_agents; ++b) {
+                    if (!((team_col >> b) & 1u))
+                        continue;
+                    const int pb = pids[e * n_agents + b];
+                    if (pb < 0 || pb >= P)
+                        continue;
+                    atomicAdd(&s_sum[pb], (unsigned long long)fx);
+                    atomicAdd(&s_sq[pb], (unsigned long long)fsq);
+                    atomicAdd(&s_cnt[pb], 1u);
+                }
+            }
+        }
+        __syncthreads();
+        for (int c = threadIdx.x; c < P; c += kPayoffThreads) {
+            const unsigned int k = s_cnt[c];
+            if (k) {
+                const int64_t cell = (int64_t)p * P + c;
+                atomicAdd(&sum[cell], s_sum[c]);
+                atomicAdd(&sumsq[cell], s_sq[c]);
+                atomicAdd(&cnt[cell], (unsigned long long)k);
+            }
+        }
+        __syncthreads();       // the row is cleared for the next segment
     }
 }
 
 hipError_t launch_payoff_bucketed(const float* ret, const int32_t* pids, const int32_t* perm,
                                   const int32_t* offsets, int64_t n_envs, int n_agents,
-                                  uint32_t team_row, uint32_t team_col, int P,
+                                  uint32_t team_row, uint32_t team_col, int P, int n_cus,
                                   unsigned long long* sum, unsigned long long* sumsq,
                                   unsigned long long* cnt, hipStream_t s)
 {
-    const int parts = std::max(1, std::min(64, 1024 / P));
-    payoff_bucketed_kernel<<<dim3(P, parts), kPayoffThreads, 0, s>>>(
-        ret, pids, perm, offsets, n_envs, n_agents, team_row, team_col, P, sum, sumsq, cnt);
+    const int64_t ns = n_envs * n_agents;
+    // about four workgroups per CU, at least 256 slots each
+    const int64_t want = std::max<int64_t>(1, std::min<int64_t>(4 * (int64_t)n_cus,
+                                                                (ns + 255) / 256));
+    const int64_t rows = (ns + want - 1) / want;
+    const int grid = (int)((ns + rows - 1) / rows);
+    payoff_bucketed_kernel<<<grid, kPayoffThreads, 0, s>>>(ret, pids, perm, offsets, n_envs,
+                                                           n_agents, team_row, team_col, P,
+                                                           rows, sum, sumsq, cnt);
+    return hipGetLastError();
+}
+
+bool payoff_stream_fits(int P)
+{
+    return P * P <= kPayoffStreamMaxCells;
+}
+
+hipError_t launch_payoff_stream(const float* ret, const int32_t* pids, int64_t n_envs,
+                                int n_agents, uint32_t team_row, uint32_t team_col, int P,
+                                int n_cus, unsigned long long* sum, unsigned long long* sumsq,
+                                unsigned long long* cnt, hipStream_t s)
+{
+    const int cells = P * P;
+    // up to four workgroups per CU (two for the 80 KB table), at least 1024
+    // envs each
+    const int per_cu = cells <= 1024 ? 4 : 2;
+    const int grid = (int)std::max<int64_t>(
+        1, std::min<int64_t>((int64_t)per_cu * n_cus, (n_envs + 1023) / 1024));
+    auto go = [&](auto cells_c) {
+        constexpr int C = decltype(cells_c)::value;
+        if (n_agents == 2)
+            payoff_stream_kernel<C, 2><<<grid, kPayoffStreamThreads, 0, s>>>(
+                ret, pids, n_envs, n_agents, team_row, team_col, P, sum, sumsq, cnt);
+        else
+            payoff_stream_kernel<C, 0><<<grid, kPayoffStreamThreads, 0, s>>>(
+                ret, pids, n_envs, n_agents, team_row, team_col, P, sum, sumsq, cnt);
+    };
+    if (cells <= 256)
+        go(std::integral_constant<int, 256>{});
+    else if (cells <= 1024)
+        go(std::integral_constant<int, 1024>{});
+    else if (cells <= kPayoffStreamMaxCells)
+        go(std::integral_constant<int, kPayoffStreamMaxCells>{});
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
