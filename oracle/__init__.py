@@ -295,6 +295,68 @@ def payoff_matrix(mean):
     return np.where(np.isnan(mean), 0.0, mean)
 
 
+# ---------------------------------------------------------------- alpha-rank
+#
+# The alpha-rank meta-solver that the paper names beside fictitious play and
+# the LP solver for PSRO (Sec. 4.2, Table 3), as defined by its authors
+# (Omidshafiei et al., 2019, "alpha-Rank: Multi-Agent Evaluation by
+# Evolution"), single-population form: the P policies form one population
+# (every seat draws from the same pool, Sec. 3.1), and the table's game is
+# made symmetric by letting two policies meet once on each side.
+
+def alpharank_fixation(u, m):
+    """Fixation probability of a mutant whose fitness exceeds the resident's
+    by u / alpha (u = alpha * difference) in a population of m (Fermi/Moran
+    selection): (1 - e^-u) / (1 - e^-(m u)); 1/m when u = 0.  fp64."""
+    u = float(u)
+    if u == 0.0:
+        return 1.0 / m
+    if u > 0.0:
+        return float(np.expm1(-u) / np.expm1(-m * u))
+    # u < 0: the same ratio with e^((m-1) u) taken out, so that it underflows
+    # gracefully instead of dividing two overflowing terms
+    v = -u
+    return float(np.exp(-(m - 1) * v) * (np.expm1(-v) / np.expm1(-m * v)))
+
+
+def alpharank_chain(M, alpha, m):
+    """Transition matrix C [P][P] (fp64) of the alpha-rank Markov chain on the
+    monomorphic states of the game with row payoff M (the column side gets
+    -M): resident r, mutant s != r meet once on each side, so the mutant's
+    payoff is (M[s][r] - M[r][s]) / 2 and the resident's its negative; the
+    fitness difference is u = alpha (M[s][r] - M[r][s]).  C[r][s] =
+    rho(u) / (P - 1) for s != r (a mutation picks one of the other policies
+    uniformly), C[r][r] = 1 - (sum of the row's other entries)."""
+    M = np.asarray(M, np.float64)
+    P = M.shape[0]
+    C = np.zeros((P, P), np.float64)
+    if P == 1:
+        C[0, 0] = 1.0
+        return C
+    for r in range(P):
+        for s in range(P):
+            if s != r:
+                u = alpha * (float(M[s, r]) - float(M[r, s]))
+                C[r, s] = alpharank_fixation(u, m) / (P - 1)
+        C[r, r] = 1.0 - (C[r].sum() - C[r, r])
+    return C
+
+
+def alpharank(M, alpha, m):
+    """alpha-rank distribution pi [P] (fp64): the stationary distribution of
+    alpharank_chain, pi^T C = pi^T with sum(pi) = 1, solved as the linear
+    system (C^T - I) pi = 0 with the last equation replaced by sum(pi) = 1
+    (unique: for finite alpha every rho is positive, so the chain is
+    irreducible)."""
+    C = alpharank_chain(M, alpha, m)
+    P = C.shape[0]
+    A = C.T - np.eye(P)
+    A[P - 1, :] = 1.0
+    b = np.zeros(P, np.float64)
+    b[P - 1] = 1.0
+    return np.linalg.solve(A, b)
+
+
 # ---------------------------------------------------------------- configuration
 
 class _Cfg:
