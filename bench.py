@@ -277,12 +277,19 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
     gap = torch.empty(1, dtype=torch.float64, device="cuda")
     ids = torch.empty((n, na), dtype=torch.int32, device="cuda")
     agg = torch.empty(5, dtype=torch.float64, device="cuda")
+    pi_ar = torch.empty(P, dtype=torch.float64, device="cuda")
+    sig_ar = torch.empty((2, P), dtype=torch.float32, device="cuda")
+    work_ar = torch.empty((P, P), dtype=torch.float64, device="cuda")
     stages = {
         "payoff_matrix": lambda: pop.payoff_matrix(out=game),
         "solve_fp": lambda: M.solve_fp(game, iters, sigma=sigma, gap=gap),
         "meta_sample_device": lambda: M.meta_sample_device(sigma, P, n, na, wl.seed + 1,
                                                            seat_row=seat_row, out=ids),
         "aggregate": lambda: M.aggregate(game, sigma, P - 1, P - 1, out=agg),
+        # the alternative meta-solver (alpha = 1, population 50), timed alone:
+        # it is not part of the fictitious-play update's total
+        "solve_alpharank": lambda: M.solve_alpharank(game, 1.0, 50, pi=pi_ar, sigma=sig_ar,
+                                                     work=work_ar),
     }
     out = {"fp_iterations": iters, "policies": P, "envs": n}
     for name, fn in stages.items():
@@ -297,7 +304,7 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
         torch.cuda.synchronize()
         out[name + "_us"] = round(1000.0 * e0.elapsed_time(e1) / reps, 2)
     out["solve_fp_ns_per_iteration"] = round(1000.0 * out["solve_fp_us"] / iters, 1)
-    out["total_us"] = round(sum(out[k + "_us"] for k in stages), 2)
+    out["total_us"] = round(sum(out[k + "_us"] for k in stages if k != "solve_alpharank"), 2)
     out["gap"] = float(gap.cpu()[0])
     out["improvement_of_policy_P-1"] = float(agg.cpu()[4])
     pop.payoff(reset=True)

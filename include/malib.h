@@ -394,6 +394,36 @@ malib_status malib_solve_fp(const double* M, int32_t n_policies, int32_t iterati
                             float* sigma, double* gap, void* stream);
 
 /*
+ * alpha-rank on the table (the meta-solver named beside fictitious play and
+ * the LP solver for the PSRO experiments, Sec. 4.2, Table 3), in its authors'
+ * single-population form (Omidshafiei et al., 2019): the P policies are one
+ * population, and two policies meet once on each side of the game (the row
+ * side receives M[i][j], the column side -M[i][j]), so a mutant s in a
+ * population of r has fitness advantage u = alpha (M[s][r] - M[r][s]).  Its
+ * fixation probability in a population of m is rho(u) = (1 - e^-u) /
+ * (1 - e^-(m u)), 1/m at u = 0; a mutation picks one of the other P - 1
+ * policies uniformly, so the chain moves r -> s with probability
+ * rho / (P - 1).  pi is the chain's stationary distribution (unique: every
+ * rho > 0 for finite arguments), computed with the Grassmann-Taksar-Heyman
+ * elimination in fp64 (no subtractions; small probabilities keep their
+ * relative accuracy).
+ *  M:      device fp64 [P][P], finite (e.g. from malib_payoff_matrix).
+ *  alpha:  ranking intensity, finite, >= 0 (0: the uniform distribution).
+ *  m:      population size, 1 .. 10^6.
+ *  work:   device fp64 [P][P] workspace, needed for P > 128 (NULL allowed
+ *          below: the chain then lives in LDS).
+ *  pi:     device fp64 [P] output.
+ *  sigma:  device fp32 [2][P] or NULL: pi in both weight rows, usable
+ *          directly by malib_meta_sample_device.
+ * A fitness gap so large that some rho underflows to 0 can make the chain
+ * reducible; pi is then undefined (NaN or Inf entries).  Asynchronous on
+ * `stream`; one workgroup.
+ */
+malib_status malib_solve_alpharank(const double* M, int32_t n_policies, double alpha,
+                                   int32_t m, double* work, double* pi, float* sigma,
+                                   void* stream);
+
+/*
  * Aggregate payoffs of a meta-strategy pair on a game, for the PSRO
  * convergence judgement of the example API's main loop (Appendix C.2:
  * aggregate(equilibrium) and aggregate(equilibrium, brs), then the

@@ -28,6 +28,7 @@ EXPORTS = [
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
     "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate", "malib_rollout_batch_traj",
     "malib_pop_policy_ids", "malib_rollout_batch_noalloc", "malib_pop_set_graph",
+    "malib_solve_alpharank",
 ]
 
 
@@ -105,6 +106,8 @@ def lib():
         L.malib_payoff_matrix.restype = i32
         L.malib_solve_fp.argtypes = [vp, i32, i32, vp, vp, vp]
         L.malib_solve_fp.restype = i32
+        L.malib_solve_alpharank.argtypes = [vp, i32, C.c_double, i32, vp, vp, vp, vp]
+        L.malib_solve_alpharank.restype = i32
         L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, vp, u64, i64, vp, vp]
         L.malib_meta_sample_device.restype = i32
         L.malib_rollout_batch_traj.argtypes = [vp, C.POINTER(EnvDesc), i64, vp, u64, i64, i32,
@@ -390,6 +393,24 @@ def solve_fp(M, iterations: int, *, sigma=None, gap=None, stream=None):
     _check(lib().malib_solve_fp(_dptr(M), P, iterations, _dptr(sigma), _dptr(gap),
                                 _stream(stream)))
     return sigma, gap
+
+
+def solve_alpharank(M, alpha: float, m: int, *, pi=None, sigma=None, work=None, stream=None):
+    """malib_solve_alpharank on a device fp64 [P][P] game: returns (pi [P]
+    fp64, sigma [2][P] fp32 weight rows), device tensors; a [P][P] fp64
+    workspace is allocated here when P > 128 and none is given."""
+    import torch
+    P = M.shape[0]
+    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
+    if pi is None:
+        pi = torch.empty(P, dtype=torch.float64, device=M.device)
+    if sigma is None:
+        sigma = torch.empty((2, P), dtype=torch.float32, device=M.device)
+    if work is None and P > 128:
+        work = torch.empty((P, P), dtype=torch.float64, device=M.device)
+    _check(lib().malib_solve_alpharank(_dptr(M), P, float(alpha), int(m), _dptr(work),
+                                       _dptr(pi), _dptr(sigma), _stream(stream)))
+    return pi, sigma
 
 
 def aggregate(M, sigma, br_row: int = -1, br_col: int = -1, *, out=None, stream=None):

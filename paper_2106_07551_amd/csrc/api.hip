@@ -14,6 +14,8 @@
 #include "device.hpp"
 #include "internal.hpp"
 
+#include <cmath>
+
 using namespace malib;
 
 struct malib_pop : public Pop {};
@@ -1185,6 +1187,23 @@ malib_status malib_solve_fp(const double* M, int32_t P, int32_t iterations, floa
     if (iterations < 1 || iterations > (1 << 24))
         return fail(MALIB_E_INVAL, "iterations must be in [1, 2^24]");
     HIP_TRY(launch_solve_fp(M, P, iterations, sigma, gap, (hipStream_t)stream));
+    return MALIB_OK;
+}
+
+malib_status malib_solve_alpharank(const double* M, int32_t P, double alpha, int32_t m,
+                                   double* work, double* pi, float* sigma, void* stream)
+{
+    if (!M || !pi)
+        return fail(MALIB_E_INVAL, "M and pi must not be NULL");
+    if (P < 1 || P > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
+    if (!(alpha >= 0.0) || !std::isfinite(alpha))
+        return fail(MALIB_E_INVAL, "alpha must be finite and >= 0");
+    if (m < 1 || m > 1000000)
+        return fail(MALIB_E_INVAL, "population size m must be in [1, 10^6]");
+    if (alpharank_needs_work(P) && !work)
+        return fail(MALIB_E_INVAL, "n_policies > 128 needs a [P][P] fp64 workspace");
+    HIP_TRY(launch_alpharank(M, P, alpha, m, work, pi, sigma, (hipStream_t)stream));
     return MALIB_OK;
 }
 

@@ -98,6 +98,10 @@ inline int max_tiles_for(int64_t n_slots, int P, int tile_rows)
 // weights (k_solve.hip).
 hipError_t launch_payoff_matrix(const unsigned long long* sum, const unsigned long long* cnt,
                                 int P, double* M, hipStream_t s);
+// alpha-rank: one workgroup; P > 128 needs a [P][P] fp64 workspace.
+bool alpharank_needs_work(int P);
+hipError_t launch_alpharank(const double* M, int P, double alpha, int m, double* work,
+                            double* pi, float* sigma, hipStream_t s);
 hipError_t launch_solve_fp(const double* M, int P, int T, float* sigma, double* gap,
                            hipStream_t s);
 hipError_t launch_thresholds(const float* sigma, int n_sigma, int P, unsigned long long* thr,

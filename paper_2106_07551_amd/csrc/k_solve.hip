@@ -322,6 +322,130 @@ hipError_t launch_aggregate(const double* M, int P, const float* sigma, int br_r
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ alpha-rank
+//
+// Single-population alpha-rank (Omidshafiei et al., 2019; the meta-solver the
+// paper lists beside fictitious play for PSRO, Sec. 4.2, Table 3) on the
+// table's game made symmetric by a meeting on each side: a mutant s in a
+// population of r has fitness advantage u = alpha (M[s][r] - M[r][s]); its
+// fixation probability in a population of m is rho(u) = (1 - e^-u) /
+// (1 - e^-mu) (1/m at u = 0), and the chain moves r -> s with probability
+// rho / (P - 1).  The stationary distribution comes from the
+// Grassmann-Taksar-Heyman elimination, which uses only the off-diagonal
+// transition probabilities and never subtracts, so small probabilities keep
+// their relative accuracy: for n = P-1 .. 1, S = sum_{j<n} A[n][j],
+// A[i][n] /= S and A[i][j] += A[i][n] A[n][j] for i, j < n; then pi_0 = 1,
+// pi_j = sum_{i<j} pi_i A[i][j], normalized.  One workgroup of 1024 threads;
+// the matrix in LDS for P <= kArLdsMax, else in the caller's workspace.
+
+constexpr int kArThreads = 1024;
+constexpr int kArLdsMax = 128;
+
+__device__ __forceinline__ double ar_fixation(double u, int m)
+{
+    if (u == 0.0)
+        return 1.0 / m;
+    if (u > 0.0)
+        return expm1(-u) / expm1(-m * u);
+    // u < 0: e^((m-1) u) taken out, so that the ratio underflows gracefully
+    const double v = -u;
+    return exp(-(m - 1) * v) * (expm1(-v) / expm1(-m * v));
+}
+
+// Sum of one value per thread over the workgroup (fixed shuffle/LDS order).
+__device__ __forceinline__ double ar_block_sum(double v, double* red)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v += __shfl_xor(v, off, 64);
+    __syncthreads();        // red is reused
+    if (lane == 0)
+        red[wave] = v;
+    __syncthreads();
+    double t = 0.0;
+#pragma unroll
+    for (int w = 0; w < kArThreads / 64; ++w)
+        t += red[w];
+    return t;
+}
+
+template <bool IN_LDS>
+__global__ __launch_bounds__(kArThreads) void alpharank_kernel(const double* __restrict__ M,
+                                                               int P, double alpha, int m,
+                                                               double* __restrict__ work,
+                                                               double* __restrict__ pi,
+                                                               float* __restrict__ sigma)
+{
+    __shared__ double lds[IN_LDS ? kArLdsMax * (kArLdsMax + 1) : 1];
+    __shared__ double red[kArThreads / 64];
+    __shared__ double s_pi[kMaxP];
+    double* A = IN_LDS ? lds : work;
+    const int ld = IN_LDS ? P + 1 : P;      // odd stride in LDS: column reads spread over banks
+    const int tid = threadIdx.x;
+    // ---- the chain's off-diagonal transition probabilities
+    const double mut = P > 1 ? 1.0 / (P - 1) : 0.0;
+    for (int idx = tid; idx < P * P; idx += kArThreads) {
+        const int r = idx / P, c = idx - r * P;
+        double v = 0.0;
+        if (r != c)
+            v = ar_fixation(alpha * (M[(size_t)c * P + r] - M[(size_t)r * P + c]), m) * mut;
+        A[(size_t)r * ld + c] = v;
+    }
+    __syncthreads();
+    // ---- elimination, states P-1 .. 1; thread (ti, tj) of a 32 x 32 grid
+    // updates A[i][j] for i = ti mod 32, j = tj mod 32
+    const int ti = tid >> 5, tj = tid & 31;
+    for (int n = P - 1; n >= 1; --n) {
+        const double S = ar_block_sum(tid < n ? A[(size_t)n * ld + tid] : 0.0, red);
+        for (int i = tid; i < n; i += kArThreads)
+            A[(size_t)i * ld + n] /= S;
+        __syncthreads();
+        for (int i = ti; i < n; i += 32) {
+            const double ain = A[(size_t)i * ld + n];
+            for (int j = tj; j < n; j += 32)
+                A[(size_t)i * ld + j] += ain * A[(size_t)n * ld + j];
+        }
+        __syncthreads();
+    }
+    // ---- back substitution, then normalization
+    if (tid == 0)
+        s_pi[0] = 1.0;
+    __syncthreads();
+    for (int j = 1; j < P; ++j) {
+        const double v = ar_block_sum(tid < j ? s_pi[tid] * A[(size_t)tid * ld + j] : 0.0, red);
+        if (tid == 0)
+            s_pi[j] = v;
+        __syncthreads();
+    }
+    const double total = ar_block_sum(tid < P ? s_pi[tid] : 0.0, red);
+    if (tid < P) {
+        const double x = s_pi[tid] / total;
+        pi[tid] = x;
+        if (sigma) {
+            sigma[tid] = (float)x;
+            sigma[P + tid] = (float)x;
+        }
+    }
+}
+
+bool alpharank_needs_work(int P)
+{
+    return P > kArLdsMax;
+}
+
+hipError_t launch_alpharank(const double* M, int P, double alpha, int m, double* work,
+                            double* pi, float* sigma, hipStream_t s)
+{
+    if (P > kMaxP || P > kArThreads || (P > kArLdsMax && !work))
+        return hipErrorInvalidValue;
+    if (P <= kArLdsMax)
+        alpharank_kernel<true><<<1, kArThreads, 0, s>>>(M, P, alpha, m, nullptr, pi, sigma);
+    else
+        alpharank_kernel<false><<<1, kArThreads, 0, s>>>(M, P, alpha, m, work, pi, sigma);
+    return hipGetLastError();
+}
+
 // Thresholds of meta-sampling from device weights, the same fp64 arithmetic as
 // the host path: T_m = floor(C_m / C_{P-1} * 2^32) from the sequential fp64
 // cumulative sum C of row r, T_{P-1} = 2^32.  A row with a negative or

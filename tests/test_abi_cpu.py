@@ -78,6 +78,16 @@ def test_validation_before_device_work():
     assert L.malib_solve_fp(dev, 4, (1 << 24) + 1, dev, None, None) == B.E_INVAL
     assert L.malib_solve_fp(dev, 257, 10, dev, None, None) == B.E_INVAL
     assert L.malib_solve_fp(None, 4, 10, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(None, 4, 1.0, 10, None, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 4, 1.0, 10, None, None, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 0, 1.0, 10, None, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 257, 1.0, 10, None, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 4, -1.0, 10, None, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 4, float("nan"), 10, None, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 4, float("inf"), 10, None, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 4, 1.0, 0, None, dev, None, None) == B.E_INVAL
+    assert L.malib_solve_alpharank(dev, 200, 1.0, 10, None, dev, None, None) == B.E_INVAL
+    assert b"workspace" in L.malib_last_error()
     assert L.malib_payoff_matrix(None, dev, None) == B.E_INVAL
     assert L.malib_aggregate(dev, 4, dev, 4, 0, dev, None) == B.E_INVAL
     assert L.malib_aggregate(dev, 4, dev, 0, -2, dev, None) == B.E_INVAL
