@@ -887,6 +887,9 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     __shared__ __attribute__((aligned(16))) uint16_t buf[BUF];
     __shared__ int row_slot[MR];
     __shared__ int row_env[MR];
+    // the tile's hidden-layer biases, staged with the rows: the layers start
+    // their accumulators from LDS instead of waiting on fresh global loads
+    __shared__ __attribute__((aligned(16))) float bias[2][HID];
     // Gumbel noise of the rows' slots when the kernel samples the actions
     // (feature observations), [MR][kMaxActions]
     constexpr int GZ = OBS == kObsFeature ? MR * kMaxActions : 1;
@@ -921,6 +924,10 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
         row_slot[tid] = tid < nrows ? a.perm[r0 + tid] : -1;
         row_env[tid] = tid < nrows ? a.perm_env[r0 + tid] : -1;
     }
+    for (int i = tid; i < HID; i += THREADS) {
+        bias[0][i] = a.b1[p * HID + i];
+        bias[1][i] = a.b2[p * HID + i];
+    }
     __syncthreads();
     if constexpr (OBS == kObsFeature) {
         // the rows' Gumbel noise while the observation rows are fetched: one
@@ -951,14 +958,14 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     f32x16 acc[S::NT][S::RT];
     // ---- layer 1: KIN -> HID
     mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W1, KIN / 16, nt0, rt0, buf, lane,
-                                            a.b1 + p * HID, acc);
+                                            bias[0], acc);
     ring_fill(ring, W2, HID / 16, nt0, lane);      // overlaps the epilogue
     __syncthreads();
     hidden_epilogue<S::NT, S::RT, LDW>(acc, nt0, rt0, buf, lane);
     __syncthreads();
     // ---- layer 2: HID -> HID
     mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W2, HID / 16, nt0, rt0, buf, lane,
-                                            a.b2 + p * HID, acc);
+                                            bias[1], acc);
     // ---- layer 3 from the accumulators, partial logits summed through LDS
     uint4 w3[S::NT][2];
     load_w3<S::NT>(w3, frag_src(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16), nt0, lane);
