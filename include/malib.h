@@ -71,12 +71,17 @@ enum {
  *
  * Supported shapes:
  *  - TABULAR: n_layers = 0, tab_logits device fp32 [P][n_actions].
- *  - MLP_F32: n_layers = 3, dims = {24, h, h, 3} with h in {32, 64}: the
- *    iterated matrix game's observation (in = 8 * n_actions) and actions.
- *  - MLP_BF16: n_layers = 3, dims = {in, h, h, A} with 1 <= in <= 512,
- *    h in {64, 128, 256, 512}, A <= 32.  fp32 weights are rounded to bf16
- *    (nearest, ties to even) when the handle is created.
- * 1 <= P <= 256, 1 <= n_actions <= 32.
+ *  - MLP_F32 and MLP_BF16: n_layers = 3, dims = {in, h1, h2, A} with
+ *    1 <= in, h1, h2 <= 1024 and A = n_actions; `in` must be the
+ *    environment's observation width (iterated game 8 * n_actions, pursuit
+ *    75, feature games d).  bf16 populations have their fp32 weights rounded
+ *    to bf16 (nearest, ties to even) when the handle is created.
+ *    Specialized MFMA kernels run fp32 {24, h, h, 3} with h in {32, 64} and
+ *    bf16 {in <= 512, h, h, A} with h in {64, 128, 256, 512}; every other
+ *    shape runs a generic kernel (fp32 fused multiply-add chains over the
+ *    inputs, same arithmetic per element, lower throughput).
+ * 1 <= P <= 256, 1 <= n_actions <= 32.  Widths above 1024 return
+ * MALIB_E_UNSUPPORTED before any device work.
  */
 typedef struct {
     int32_t kind;                 /* MALIB_POLICY_* */

@@ -162,16 +162,19 @@ const char* malib_last_error(void) { return g_last_error; }
 
 // ------------------------------------------------------------------- create
 
-// Validates a population description; on success *in_dim and *hid hold the
-// MLP input and hidden widths (0 for tabular populations).
-static malib_status check_desc(const malib_pop_desc* desc, int* in_dim, int* hid_out)
+// Validates a population description; on success dims = {in, h1, h2, A}
+// (zeros for tabular populations) and *generic tells whether the MLP needs
+// the generic kernel (a shape the specialized kernels do not take).
+static malib_status check_desc(const malib_pop_desc* desc, int (&dims)[4], bool* generic)
 {
     const int P = desc->n_policies, A = desc->n_actions;
     if (P < 1 || P > kMaxP)
         return fail(MALIB_E_INVAL, "n_policies must be in [1, %d], got %d", kMaxP, P);
     if (A < 1 || A > kMaxActions)
         return fail(MALIB_E_INVAL, "n_actions must be in [1, %d], got %d", kMaxActions, A);
-    int in = 0, hid = 0;
+    for (int l = 0; l < 4; ++l)
+        dims[l] = 0;
+    *generic = false;
     if (desc->kind == MALIB_POLICY_TABULAR) {
         if (!desc->tab_logits)
             return fail(MALIB_E_INVAL, "tabular population needs tab_logits");
@@ -184,33 +187,59 @@ static malib_status check_desc(const malib_pop_desc* desc, int* in_dim, int* hid
         for (int l = 0; l < 3; ++l)
             if (!desc->weights[l])
                 return fail(MALIB_E_INVAL, "weights[%d] is NULL", l);
-        in = desc->dims[0];
-        hid = desc->dims[1];
-        if (desc->dims[2] != hid)
-            return fail(MALIB_E_UNSUPPORTED, "hidden layers must have equal width (%d, %d)",
-                        desc->dims[1], desc->dims[2]);
-        if (desc->dims[3] != A)
-            return fail(MALIB_E_INVAL, "dims[3] (%d) must equal n_actions (%d)", desc->dims[3],
-                        A);
-        if (desc->kind == MALIB_POLICY_MLP_F32) {
-            if (!(hid == 32 || hid == 64))
-                return fail(MALIB_E_UNSUPPORTED, "fp32 MLP hidden width must be 32 or 64");
-            if (in != 24 || A != 3)
-                return fail(MALIB_E_UNSUPPORTED,
-                            "fp32 MLP policies take the iterated-game observation (24 inputs, "
-                            "3 actions)");
-        } else {
-            if (!(hid == 64 || hid == 128 || hid == 256 || hid == 512))
-                return fail(MALIB_E_UNSUPPORTED, "bf16 MLP hidden width must be 64/128/256/512");
-            if (in < 1 || in > 512)
-                return fail(MALIB_E_UNSUPPORTED, "bf16 MLP input width must be in [1, 512]");
-        }
+        for (int l = 0; l < 4; ++l)
+            dims[l] = desc->dims[l];
+        if (dims[3] != A)
+            return fail(MALIB_E_INVAL, "dims[3] (%d) must equal n_actions (%d)", dims[3], A);
+        for (int l = 0; l < 3; ++l)
+            if (dims[l] < 1 || dims[l] > kGenericMaxWidth)
+                return fail(MALIB_E_UNSUPPORTED, "MLP widths must be in [1, %d], got dims[%d] = %d",
+                            kGenericMaxWidth, l, dims[l]);
+        const int in = dims[0], h1 = dims[1], h2 = dims[2];
+        bool special;
+        if (desc->kind == MALIB_POLICY_MLP_F32)
+            special = in == 24 && A == 3 && h1 == h2 && (h1 == 32 || h1 == 64);
+        else
+            special = h1 == h2 && (h1 == 64 || h1 == 128 || h1 == 256 || h1 == 512) && in <= 512;
+        *generic = !special;
     } else {
         return fail(MALIB_E_INVAL, "unknown policy kind %d", desc->kind);
     }
-    *in_dim = in;
-    *hid_out = hid;
     return MALIB_OK;
+}
+
+// Bytes of one policy's layer-l weights in the handle's layout.
+static size_t weight_bytes(const Pop& p, int l)
+{
+    const int fi = p.dims[l], fo = p.dims[l + 1];
+    if (p.generic)
+        return (p.kind == MALIB_POLICY_MLP_F32 ? 4 : 2) * (size_t)fo * fi;
+    if (p.kind == MALIB_POLICY_MLP_F32)
+        return sizeof(float) * (size_t)fo * fi;
+    const int ip = l == 0 ? p.in_pad : round_up(fi, 16);
+    const int op = round_up(fo, 32);
+    return (size_t)(op / 32) * (ip / 16) * 64 * 16;
+}
+
+// k policies' fp32 weights of layer l ([k][out][in], device) into the
+// handle's layout at dst: the generic kernel's [k][out][in] (fp32, or bf16
+// bits), or the specialized kernels' packed MFMA operand layouts.
+static hipError_t store_weights(const Pop& p, int l, const float* src, int k, void* dst,
+                                hipStream_t s)
+{
+    const int fi = p.dims[l], fo = p.dims[l + 1];
+    if (p.generic) {
+        const int64_t n = (int64_t)k * fo * fi;
+        if (p.kind == MALIB_POLICY_MLP_F32)
+            return hipMemcpyAsync(dst, src, sizeof(float) * n, hipMemcpyDeviceToDevice, s);
+        return launch_round_bf16(src, n, (uint16_t*)dst, s);
+    }
+    if (p.kind == MALIB_POLICY_MLP_F32)
+        return launch_pack_f32(src, k, l, p.hid, p.A, (float*)dst, s);
+    const int ip = l == 0 ? p.in_pad : round_up(fi, 16);
+    const int op = round_up(fo, 32);
+    // the output layer in the k order of the layer-2 accumulators
+    return launch_pack_bf16(src, k, fo, fi, op, ip, l == 2, dst, s);
 }
 
 // The caller ids of the policies a description adds at indices first ..
@@ -241,12 +270,14 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
         return fail(MALIB_E_INVAL, "desc is NULL");
     hipStream_t s = (hipStream_t)stream;
     const int P = desc->n_policies, A = desc->n_actions;
-    int in = 0, hid = 0;
+    int dims[4];
+    bool generic = false;
     {
-        const malib_status st = check_desc(desc, &in, &hid);
+        const malib_status st = check_desc(desc, dims, &generic);
         if (st != MALIB_OK)
             return st;
     }
+    const int in = dims[0], hid = dims[1];
     std::vector<int64_t> ids;
     {
         const malib_status st = read_ids(desc, 0, {}, ids);
@@ -281,35 +312,25 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
     p->A = A;
     p->in_dim = in;
     p->hid = hid;
+    p->generic = generic;
+    for (int l = 0; l < 4; ++l)
+        p->dims[l] = dims[l];
     if (desc->kind == MALIB_POLICY_TABULAR) {
         TRY(hipMalloc((void**)&p->tab, sizeof(float) * P * A));
         TRY(hipMemcpyAsync(p->tab, desc->tab_logits, sizeof(float) * P * A,
                            hipMemcpyDeviceToDevice, s));
     } else {
-        const int dims[4] = {in, hid, hid, A};
         p->in_pad = round_up(in, 16);
         for (int l = 0; l < 3; ++l) {
-            int fi = dims[l], fo = dims[l + 1];
+            const int fo = dims[l + 1];
             size_t nb = sizeof(float) * (size_t)P * fo;
             TRY(hipMalloc((void**)&p->b[l], nb));
             if (desc->biases && desc->biases[l])
                 TRY(hipMemcpyAsync(p->b[l], desc->biases[l], nb, hipMemcpyDeviceToDevice, s));
             else
                 TRY(hipMemsetAsync(p->b[l], 0, nb, s));
-            if (desc->kind == MALIB_POLICY_MLP_F32) {
-                // repacked into the MFMA operand layouts (same size)
-                size_t wb = sizeof(float) * (size_t)P * fo * fi;
-                TRY(hipMalloc(&p->w[l], wb));
-                TRY(launch_pack_f32((const float*)desc->weights[l], P, l, hid, A,
-                                    (float*)p->w[l], s));
-            } else {
-                int ip = l == 0 ? p->in_pad : round_up(fi, 16);
-                int op = round_up(fo, 32);
-                size_t wb = (size_t)P * (op / 32) * (ip / 16) * 64 * 16;
-                TRY(hipMalloc(&p->w[l], wb));
-                // the output layer in the k order of the layer-2 accumulators
-                TRY(launch_pack_bf16(desc->weights[l], P, fo, fi, op, ip, l == 2, p->w[l], s));
-            }
+            TRY(hipMalloc(&p->w[l], weight_bytes(*p, l) * P));
+            TRY(store_weights(*p, l, desc->weights[l], P, p->w[l], s));
         }
     }
     const size_t PP = (size_t)P * P, acc_bytes = sizeof(unsigned long long) * (3 * PP + 2);
@@ -367,9 +388,10 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
 {
     if (!pop || !add)
         return fail(MALIB_E_INVAL, "pop and add must not be NULL");
-    int in = 0, hid = 0;
+    int dims[4];
+    bool generic = false;
     {
-        const malib_status st = check_desc(add, &in, &hid);
+        const malib_status st = check_desc(add, dims, &generic);
         if (st != MALIB_OK)
             return st;
     }
@@ -379,9 +401,11 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
     if (add->n_actions != pop->A)
         return fail(MALIB_E_INVAL, "n_actions %d differs from the population's (%d)",
                     add->n_actions, pop->A);
-    if (in != pop->in_dim || hid != pop->hid)
-        return fail(MALIB_E_INVAL, "dims (%d, %d) differ from the population's (%d, %d)", in,
-                    hid, pop->in_dim, pop->hid);
+    for (int l = 0; l < 3; ++l)
+        if (dims[l] != pop->dims[l])
+            return fail(MALIB_E_INVAL, "dims {%d, %d, %d} differ from the population's "
+                        "{%d, %d, %d}", dims[0], dims[1], dims[2], pop->dims[0],
+                        pop->dims[1], pop->dims[2]);
     const int P0 = pop->P, k = add->n_policies, P = P0 + k, A = pop->A;
     if (P > kMaxP)
         return fail(MALIB_E_INVAL, "%d + %d policies exceed %d", P0, k, kMaxP);
@@ -433,9 +457,8 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
         TRY(hipMemcpyAsync(tab + (size_t)P0 * A, add->tab_logits, per * k,
                            hipMemcpyDeviceToDevice, s));
     } else {
-        const int dims[4] = {in, hid, hid, A};
         for (int l = 0; l < 3; ++l) {
-            const int fi = dims[l], fo = dims[l + 1];
+            const int fo = dims[l + 1];
             const size_t bper = sizeof(float) * fo;
             TRY(hipMalloc((void**)&b[l], bper * P));
             TRY(hipMemcpyAsync(b[l], pop->b[l], bper * P0, hipMemcpyDeviceToDevice, s));
@@ -444,22 +467,11 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
                                    hipMemcpyDeviceToDevice, s));
             else
                 TRY(hipMemsetAsync(b[l] + (size_t)P0 * fo, 0, bper * k, s));
-            // packed layouts keep each policy's weights contiguous, policy-major
-            if (pop->kind == MALIB_POLICY_MLP_F32) {
-                const size_t wper = sizeof(float) * (size_t)fo * fi;
-                TRY(hipMalloc(&w[l], wper * P));
-                TRY(hipMemcpyAsync(w[l], pop->w[l], wper * P0, hipMemcpyDeviceToDevice, s));
-                TRY(launch_pack_f32((const float*)add->weights[l], k, l, hid, A,
-                                    (float*)((char*)w[l] + wper * P0), s));
-            } else {
-                const int ip = l == 0 ? pop->in_pad : round_up(fi, 16);
-                const int op = round_up(fo, 32);
-                const size_t wper = (size_t)(op / 32) * (ip / 16) * 64 * 16;
-                TRY(hipMalloc(&w[l], wper * P));
-                TRY(hipMemcpyAsync(w[l], pop->w[l], wper * P0, hipMemcpyDeviceToDevice, s));
-                TRY(launch_pack_bf16(add->weights[l], k, fo, fi, op, ip, l == 2,
-                                     (char*)w[l] + wper * P0, s));
-            }
+            // every layout keeps each policy's weights contiguous, policy-major
+            const size_t wper = weight_bytes(*pop, l);
+            TRY(hipMalloc(&w[l], wper * P));
+            TRY(hipMemcpyAsync(w[l], pop->w[l], wper * P0, hipMemcpyDeviceToDevice, s));
+            TRY(store_weights(*pop, l, add->weights[l], k, (char*)w[l] + wper * P0, s));
         }
     }
     const size_t PP = (size_t)P * P, acc_bytes = sizeof(unsigned long long) * (3 * PP + 2);
@@ -654,9 +666,7 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
     case MALIB_ENV_PURSUIT:
         if (n_agents != 2 || env->n_actions != 5 || env->grid < 5 || env->grid > 16)
             return fail(MALIB_E_INVAL, "pursuit: 2 seats, 5 actions, 5 <= grid <= 16");
-        if (pop->kind == MALIB_POLICY_MLP_F32)
-            return fail(MALIB_E_UNSUPPORTED, "pursuit needs bf16 or tabular policies");
-        if (pop->kind == MALIB_POLICY_MLP_BF16 && pop->in_dim != 75)
+        if (pop->kind != MALIB_POLICY_TABULAR && pop->in_dim != 75)
             return fail(MALIB_E_INVAL, "pursuit observation has 75 inputs");
         break;
     case MALIB_ENV_FEATURE:
@@ -664,9 +674,7 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
             return fail(MALIB_E_UNSUPPORTED, "feature dimension must be 64/128/256/512");
         if (!env->W || !env->emb || !env->u)
             return fail(MALIB_E_INVAL, "feature dynamics need W, emb and u");
-        if (pop->kind == MALIB_POLICY_MLP_F32)
-            return fail(MALIB_E_UNSUPPORTED, "feature games need bf16 or tabular policies");
-        if (pop->kind == MALIB_POLICY_MLP_BF16 && pop->in_dim != env->d)
+        if (pop->kind != MALIB_POLICY_TABULAR && pop->in_dim != env->d)
             return fail(MALIB_E_INVAL, "policy input width must equal d");
         break;
     default:
@@ -677,9 +685,10 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
     const int64_t ns = n_envs * n_agents;
     plan.ns = ns;
     plan.mlp = pop->kind != MALIB_POLICY_TABULAR;
-    plan.persist = pop->kind == MALIB_POLICY_MLP_BF16 &&
+    plan.persist = pop->kind == MALIB_POLICY_MLP_BF16 && !pop->generic &&
                    use_persist_kernel(env->kind, pop->in_pad, ns, pop->P);
-    plan.tile_rows = pop->kind == MALIB_POLICY_MLP_BF16
+    plan.tile_rows = pop->generic ? kGenericTileRows
+                     : pop->kind == MALIB_POLICY_MLP_BF16
                          ? (plan.persist ? kPersistRows : kBf16TileRows)
                          : kF32TileRows;
     plan.max_tiles = max_tiles_for(ns, pop->P, plan.tile_rows);
@@ -688,8 +697,8 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
     // bf16 observation rows for the 64-row policy kernel (its gather reads half
     // the bytes); the persistent kernel converts the fp32 state itself, since
     // at d = 512 the extra rows cost the env step more than they save
-    plan.bf16_obs =
-        env->kind == MALIB_ENV_FEATURE && pop->kind == MALIB_POLICY_MLP_BF16 && !plan.persist;
+    plan.bf16_obs = env->kind == MALIB_ENV_FEATURE && pop->kind == MALIB_POLICY_MLP_BF16 &&
+                    !pop->generic && !plan.persist;
     // feature games with the 64-row kernel: Gumbel-max sampling in the policy
     // kernel (its noise is drawn while the observation rows are fetched), so
     // the env step only reads one action byte per slot
@@ -835,6 +844,9 @@ static malib_status launch_rollout(malib_pop_t pop, const malib_env_desc* env, i
         if (pop->kind == MALIB_POLICY_TABULAR)
             HIP_TRY(launch_tabular(pop->tab, pair_assign, ns, pop->A, pop->P, pop->dev_flags,
                                    logits, s));
+        else if (pop->generic)
+            HIP_TRY(launch_mlp_generic(*pop, env->kind, n_agents, env->grid, b.perm, b.perm_env,
+                                       b.tile_info, plan.max_tiles, ns, cur, logits, s));
         else if (pop->kind == MALIB_POLICY_MLP_F32)
             HIP_TRY(launch_mlp_f32(*pop, b.perm, b.tile_info, ns, n_agents, cur, logits, s));
         else if (persist)

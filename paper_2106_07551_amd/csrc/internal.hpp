@@ -44,6 +44,10 @@ struct Pop {
     int A = 0;
     int in_dim = 0, hid = 0;
     int in_pad = 0;               // bf16: input padded to a multiple of 16
+    // generic MLP (shapes the specialized kernels do not take): weights kept
+    // as [P][out][in] (fp32, or bf16 bits), dims = {in, h1, h2, A}
+    bool generic = false;
+    int dims[4] = {0, 0, 0, 0};
     int device = 0;
     int n_cus = 0;                // compute units of the device
     // packed weights
@@ -234,6 +238,15 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
                            int tile_rows, const int32_t* perm, const int32_t* perm_env,
                            const int4* tile_info, int64_t n_slots, const void* state,
                            float* logits, const KernelSample* ks, hipStream_t s);
+// Generic MLP forward (k_policy.hip): tiles of kGenericTileRows rows, widths
+// up to kGenericMaxWidth; logits for the env step to sample.
+constexpr int kGenericTileRows = 8;
+constexpr int kGenericMaxWidth = 1024;
+hipError_t launch_mlp_generic(const Pop& pop, int env_kind, int n_agents, int grid,
+                              const int32_t* perm, const int32_t* perm_env,
+                              const int4* tile_info, int max_tiles, int64_t n_slots,
+                              const void* state, float* logits, hipStream_t s);
+hipError_t launch_round_bf16(const float* w, int64_t n, uint16_t* out, hipStream_t s);
 // Feature observations of d = 512 with >= 256 slots per policy on average:
 // persistent kernel over 128-row tiles (one eight-wave workgroup per CU, output
 // layer fed from the layer-2 accumulators).  For narrower observations the

@@ -992,6 +992,189 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     }
 }
 
+// ------------------------------------------------------------ generic MLP
+
+// Any MLP the specialized kernels do not cover (input and hidden widths up to
+// 1024 each, the two hidden widths free, fp32 policies on every environment):
+// one workgroup per tile of kGenericTileRows rows of one policy; the rows'
+// activations in LDS (fp32 values; bf16-rounded for bf16 policies), each
+// thread forms output units tid, tid + 256, ... for every row with an fp32
+// fused multiply-add chain over the inputs, then adds the bias, applies the
+// hidden ReLU (IEEE maximum with +0: a NaN stays NaN) and, for bf16
+// policies, rounds to bf16 (products of bf16 values are exact in fp32).
+// Weights are kept as given, [P][out][in] (fp32, or bf16 bits rounded to
+// nearest even at creation).  The logits go to the env step, which samples.
+
+constexpr int kGenericThreads = 256;
+
+struct MlpGenericArgs {
+    const void* w[3];
+    const float* b[3];
+    int dims[4];
+    int bf16;
+    const int32_t* perm;
+    const int32_t* perm_env;
+    const int4* tile_info;
+    int max_tiles;
+    int env_kind;
+    const void* state;      // iterated game: uint16 history; pursuit: uint8 [2][n]; feature: fp32 [n][d]
+    int n_agents, grid, A;
+    int64_t n_envs;
+    float* logits;
+};
+
+// Observation element k of seat `seat` of env `env` (the encodings of the
+// other policy kernels, element by element).
+__device__ __forceinline__ float generic_obs(const MlpGenericArgs& a, int env, int seat, int k)
+{
+    if (a.env_kind == MALIB_ENV_FEATURE)
+        return ((const float*)a.state)[(int64_t)env * a.dims[0] + k];
+    if (a.env_kind == MALIB_ENV_PURSUIT) {
+        const uint8_t* pos = (const uint8_t*)a.state;
+        const int G = a.grid, pc = pos[env], ec = pos[a.n_envs + env];
+        const int self = seat == 0 ? pc : ec;
+        const int o = k / 3, c = k - 3 * o;
+        const int dy = o / 5 - 2, dx = o - (o / 5) * 5 - 2;
+        int x = self % G + dx, y = self / G + dy;     // |dx|, |dy| <= 2 < G
+        x += x < 0 ? G : 0;
+        x -= x >= G ? G : 0;
+        y += y < 0 ? G : 0;
+        y -= y >= G ? G : 0;
+        const int cell = y * G + x;
+        if (c == 0)
+            return cell == pc ? 1.0f : 0.0f;
+        if (c == 1)
+            return cell == ec ? 1.0f : 0.0f;
+        return o == 12 ? 1.0f : 0.0f;
+    }
+    const uint16_t* hist = (const uint16_t*)a.state;
+    return iter_obs(hist[env], seat, a.A, k);
+}
+
+__device__ __forceinline__ float bf16_value(float x)
+{
+    return __uint_as_float((uint32_t)bf16_bits(x) << 16);
+}
+
+__device__ __forceinline__ float generic_weight(const MlpGenericArgs& a, int l, int64_t i)
+{
+    if (a.bf16)
+        return __uint_as_float((uint32_t)((const uint16_t*)a.w[l])[i] << 16);
+    return ((const float*)a.w[l])[i];
+}
+
+__global__ __launch_bounds__(kGenericThreads) void mlp_generic_kernel(MlpGenericArgs a)
+{
+    constexpr int R = kGenericTileRows, W = kGenericMaxWidth;
+    __shared__ float xa[R * W];
+    __shared__ float xb[R * W];
+    __shared__ int row_slot[R], row_env[R];
+    const int t = blockIdx.x, tid = threadIdx.x;
+    if (t >= a.max_tiles)
+        return;
+    const int4 ti = a.tile_info[t];
+    const int p = ti.x;
+    if (p < 0)
+        return;
+    if (tid < R) {
+        row_slot[tid] = tid < ti.z ? a.perm[ti.y + tid] : -1;
+        row_env[tid] = tid < ti.z ? a.perm_env[ti.y + tid] : -1;
+    }
+    __syncthreads();
+    const int in0 = a.dims[0];
+    for (int i = tid; i < R * in0; i += kGenericThreads) {
+        const int r = i / in0, k = i - r * in0;
+        const int env = row_env[r];
+        float v = 0.0f;
+        if (env >= 0)
+            v = generic_obs(a, env, row_slot[r] - env * a.n_agents, k);
+        xa[r * W + k] = a.bf16 ? bf16_value(v) : v;
+    }
+    __syncthreads();
+    float* x = xa;
+    float* y = xb;
+    for (int l = 0; l < 3; ++l) {
+        const int in = a.dims[l], out = a.dims[l + 1];
+        const int64_t wbase = (int64_t)p * out * in;
+        for (int o = tid; o < out; o += kGenericThreads) {
+            float acc[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                acc[r] = 0.0f;
+            const int64_t wrow = wbase + (int64_t)o * in;
+            for (int k = 0; k < in; ++k) {
+                const float w = generic_weight(a, l, wrow + k);
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    acc[r] = __builtin_fmaf(w, x[r * W + k], acc[r]);
+            }
+            const float b = a.b[l][(int64_t)p * out + o];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float v = acc[r] + b;
+                if (l < 2) {
+                    v = relu_f32(v);
+                    y[r * W + o] = a.bf16 ? bf16_value(v) : v;
+                } else if (r < ti.z) {
+                    a.logits[(int64_t)row_slot[r] * a.A + o] = v;
+                }
+            }
+        }
+        __syncthreads();
+        float* tmp = x;
+        x = y;
+        y = tmp;
+    }
+}
+
+hipError_t launch_mlp_generic(const Pop& pop, int env_kind, int n_agents, int grid,
+                              const int32_t* perm, const int32_t* perm_env,
+                              const int4* tile_info, int max_tiles, int64_t n_slots,
+                              const void* state, float* logits, hipStream_t s)
+{
+    MlpGenericArgs a = {};
+    for (int l = 0; l < 3; ++l) {
+        a.w[l] = pop.w[l];
+        a.b[l] = pop.b[l];
+    }
+    for (int l = 0; l < 4; ++l) {
+        a.dims[l] = pop.dims[l];
+        if (pop.dims[l] < 1 || pop.dims[l] > kGenericMaxWidth)
+            return hipErrorInvalidValue;
+    }
+    a.bf16 = pop.kind == MALIB_POLICY_MLP_BF16;
+    a.perm = perm;
+    a.perm_env = perm_env;
+    a.tile_info = tile_info;
+    a.max_tiles = max_tiles;
+    a.env_kind = env_kind;
+    a.state = state;
+    a.n_agents = n_agents;
+    a.grid = grid;
+    a.A = pop.A;
+    a.n_envs = n_slots / n_agents;
+    a.logits = logits;
+    mlp_generic_kernel<<<max_tiles, kGenericThreads, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+// fp32 weights -> bf16 bits (round to nearest even), [n] elements.
+__global__ void round_bf16_kernel(const float* __restrict__ w, int64_t n,
+                                  uint16_t* __restrict__ out)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        out[i] = bf16_bits(w[i]);
+}
+
+hipError_t launch_round_bf16(const float* w, int64_t n, uint16_t* out, hipStream_t s)
+{
+    if (n <= 0)
+        return hipSuccess;
+    round_bf16_kernel<<<(int)((n + 255) / 256), 256, 0, s>>>(w, n, out);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------ persistent bf16 MLP
 
 // Feature observations, large batches: one persistent workgroup of eight

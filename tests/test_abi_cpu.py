@@ -48,6 +48,19 @@ def test_validation_before_device_work():
     assert L.malib_pop_create(C.byref(d), None, C.byref(h)) == B.E_INVAL   # no tab_logits
     d.kind, d.n_layers = B.POLICY_MLP_BF16, 2
     assert L.malib_pop_create(C.byref(d), None, C.byref(h)) == B.E_UNSUPPORTED
+    # widths beyond 1024, for either MLP kind (the weight pointers are never read)
+    fake = (C.c_void_p * 3)(16, 16, 16)
+    for kind in (B.POLICY_MLP_F32, B.POLICY_MLP_BF16):
+        for dims in ([24, 1025, 64, 3], [2048, 64, 64, 3], [24, 64, 4096, 3]):
+            dd = (C.c_int32 * 4)(*dims)
+            d.kind, d.n_layers, d.n_actions = kind, 3, 3
+            d.dims = C.cast(dd, type(d.dims))
+            d.weights = C.cast(fake, type(d.weights))
+            assert L.malib_pop_create(C.byref(d), None, C.byref(h)) == B.E_UNSUPPORTED, dims
+            assert b"1024" in L.malib_last_error()
+    dd = (C.c_int32 * 4)(24, 64, 64, 5)        # dims[3] != n_actions
+    d.dims = C.cast(dd, type(d.dims))
+    assert L.malib_pop_create(C.byref(d), None, C.byref(h)) == B.E_INVAL
     assert L.malib_pop_create(None, None, C.byref(h)) == B.E_INVAL
     assert L.malib_rollout_batch(None, None, 1, None, 0, 0, 1, None, None, None) == B.E_INVAL
     assert L.malib_payoff_eval(None, None, 0, None, None, None, None) == B.E_INVAL

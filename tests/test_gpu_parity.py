@@ -418,9 +418,12 @@ def test_host_validation_errors():
     bad = M.Env(M.ENV_FEATURE, 2, 18, team=[1, -1], d=96, W=None, emb=None, u=None)
     with pytest.raises(M.MalibError):
         pop.rollout(bad, wl.n_envs, pairs, wl.seed, 2)
-    with pytest.raises(M.MalibError):
-        M.Population(M.POLICY_MLP_BF16, 2, 18, dims=[512, 500, 500, 18],
+    # widths beyond 1024 are rejected before any device work (the weights
+    # below are never read)
+    with pytest.raises(M.MalibError) as e:
+        M.Population(M.POLICY_MLP_BF16, 2, 18, dims=[512, 2048, 2048, 18],
                      weights=[torch.zeros(1, device="cuda")] * 3)
+    assert e.value.status == M.binding.E_UNSUPPORTED
     pop.close()
 
 

@@ -211,3 +211,19 @@ def random_pairs(P: int, n_envs: int, n_agents: int, variant: int = 0) -> np.nda
     """Uniform i.i.d. policy ids (an input-side assignment for tests)."""
     rng = np.random.default_rng([2106, 7551, 99, variant])
     return rng.integers(0, P, size=(n_envs, n_agents), dtype=np.int64).astype(np.int32)
+
+
+def with_policies(wl: Workload, pol_kind: int, dims, *, variant: int = 0,
+                  bias_var: float = 0.0) -> Workload:
+    """The same game, pairings and seed with another population of wl.P MLP
+    policies of the given kind and dims [in, h1, h2, A] (weights N(0,
+    1/fan_in), bf16 values for bf16 policies; biases N(0, bias_var), zero
+    when bias_var is 0)."""
+    rng = _rng(90 + wl.number, variant)
+    Ws, bs = _mlp(rng, wl.P, list(dims), bf16=pol_kind == MLP_BF16)
+    if bias_var > 0.0:
+        bs = [_normal(rng, bias_var, b.shape) for b in bs]
+    out = dataclasses.replace(wl, pol_kind=pol_kind, dims=list(dims), weights=Ws, biases=bs)
+    out.name = f"{wl.name}-{'f32' if pol_kind == MLP_F32 else 'bf16'}-" + \
+        "x".join(str(x) for x in dims)
+    return out
