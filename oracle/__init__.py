@@ -357,6 +357,48 @@ def alpharank(M, alpha, m):
     return np.linalg.solve(A, b)
 
 
+# ---------------------------------------------------------------- LP solver
+#
+# The LP meta-solver the paper lists beside fictitious play and alpha-rank for
+# PSRO (Sec. 4.2): the exact equilibrium of the two-player zero-sum meta-game
+# (the row side receives M[i][j], the column side -M[i][j]).  By the minimax
+# theorem its value v = max over x of min over j of (x^T M)_j = min over y of
+# max over i of (M y)_i; the row side's optimal x solves
+#   maximize v  subject to  sum_i x_i M[i][j] >= v for every j,
+#                           sum_i x_i = 1,  x >= 0,
+# and the column side's y the mirror problem.  Each is handed to scipy's
+# linprog (HiGHS) as written.
+
+def solve_lp(M):
+    """Value and optimal strategies of the zero-sum game M (P x P, fp64):
+    returns (v, x, y), x and y fp64 [P].  The strategies need not be unique;
+    the value is."""
+    from scipy.optimize import linprog
+    M = np.asarray(M, np.float64)
+    P, Q = M.shape
+    # row side: variables (x_0 .. x_{P-1}, v); minimize -v
+    c = np.zeros(P + 1)
+    c[-1] = -1.0
+    A_ub = np.hstack([-M.T, np.ones((Q, 1))])          # v - (x^T M)_j <= 0
+    b_ub = np.zeros(Q)
+    A_eq = np.zeros((1, P + 1))
+    A_eq[0, :P] = 1.0
+    bounds = [(0, None)] * P + [(None, None)]
+    rx = linprog(c, A_ub=A_ub, b_ub=b_ub, A_eq=A_eq, b_eq=[1.0], bounds=bounds,
+                 method="highs")
+    # column side: variables (y, w); minimize w subject to (M y)_i <= w
+    c2 = np.zeros(Q + 1)
+    c2[-1] = 1.0
+    A2 = np.hstack([M, -np.ones((P, 1))])
+    A2eq = np.zeros((1, Q + 1))
+    A2eq[0, :Q] = 1.0
+    ry = linprog(c2, A_ub=A2, b_ub=np.zeros(P), A_eq=A2eq, b_eq=[1.0],
+                 bounds=[(0, None)] * Q + [(None, None)], method="highs")
+    if rx.status != 0 or ry.status != 0:
+        raise RuntimeError(f"linprog failed: {rx.message} / {ry.message}")
+    return float(-rx.fun), rx.x[:P].copy(), ry.x[:Q].copy()
+
+
 # ---------------------------------------------------------------- configuration
 
 class _Cfg:
