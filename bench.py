@@ -280,6 +280,7 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
     pi_ar = torch.empty(P, dtype=torch.float64, device="cuda")
     sig_ar = torch.empty((2, P), dtype=torch.float32, device="cuda")
     work_ar = torch.empty((P, P), dtype=torch.float64, device="cuda")
+    work_lp = torch.empty((P + 1) * (2 * P + 1), dtype=torch.float64, device="cuda")
     stages = {
         "payoff_matrix": lambda: pop.payoff_matrix(out=game),
         "solve_fp": lambda: M.solve_fp(game, iters, sigma=sigma, gap=gap),
@@ -290,6 +291,8 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
         # it is not part of the fictitious-play update's total
         "solve_alpharank": lambda: M.solve_alpharank(game, 1.0, 50, pi=pi_ar, sigma=sig_ar,
                                                      work=work_ar),
+        # and the LP solver (exact equilibrium), also outside the total
+        "solve_lp": lambda: M.solve_lp(game, work=work_lp),
     }
     out = {"fp_iterations": iters, "policies": P, "envs": n}
     for name, fn in stages.items():
@@ -304,7 +307,8 @@ def meta_update_timing(M, pop, env, wl, pairs, iters, reps=5):
         torch.cuda.synchronize()
         out[name + "_us"] = round(1000.0 * e0.elapsed_time(e1) / reps, 2)
     out["solve_fp_ns_per_iteration"] = round(1000.0 * out["solve_fp_us"] / iters, 1)
-    out["total_us"] = round(sum(out[k + "_us"] for k in stages if k != "solve_alpharank"), 2)
+    out["total_us"] = round(sum(out[k + "_us"] for k in stages
+                                if k not in ("solve_alpharank", "solve_lp")), 2)
     out["gap"] = float(gap.cpu()[0])
     out["improvement_of_policy_P-1"] = float(agg.cpu()[4])
     pop.payoff(reset=True)

@@ -399,6 +399,28 @@ malib_status malib_solve_fp(const double* M, int32_t n_policies, int32_t iterati
                             float* sigma, double* gap, void* stream);
 
 /*
+ * The LP meta-solver (named beside fictitious play and alpha-rank for the
+ * PSRO experiments, Sec. 4.2): the exact equilibrium of the two-player
+ * zero-sum game M (the row side receives M[i][j], the column side -M[i][j]),
+ * its value v = max_x min_j (x^T M)_j = min_y max_i (M y)_i, by the primal
+ * simplex method (Bland's rule, fp64) on the column side's problem after
+ * shifting M to positive entries; the row side's strategy is the dual
+ * solution.  Optimal strategies need not be unique; the value is.
+ *  M:      device fp64 [P][P], finite.
+ *  work:   device fp64 [P+1][2P+1] workspace, needed for P > 96 (NULL
+ *          allowed below: the tableau then lives in LDS).
+ *  value:  device fp64 [1]; x, y: device fp64 [P] (row and column side).
+ *  sigma:  device fp32 [2][P] or NULL: x and y as weight rows for
+ *          malib_meta_sample_device.
+ *  pivots: device int32 [1] or NULL: simplex pivots taken, -1 if the limit
+ *          of 64 P + 256 pivots was reached (value, x and y are then NaN).
+ * Asynchronous on `stream`; one workgroup.
+ */
+malib_status malib_solve_lp(const double* M, int32_t n_policies, double* work, double* value,
+                            double* x, double* y, float* sigma, int32_t* pivots,
+                            void* stream);
+
+/*
  * alpha-rank on the table (the meta-solver named beside fictitious play and
  * the LP solver for the PSRO experiments, Sec. 4.2, Table 3), in its authors'
  * single-population form (Omidshafiei et al., 2019): the P policies are one

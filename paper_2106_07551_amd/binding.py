@@ -28,7 +28,7 @@ EXPORTS = [
     "malib_payoff_matrix", "malib_solve_fp", "malib_meta_sample_device",
     "malib_pop_extend", "malib_expansion_pairs", "malib_aggregate", "malib_rollout_batch_traj",
     "malib_pop_policy_ids", "malib_rollout_batch_noalloc", "malib_pop_set_graph",
-    "malib_solve_alpharank",
+    "malib_solve_alpharank", "malib_solve_lp",
 ]
 
 
@@ -108,6 +108,8 @@ def lib():
         L.malib_solve_fp.restype = i32
         L.malib_solve_alpharank.argtypes = [vp, i32, C.c_double, i32, vp, vp, vp, vp]
         L.malib_solve_alpharank.restype = i32
+        L.malib_solve_lp.argtypes = [vp, i32, vp, vp, vp, vp, vp, vp, vp]
+        L.malib_solve_lp.restype = i32
         L.malib_meta_sample_device.argtypes = [vp, i32, i32, i64, i32, vp, u64, i64, vp, vp]
         L.malib_meta_sample_device.restype = i32
         L.malib_rollout_batch_traj.argtypes = [vp, C.POINTER(EnvDesc), i64, vp, u64, i64, i32,
@@ -393,6 +395,26 @@ def solve_fp(M, iterations: int, *, sigma=None, gap=None, stream=None):
     _check(lib().malib_solve_fp(_dptr(M), P, iterations, _dptr(sigma), _dptr(gap),
                                 _stream(stream)))
     return sigma, gap
+
+
+def solve_lp(M, *, work=None, stream=None):
+    """malib_solve_lp on a device fp64 [P][P] game: returns (value [1] fp64,
+    x [P] fp64, y [P] fp64, sigma [2][P] fp32, pivots [1] int32), device
+    tensors; a workspace is allocated here when P > 96 and none is given."""
+    import torch
+    P = M.shape[0]
+    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
+    dev = M.device
+    value = torch.empty(1, dtype=torch.float64, device=dev)
+    x = torch.empty(P, dtype=torch.float64, device=dev)
+    y = torch.empty(P, dtype=torch.float64, device=dev)
+    sigma = torch.empty((2, P), dtype=torch.float32, device=dev)
+    pivots = torch.empty(1, dtype=torch.int32, device=dev)
+    if work is None and P > 96:
+        work = torch.empty((P + 1) * (2 * P + 1), dtype=torch.float64, device=dev)
+    _check(lib().malib_solve_lp(_dptr(M), P, _dptr(work), _dptr(value), _dptr(x), _dptr(y),
+                                _dptr(sigma), _dptr(pivots), _stream(stream)))
+    return value, x, y, sigma, pivots
 
 
 def solve_alpharank(M, alpha: float, m: int, *, pi=None, sigma=None, work=None, stream=None):

@@ -1219,6 +1219,20 @@ malib_status malib_solve_alpharank(const double* M, int32_t P, double alpha, int
     return MALIB_OK;
 }
 
+malib_status malib_solve_lp(const double* M, int32_t P, double* work, double* value, double* x,
+                            double* y, float* sigma, int32_t* pivots, void* stream)
+{
+    if (!M || !value || !x || !y)
+        return fail(MALIB_E_INVAL, "M, value, x and y must not be NULL");
+    if (P < 1 || P > kMaxP)
+        return fail(MALIB_E_INVAL, "n_policies must be in [1, %d]", kMaxP);
+    if (lp_needs_work(P) && !work)
+        return fail(MALIB_E_INVAL, "n_policies > 96 needs a [P+1][2P+1] fp64 workspace");
+    HIP_TRY(launch_lp(M, P, 64 * P + 256, work, value, x, y, sigma, pivots,
+                      (hipStream_t)stream));
+    return MALIB_OK;
+}
+
 malib_status malib_aggregate(const double* M, int32_t P, const float* sigma, int32_t br_row,
                              int32_t br_col, double* out, void* stream)
 {

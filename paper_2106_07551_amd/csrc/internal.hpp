@@ -102,6 +102,11 @@ inline int max_tiles_for(int64_t n_slots, int P, int tile_rows)
 // weights (k_solve.hip).
 hipError_t launch_payoff_matrix(const unsigned long long* sum, const unsigned long long* cnt,
                                 int P, double* M, hipStream_t s);
+// LP solver (primal simplex, one workgroup); P > 96 needs a [P+1][2P+1] fp64
+// workspace.
+bool lp_needs_work(int P);
+hipError_t launch_lp(const double* M, int P, int max_pivots, double* work, double* value,
+                     double* x, double* y, float* sigma, int* pivots, hipStream_t s);
 // alpha-rank: one workgroup; P > 128 needs a [P][P] fp64 workspace.
 bool alpharank_needs_work(int P);
 hipError_t launch_alpharank(const double* M, int P, double alpha, int m, double* work,

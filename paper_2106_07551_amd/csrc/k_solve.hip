@@ -446,6 +446,211 @@ hipError_t launch_alpharank(const double* M, int P, double alpha, int m, double*
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ LP solver
+//
+// The zero-sum meta-game's exact equilibrium (the LP solver of the PSRO
+// experiments, Sec. 4.2) by the primal simplex method on the column side's
+// problem after a shift that makes every payoff positive: with
+// M' = M - min(M) + 1, maximize sum_j w_j subject to M' w <= 1, w >= 0.  The
+// origin is feasible (slack basis).  At the optimum the column side's
+// strategy is y = w / sum w, the row side's x = u / sum u with u the slack
+// columns' reduced costs (the dual solution), and the value is
+// 1 / sum w + min(M) - 1.  The entering column is the most negative reduced
+// cost (Dantzig); after kLpDegenerate consecutive degenerate pivots (zero
+// ratio) the solver switches to Bland's rule (the lowest entering column, the
+// lowest basic variable among tied ratios), which cannot cycle, until a pivot
+// makes progress again.  One workgroup:
+// the tableau [P+1][2P+1] (fp64) in LDS for P <= kLpLdsMax, else in the
+// caller's workspace; each pivot finds the entering column and the pivot row
+// with block reductions, stages the column and the scaled pivot row in LDS
+// and updates the other rows.
+
+constexpr int kLpThreads = 1024;
+constexpr int kLpLdsMax = 96;
+constexpr double kLpEps = 1e-11;
+constexpr int kLpDegenerate = 8;
+
+__device__ __forceinline__ double lp_block_min(double v, double* red)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v = fmin(v, __shfl_xor(v, off, 64));
+    __syncthreads();
+    if (lane == 0)
+        red[wave] = v;
+    __syncthreads();
+    double t = red[0];
+#pragma unroll
+    for (int w = 1; w < kLpThreads / 64; ++w)
+        t = fmin(t, red[w]);
+    return t;
+}
+
+__device__ __forceinline__ int lp_block_min_int(int v, int* red)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        v = min(v, __shfl_xor(v, off, 64));
+    __syncthreads();
+    if (lane == 0)
+        red[wave] = v;
+    __syncthreads();
+    int t = red[0];
+#pragma unroll
+    for (int w = 1; w < kLpThreads / 64; ++w)
+        t = min(t, red[w]);
+    return t;
+}
+
+template <bool IN_LDS>
+__global__ __launch_bounds__(kLpThreads) void lp_kernel(const double* __restrict__ M, int P,
+                                                        int max_pivots,
+                                                        double* __restrict__ work,
+                                                        double* __restrict__ value,
+                                                        double* __restrict__ x,
+                                                        double* __restrict__ y,
+                                                        float* __restrict__ sigma,
+                                                        int* __restrict__ pivots)
+{
+    constexpr int LDS_N = IN_LDS ? (kLpLdsMax + 1) * (2 * kLpLdsMax + 1) : 1;
+    __shared__ double lds[LDS_N];
+    __shared__ double col[kMaxP + 1];
+    __shared__ double prow[2 * kMaxP + 1];
+    __shared__ int basis[kMaxP];
+    __shared__ double redd[kLpThreads / 64];
+    __shared__ int redi[kLpThreads / 64];
+    const int tid = threadIdx.x;
+    const int W = 2 * P + 1;                 // columns: w (P), slacks (P), right-hand side
+    double* T = IN_LDS ? lds : work;
+    // ---- the shift: min(M)
+    double mn = INFINITY;
+    for (int i = tid; i < P * P; i += kLpThreads)
+        mn = fmin(mn, M[i]);
+    mn = lp_block_min(mn, redd);
+    // ---- the initial tableau (slack basis)
+    for (int idx = tid; idx < (P + 1) * W; idx += kLpThreads) {
+        const int i = idx / W, j = idx - i * W;
+        double v;
+        if (i < P)
+            v = j < P ? M[(size_t)i * P + j] - mn + 1.0 : (j < 2 * P ? (j - P == i ? 1.0 : 0.0)
+                                                                   : 1.0);
+        else
+            v = j < P ? -1.0 : 0.0;
+        T[idx] = v;
+    }
+    if (tid < P)
+        basis[tid] = P + tid;
+    __syncthreads();
+    int it = 0, degenerate = 0;
+    bool done = false;
+    for (; it < max_pivots; ++it) {
+        // entering column: the most negative reduced cost (the lowest column
+        // among equal ones), or under Bland's rule the lowest negative one
+        const bool bland = degenerate >= kLpDegenerate;
+        double best = INFINITY;
+        if (!bland)
+            for (int j = tid; j < 2 * P; j += kLpThreads)
+                best = fmin(best, T[(size_t)P * W + j]);
+        const double dmin = bland ? -INFINITY : lp_block_min(best, redd);
+        int cand = INT_MAX;
+        for (int j = tid; j < 2 * P; j += kLpThreads) {
+            const double c = T[(size_t)P * W + j];
+            if (c < -kLpEps && (bland || c == dmin))
+                cand = min(cand, j);
+        }
+        const int e = lp_block_min_int(cand, redi);
+        if (e == INT_MAX) {
+            done = true;
+            break;
+        }
+        for (int i = tid; i <= P; i += kLpThreads)
+            col[i] = T[(size_t)i * W + e];
+        __syncthreads();
+        // ratio test: the smallest rhs / col over rows with col > 0, then the
+        // lowest basic variable among the rows within rounding of it
+        double ratio = INFINITY;
+        for (int i = tid; i < P; i += kLpThreads)
+            if (col[i] > kLpEps)
+                ratio = T[(size_t)i * W + 2 * P] / col[i];
+        const double rmin = lp_block_min(ratio, redd);
+        if (!(rmin < INFINITY))
+            break;                           // unbounded: not reachable for M' > 0
+        int bcand = INT_MAX;
+        for (int i = tid; i < P; i += kLpThreads)
+            if (col[i] > kLpEps &&
+                T[(size_t)i * W + 2 * P] / col[i] <= rmin + 1e-12 * fmax(1.0, rmin))
+                bcand = min(bcand, basis[i] * 1024 + i);   // P <= 256 < 1024
+        const int rb = lp_block_min_int(bcand, redi);
+        const int r = rb & 1023;
+        degenerate = rmin <= 0.0 ? degenerate + 1 : 0;
+        // scaled pivot row, then every other row
+        const double piv = col[r];
+        for (int j = tid; j < W; j += kLpThreads) {
+            const double v = T[(size_t)r * W + j] / piv;
+            prow[j] = v;
+            T[(size_t)r * W + j] = v;
+        }
+        __syncthreads();
+        for (int idx = tid; idx < (P + 1) * W; idx += kLpThreads) {
+            const int i = idx / W, j = idx - i * W;
+            if (i != r)
+                T[idx] -= col[i] * prow[j];
+        }
+        if (tid == 0)
+            basis[r] = e;
+        __syncthreads();
+    }
+    // ---- read the solution
+    const double total = T[(size_t)P * W + 2 * P];      // sum of w = sum of u
+    const bool ok = done && total > 0.0;
+    for (int j = tid; j < P; j += kLpThreads) {
+        y[j] = 0.0;
+        x[j] = ok ? T[(size_t)P * W + P + j] / total : (double)NAN;
+    }
+    __syncthreads();
+    for (int i = tid; i < P; i += kLpThreads) {
+        if (basis[i] < P)
+            y[basis[i]] = ok ? T[(size_t)i * W + 2 * P] / total : (double)NAN;
+    }
+    __syncthreads();
+    if (!ok)
+        for (int j = tid; j < P; j += kLpThreads)
+            y[j] = (double)NAN;
+    if (sigma) {
+        __syncthreads();
+        for (int j = tid; j < P; j += kLpThreads) {
+            sigma[j] = (float)x[j];
+            sigma[P + j] = (float)y[j];
+        }
+    }
+    if (tid == 0) {
+        *value = ok ? 1.0 / total + mn - 1.0 : (double)NAN;
+        if (pivots)
+            *pivots = done ? it : -1;
+    }
+}
+
+bool lp_needs_work(int P)
+{
+    return P > kLpLdsMax;
+}
+
+hipError_t launch_lp(const double* M, int P, int max_pivots, double* work, double* value,
+                     double* x, double* y, float* sigma, int* pivots, hipStream_t s)
+{
+    if (P > kMaxP || (P > kLpLdsMax && !work))
+        return hipErrorInvalidValue;
+    if (P <= kLpLdsMax)
+        lp_kernel<true><<<1, kLpThreads, 0, s>>>(M, P, max_pivots, nullptr, value, x, y, sigma,
+                                                  pivots);
+    else
+        lp_kernel<false><<<1, kLpThreads, 0, s>>>(M, P, max_pivots, work, value, x, y, sigma,
+                                                   pivots);
+    return hipGetLastError();
+}
+
 // Thresholds of meta-sampling from device weights, the same fp64 arithmetic as
 // the host path: T_m = floor(C_m / C_{P-1} * 2^32) from the sequential fp64
 // cumulative sum C of row r, T_{P-1} = 2^32.  A row with a negative or

@@ -101,6 +101,12 @@ def test_validation_before_device_work():
     assert L.malib_solve_alpharank(dev, 4, 1.0, 0, None, dev, None, None) == B.E_INVAL
     assert L.malib_solve_alpharank(dev, 200, 1.0, 10, None, dev, None, None) == B.E_INVAL
     assert b"workspace" in L.malib_last_error()
+    assert L.malib_solve_lp(None, 4, None, dev, dev, dev, None, None, None) == B.E_INVAL
+    assert L.malib_solve_lp(dev, 4, None, None, dev, dev, None, None, None) == B.E_INVAL
+    assert L.malib_solve_lp(dev, 0, None, dev, dev, dev, None, None, None) == B.E_INVAL
+    assert L.malib_solve_lp(dev, 257, None, dev, dev, dev, None, None, None) == B.E_INVAL
+    assert L.malib_solve_lp(dev, 97, None, dev, dev, dev, None, None, None) == B.E_INVAL
+    assert b"workspace" in L.malib_last_error()
     assert L.malib_payoff_matrix(None, dev, None) == B.E_INVAL
     assert L.malib_aggregate(dev, 4, dev, 4, 0, dev, None) == B.E_INVAL
     assert L.malib_aggregate(dev, 4, dev, 0, -2, dev, None) == B.E_INVAL
