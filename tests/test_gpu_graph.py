@@ -50,6 +50,8 @@ CASES = {
     "pursuit": lambda: W.make(3, n_envs=4000, horizon=60),
     "iter": lambda: W.make(2, P=8, per_pair=64),
     "matrix": lambda: W.make(1, per_pair=512),
+    "iter_generic_f32": lambda: W.with_policies(W.make(2, P=4, per_pair=40, horizon=6),
+                                                W.MLP_F32, [24, 80, 48, 3]),
 }
 
 

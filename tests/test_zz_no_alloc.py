@@ -45,6 +45,8 @@ CASES = {
     "pursuit": lambda: W.make(3, n_envs=4000, horizon=60),
     "iter": lambda: W.make(2, P=8, per_pair=64),
     "matrix": lambda: W.make(1, per_pair=512),
+    "pursuit_generic_bf16": lambda: W.with_policies(W.make(3, P=6, n_envs=700, horizon=20),
+                                                    W.MLP_BF16, [75, 96, 40, 5]),
 }
 
 
