@@ -568,6 +568,7 @@ struct RolloutPlan {
     int64_t ns = 0;               // agent slots
     bool mlp = false, persist = false, bf16_obs = false;
     bool kernel_sample = false;   // the 64-row policy kernel samples the actions
+    bool striped = false;         // tile table in XCD segments (the 64-row kernel)
     int tile_rows = 0, max_tiles = 0, n_chunks = 0;
     int64_t state_bytes = 0;      // one state buffer (FEATURE has two)
 };
@@ -691,7 +692,9 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
                      : pop->kind == MALIB_POLICY_MLP_BF16
                          ? (plan.persist ? kPersistRows : kBf16TileRows)
                          : kF32TileRows;
-    plan.max_tiles = max_tiles_for(ns, pop->P, plan.tile_rows);
+    plan.striped = pop->kind == MALIB_POLICY_MLP_BF16 && !pop->generic && !plan.persist;
+    plan.max_tiles = plan.striped ? striped_entries(ns, pop->P, plan.tile_rows)
+                                  : max_tiles_for(ns, pop->P, plan.tile_rows);
     plan.n_chunks = (int)((ns + kBucketChunk - 1) / kBucketChunk);
     plan.state_bytes = state_bytes_per_env(env->kind, env->d) * n_envs;
     // bf16 observation rows for the 64-row policy kernel (its gather reads half
@@ -814,8 +817,8 @@ static malib_status launch_rollout(malib_pop_t pop, const malib_env_desc* env, i
     HIP_TRY(launch_zero_f32(ret, ns, s));
     if (mlp)
         HIP_TRY(launch_bucket(pair_assign, ns, n_agents, pop->P, plan.tile_rows, plan.max_tiles,
-                              b.hist, b.base, b.perm, b.perm_env, b.offsets, b.tile_off,
-                              b.tile_info, pop->dev_flags, s));
+                              plan.striped, b.hist, b.base, b.perm, b.perm_env, b.offsets,
+                              b.tile_off, b.tile_info, pop->dev_flags, s));
     HIP_TRY(launch_reset(ea, n_envs, seed, env_offset, cur, done, s));
     if (env->kind == MALIB_ENV_FEATURE)
         HIP_TRY(launch_transpose(env->W, b.wt, env->d, s));

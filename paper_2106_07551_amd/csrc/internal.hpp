@@ -87,15 +87,24 @@ struct Pop {
 
 // Bucketing of slots by policy id (stable counting sort) + tile table:
 // perm[r] = slot of sorted row r, perm_env[r] = its env, offsets[P+1] bucket
-// bounds, tile_off[P+1] first tile of each policy, tile_info[t] = (policy,
-// first row, rows) for t < tile_off[P] and (-1, 0, 0) up to max_tiles.
+// bounds, tile_off[P+1] first tile of each policy, tile_info[n_entries]: the
+// tiles (policy, first row, rows) and padding entries (-1, 0, 0).  Plain
+// layout: entry t is tile t (padding from tile_off[P] on); striped layout
+// (n_entries a multiple of 8): 8 equal segments, each holding an equal share
+// of the tiles in order, then padding (see tile_table_kernel).
 hipError_t launch_bucket(const int32_t* pids, int64_t n_slots, int n_agents, int P,
-                         int tile_rows, int max_tiles, int32_t* hist, int32_t* base,
-                         int32_t* perm, int32_t* perm_env, int32_t* offsets, int32_t* tile_off,
-                         int4* tile_info, int* flags, hipStream_t s);
+                         int tile_rows, int n_entries, bool striped, int32_t* hist,
+                         int32_t* base, int32_t* perm, int32_t* perm_env, int32_t* offsets,
+                         int32_t* tile_off, int4* tile_info, int* flags, hipStream_t s);
 inline int max_tiles_for(int64_t n_slots, int P, int tile_rows)
 {
     return (int)((n_slots + tile_rows - 1) / tile_rows + P);
+}
+// Entries of the striped table of the 64-row bf16 kernel: max_tiles_for
+// rounded up to the 8 XCD segments (one workgroup per entry).
+inline int striped_entries(int64_t n_slots, int P, int tile_rows)
+{
+    return (max_tiles_for(n_slots, P, tile_rows) + 7) / 8 * 8;
 }
 
 // Meta-solver: the table as a game, fictitious play, thresholds from device

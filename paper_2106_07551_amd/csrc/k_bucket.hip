@@ -181,17 +181,30 @@ __global__ __launch_bounds__(kBucketThreads) void bucket_scatter_kernel(
     }
 }
 
-// One thread per tile slot: the policy owning tile t (the last policy whose
+// One thread per table entry: the policy owning tile t (the last policy whose
 // first tile is <= t, which skips empty buckets), its first row and row count.
+// Plain layout: entry e holds tile e.  Striped layout (for a kernel whose
+// workgroup b reads entry (b % 8) * (n_entries / 8) + b / 8, so that workgroups
+// on one XCD read one segment): the n_entries (a multiple of 8) form 8 equal
+// segments, segment x holds tiles [x T / 8, (x + 1) T / 8) of the T tiles in
+// order, then padding, so every XCD gets the same number of real tiles.
 __global__ void tile_table_kernel(const int32_t* __restrict__ offsets,
                                   const int32_t* __restrict__ tile_off, int P, int tile_rows,
-                                  int max_tiles, int4* __restrict__ info)
+                                  int n_entries, int striped, int4* __restrict__ info)
 {
-    int t = blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= max_tiles)
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n_entries)
         return;
-    if (t >= tile_off[P]) {
-        info[t] = make_int4(-1, 0, 0, 0);
+    const int T = tile_off[P];
+    int t = e;
+    if (striped) {
+        const int per = n_entries / 8;
+        const int x = e / per, j = e - x * per;
+        const int lo = (int)((int64_t)x * T / 8), hi = (int)((int64_t)(x + 1) * T / 8);
+        t = j < hi - lo ? lo + j : T;
+    }
+    if (t >= T) {
+        info[e] = make_int4(-1, 0, 0, 0);
         return;
     }
     int lo = 0, hi = P - 1;
@@ -204,14 +217,16 @@ __global__ void tile_table_kernel(const int32_t* __restrict__ offsets,
     }
     int r0 = offsets[lo] + (t - tile_off[lo]) * tile_rows;
     int rows = min(tile_rows, offsets[lo + 1] - r0);
-    info[t] = make_int4(lo, r0, rows, 0);
+    info[e] = make_int4(lo, r0, rows, 0);
 }
 
 hipError_t launch_bucket(const int32_t* pids, int64_t n_slots, int n_agents, int P,
-                         int tile_rows, int max_tiles, int32_t* hist, int32_t* base,
-                         int32_t* perm, int32_t* perm_env, int32_t* offsets, int32_t* tile_off,
-                         int4* tile_info, int* flags, hipStream_t s)
+                         int tile_rows, int n_entries, bool striped, int32_t* hist,
+                         int32_t* base, int32_t* perm, int32_t* perm_env, int32_t* offsets,
+                         int32_t* tile_off, int4* tile_info, int* flags, hipStream_t s)
 {
+    if (striped && n_entries % 8 != 0)
+        return hipErrorInvalidValue;
     int n_chunks = (int)((n_slots + kBucketChunk - 1) / kBucketChunk);
     bucket_hist_kernel<<<n_chunks, kBucketThreads, 0, s>>>(pids, n_slots, P, n_chunks, hist,
                                                            flags);
@@ -219,8 +234,9 @@ hipError_t launch_bucket(const int32_t* pids, int64_t n_slots, int n_agents, int
                                           tile_off);
     bucket_scatter_kernel<<<n_chunks, kBucketThreads, 0, s>>>(pids, n_slots, n_agents, P,
                                                               n_chunks, base, perm, perm_env);
-    tile_table_kernel<<<(max_tiles + 255) / 256, 256, 0, s>>>(offsets, tile_off, P, tile_rows,
-                                                             max_tiles, tile_info);
+    tile_table_kernel<<<(n_entries + 255) / 256, 256, 0, s>>>(offsets, tile_off, P, tile_rows,
+                                                             n_entries, striped ? 1 : 0,
+                                                             tile_info);
     return hipGetLastError();
 }
 

@@ -897,8 +897,9 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void ml
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-    // workgroups are dispatched round-robin over the 8 XCDs: give each XCD a
-    // contiguous run of tiles so that a policy's tiles share one L2
+    // workgroups are dispatched round-robin over the 8 XCDs: each XCD reads one
+    // segment of the striped tile table, an equal share of the tiles in order,
+    // so that a policy's tiles share one L2 and the XCDs get equal work
     const int per = a.n_blocks / 8;
     const int t = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
     if (t >= a.max_tiles)
@@ -1463,10 +1464,10 @@ hipError_t launch_mlp_bf16(const Pop& pop, int env_kind, int n_agents, int grid,
     a.n_envs = n_slots / n_agents;
     if (tile_rows != kBf16TileRows)
         return hipErrorInvalidValue;
-    const int max_tiles = max_tiles_for(n_slots, pop.P, tile_rows);
-    int blocks = (max_tiles + 7) / 8 * 8;
+    // one workgroup per entry of the striped tile table (a multiple of 8)
+    const int blocks = striped_entries(n_slots, pop.P, tile_rows);
     a.n_blocks = blocks;
-    a.max_tiles = max_tiles;
+    a.max_tiles = blocks;
     int obs = env_kind == MALIB_ENV_FEATURE ? kObsFeature
               : env_kind == MALIB_ENV_PURSUIT ? kObsPursuit : kObsIter;
     if (pop.A > (obs == kObsFeature ? kMaxActions : 8))
