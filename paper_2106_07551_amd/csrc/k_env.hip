@@ -408,10 +408,16 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
     __syncthreads();
     // the actions of this thread's envs, 8 bits per seat (bytes of seats
     // >= n_agents are never read)
+    // (a wavefront's envs are the same for all its lanes: the action bytes, and
+    // with them the embedding rows' addresses, are kept in scalar registers)
     uint64_t act_pk[EPT];
 #pragma unroll
-    for (int i = 0; i < EPT; ++i)
-        act_pk[i] = *reinterpret_cast<const uint64_t*>(act_s + (ty * EPT + i) * kMaxAgents);
+    for (int i = 0; i < EPT; ++i) {
+        const uint64_t pk =
+            *reinterpret_cast<const uint64_t*>(act_s + (ty * EPT + i) * kMaxAgents);
+        act_pk[i] = (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)pk) |
+                    ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(pk >> 32)) << 32);
+    }
 
     float acc[EPT][NJ];
 #pragma unroll
