@@ -147,8 +147,8 @@ __device__ __forceinline__ float tanh_ref(float x)
     // 1 - 2 / b with b = exp_ref(2|x|) + 1 in [4, 2^26]: 2 / b rounded is
     // twice the rounded reciprocal y of b, obtained from the hardware estimate
     // (1 ulp) by one fused Newton step, and 1 - 2y is formed with one rounding,
-    // as 1 - (2 / b) is.  (Equal to the IEEE quotient over every input: the
-    // exhaustive device test compares all 2^32 inputs with the oracle.)
+    // as 1 - (2 / b) is.  (The result equals that of the IEEE quotient for
+    // every one of the 2^32 fp32 inputs, checked exhaustively on the device.)
     const float b = exp_ref(2.0f * ax) + 1.0f;
     float y = __builtin_amdgcn_rcpf(b);
     y = __builtin_fmaf(__builtin_fmaf(-b, y, 1.0f), y, y);
