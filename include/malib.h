@@ -213,6 +213,12 @@ typedef struct {
  * P x P table: each (row-side seat a, column-side seat b) pair of an env adds
  * the return of seat a to cell (pid[a], pid[b]).
  * Limits: n_envs >= 1, n_envs * n_agents <= 2^26, 1 <= horizon <= 100000.
+ * Device buffers of the batch (logits, state, bucketing tables) are the
+ * handle's, grown with hipMalloc when a batch needs more than earlier ones.
+ * On a stream that the caller is capturing into a HIP graph, a batch that
+ * would grow them returns MALIB_E_INVAL before any device work (run one batch
+ * of that size outside the capture first, or use
+ * malib_rollout_batch_noalloc).
  */
 malib_status malib_rollout_batch(malib_pop_t pop, const malib_env_desc* env,
                                  int64_t n_envs, const int32_t* pair_assign,

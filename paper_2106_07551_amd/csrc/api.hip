@@ -610,7 +610,7 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
                     env->n_actions, pop->A);
     if (n_envs < 1)
         return fail(MALIB_E_INVAL, "n_envs must be >= 1");
-    if (n_envs * n_agents > ((int64_t)1 << 26))
+    if (n_envs > ((int64_t)1 << 26) / n_agents)
         return fail(MALIB_E_INVAL, "n_envs * n_agents exceeds 2^26");
     if (horizon < 1 || horizon > 100000)
         return fail(MALIB_E_INVAL, "horizon must be in [1, 100000]");
@@ -750,6 +750,22 @@ static void assign_bufs(void* const (&ptr)[kNumBufs], RolloutBufs& b)
     b.tile_off = (int32_t*)ptr[12];
     b.tile_info = (int4*)ptr[13];
     b.actions = (uint8_t*)ptr[14];
+}
+
+// Whether the handle's growable buffers already hold the batch.
+static bool handle_bufs_fit(const Pop& pop, const malib_env_desc* env, int64_t n_envs,
+                            const RolloutPlan& plan)
+{
+    size_t sz[kNumBufs];
+    buffer_sizes(pop, env, n_envs, plan, sz);
+    const DevBuf* db[kNumBufs] = {&pop.logits, &pop.ret, &pop.state0, &pop.state1, &pop.done,
+                                  &pop.wt, &pop.obs, &pop.perm, &pop.perm_env, &pop.hist,
+                                  &pop.base, &pop.offsets, &pop.tile_off, &pop.tile_info,
+                                  &pop.actions};
+    for (int i = 0; i < kNumBufs; ++i)
+        if (sz[i] > db[i]->bytes)
+            return false;
+    return true;
 }
 
 // The handle's growable buffers, enlarged as needed (may call hipMalloc).
@@ -933,15 +949,22 @@ static malib_status rollout_impl(malib_pop_t pop, const malib_env_desc* env, int
             snap_of[st] = i;
         }
     }
+    hipStream_t s = (hipStream_t)stream;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    HIP_TRY(hipStreamIsCapturing(s, &cap));
+    // growing a buffer synchronizes the device and frees memory, which a
+    // capture in progress does not allow
+    if (cap != hipStreamCaptureStatusNone && !handle_bufs_fit(*pop, env, n_envs, plan))
+        return fail(MALIB_E_INVAL,
+                    "the stream is being captured and this batch needs larger device buffers "
+                    "than the handle holds: run a batch of this size outside the capture "
+                    "first, or use malib_rollout_batch_noalloc");
     RolloutBufs b;
     {
         const malib_status st = handle_bufs(pop, env, n_envs, plan, b);
         if (st != MALIB_OK)
             return st;
     }
-    hipStream_t s = (hipStream_t)stream;
-    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    HIP_TRY(hipStreamIsCapturing(s, &cap));
     if (!pop->graph_mode || trace || cap != hipStreamCaptureStatusNone)
         return launch_rollout(pop, env, n_envs, pair_assign, seed, env_offset, horizon, returns,
                               trace, snap_of.empty() ? nullptr : snap_of.data(), traj, plan, b,
@@ -1145,7 +1168,7 @@ malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, i
         return fail(MALIB_E_INVAL, "n_agents must be in [1, %d]", kMaxAgents);
     if (n_sigma != 1 && n_sigma != n_agents)
         return fail(MALIB_E_INVAL, "n_sigma must be 1 or n_agents");
-    if (n_envs < 0 || n_envs * n_agents > ((int64_t)1 << 26) || env_offset < 0)
+    if (n_envs < 0 || n_envs > ((int64_t)1 << 26) / n_agents || env_offset < 0)
         return fail(MALIB_E_INVAL, "bad n_envs / env_offset");
     std::vector<unsigned long long> thr((size_t)n_sigma * P);
     for (int r = 0; r < n_sigma; ++r) {
@@ -1275,7 +1298,7 @@ malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32
             return fail(MALIB_E_INVAL, "n_sigma must be 1 or n_agents");
         seat_map = default_seat_map(n_sigma);
     }
-    if (n_envs < 0 || n_envs * n_agents > ((int64_t)1 << 26) || env_offset < 0)
+    if (n_envs < 0 || n_envs > ((int64_t)1 << 26) / n_agents || env_offset < 0)
         return fail(MALIB_E_INVAL, "bad n_envs / env_offset");
     if (n_envs == 0)
         return MALIB_OK;

@@ -73,6 +73,10 @@ def test_validation_before_device_work():
     assert L.malib_meta_sample(sig.ctypes.data, 1, 2, 10, 2, 1, 0, out, None) == B.E_INVAL
     sig = np.array([1.0, 1.0], np.float32)
     assert L.malib_meta_sample(sig.ctypes.data, 3, 2, 10, 2, 1, 0, out, None) == B.E_INVAL
+    # n_envs far past the 2^26-slot limit: rejected, no int64 overflow in the check
+    assert L.malib_meta_sample(sig.ctypes.data, 1, 2, 1 << 62, 8, 1, 0, out, None) == B.E_INVAL
+    assert L.malib_meta_sample_device(C.c_void_p(16), 1, 2, 1 << 62, 8, None, 1, 0, out,
+                                      None) == B.E_INVAL
     assert L.malib_meta_sample(sig.ctypes.data, 1, 2, 10, 9, 1, 0, out, None) == B.E_INVAL
     # device-weight sampling and the solver: argument checks come before any
     # device access (the pointers below are never dereferenced)

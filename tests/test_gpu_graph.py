@@ -157,3 +157,40 @@ def test_caller_capture_replays():
         eager.payoff(reset=True)
     eager.close()
     pop.close()
+
+
+def test_caller_capture_of_a_larger_batch_is_refused():
+    """Under the caller's capture, a batch that would grow the handle's device
+    buffers (growing synchronizes the device and frees memory, which a capture
+    does not allow) is refused with MALIB_E_INVAL before any device work: the
+    capture stays valid and ends cleanly, and the same batch runs afterwards
+    outside the capture."""
+    from paper_2106_07551_amd import workload_io as IO
+    from paper_2106_07551_amd import binding as B
+    small, big = W.make(5, n_envs=256, horizon=4), W.make(5, n_envs=1024, horizon=4)
+    env = IO.make_env(small)
+    p_small = torch.from_numpy(np.ascontiguousarray(_pairs(small), dtype=np.int32)).cuda()
+    p_big = torch.from_numpy(np.ascontiguousarray(_pairs(big), dtype=np.int32)).cuda()
+    pop = IO.make_population(small)
+    pop.rollout(env, small.n_envs, p_small, small.seed, small.horizon)   # buffers for 256 envs
+    pop.payoff(reset=True)
+    torch.cuda.synchronize()
+    x = torch.zeros(16, device="cuda")
+    g = torch.cuda.CUDAGraph()
+    err = None
+    with torch.cuda.graph(g):
+        x.add_(1.0)                        # the capture holds one node of its own
+        try:
+            pop.rollout(env, big.n_envs, p_big, big.seed, big.horizon)
+        except B.MalibError as e:
+            err = e
+    torch.cuda.synchronize()
+    assert err is not None and err.status == B.E_INVAL, err
+    assert "captured" in str(err)
+    g.replay()
+    torch.cuda.synchronize()
+    assert float(x[0]) == 1.0              # the capture ended valid; nothing of the batch in it
+    pop.rollout(env, big.n_envs, p_big, big.seed, big.horizon)
+    tab = pop.payoff(reset=True)
+    assert tab["envs"] == big.n_envs and tab["status"] == 0
+    pop.close()
