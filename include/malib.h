@@ -412,7 +412,8 @@ malib_status malib_solve_fp(const double* M, int32_t n_policies, int32_t iterati
  * simplex method (Bland's rule, fp64) on the column side's problem after
  * shifting M to positive entries; the row side's strategy is the dual
  * solution.  Optimal strategies need not be unique; the value is.
- *  M:      device fp64 [P][P], finite.
+ *  M:      device fp64 [P][P], finite (a NaN or infinite entry gives NaN
+ *          value, x, y and sigma, and pivots = -1).
  *  work:   device fp64 [P+1][2P+1] workspace, needed for P > 96 (NULL
  *          allowed below: the tableau then lives in LDS).
  *  value:  device fp64 [1]; x, y: device fp64 [P] (row and column side).

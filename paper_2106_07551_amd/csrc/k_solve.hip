@@ -524,11 +524,32 @@ __global__ __launch_bounds__(kLpThreads) void lp_kernel(const double* __restrict
     const int tid = threadIdx.x;
     const int W = 2 * P + 1;                 // columns: w (P), slacks (P), right-hand side
     double* T = IN_LDS ? lds : work;
-    // ---- the shift: min(M)
-    double mn = INFINITY;
-    for (int i = tid; i < P * P; i += kLpThreads)
-        mn = fmin(mn, M[i]);
+    // ---- the shift: min(M); a NaN or infinite entry leaves no game to solve
+    // (fmin would skip a NaN): every output is then NaN, pivots -1
+    double mn = INFINITY, finite = 1.0;
+    for (int i = tid; i < P * P; i += kLpThreads) {
+        const double v = M[i];
+        mn = fmin(mn, v);
+        if (!isfinite(v))
+            finite = 0.0;
+    }
     mn = lp_block_min(mn, redd);
+    if (lp_block_min(finite, redd) == 0.0) {
+        for (int j = tid; j < P; j += kLpThreads) {
+            x[j] = (double)NAN;
+            y[j] = (double)NAN;
+            if (sigma) {
+                sigma[j] = NAN;
+                sigma[P + j] = NAN;
+            }
+        }
+        if (tid == 0) {
+            *value = (double)NAN;
+            if (pivots)
+                *pivots = -1;
+        }
+        return;
+    }
     // ---- the initial tableau (slack basis)
     for (int idx = tid; idx < (P + 1) * W; idx += kLpThreads) {
         const int i = idx / W, j = idx - i * W;

@@ -74,3 +74,21 @@ def test_lp_on_a_4v4_table():
     game = pop.payoff_matrix().cpu().numpy()
     pop.close()
     _check(game, "4v4 table")
+
+
+@pytest.mark.parametrize("bad", [float("nan"), float("inf"), -float("inf")])
+@pytest.mark.parametrize("P", [3, 120])
+def test_lp_non_finite_game_gives_nan(bad, P):
+    """A NaN or infinite payoff leaves no game to solve: value, both
+    strategies and the weight rows are NaN and pivots is -1, for the tableau
+    in LDS (P <= 96) and in the workspace."""
+    import paper_2106_07551_amd as MA
+    M = np.random.default_rng(P).uniform(-1, 1, (P, P))
+    M[P // 2, P - 1] = bad
+    g = torch.from_numpy(M).cuda()
+    value, x, y, sigma, piv = MA.solve_lp(g)
+    torch.cuda.synchronize()
+    assert np.isnan(float(value.cpu()[0]))
+    assert np.isnan(x.cpu().numpy()).all() and np.isnan(y.cpu().numpy()).all()
+    assert np.isnan(sigma.cpu().numpy()).all()
+    assert int(piv.cpu()[0]) == -1
