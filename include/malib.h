@@ -55,6 +55,15 @@ enum {
     MALIB_E_DEVICE = -5        /* the device flagged bad data (see above) */
 };
 
+/*
+ * Allocation failures can be forced for tests of the error paths: while the
+ * environment variable MALIB_FAULT_ALLOC is set to anything but "" or "0",
+ * every device or pinned host allocation the library makes (handle creation
+ * and extension, growth of a handle's batch buffers, the meta-samplers'
+ * thresholds) fails without allocating and the call returns MALIB_E_NOMEM,
+ * leaving handles as they were.  The variable is read at each allocation.
+ */
+
 /* ---------------------------------------------------------------- population */
 
 enum {

@@ -26,6 +26,9 @@ _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 _CFLAGS = ["-O2", "-march=x86-64-v3", "-ffp-contract=off", "-fno-fast-math",
            "-fPIC", "-shared", "-std=c11", "-Wall"]
+# A prebuilt oracle library to load instead (the sanitizer test's instrumented
+# build, see build_sanitized); never rebuilt here.
+_LIB_OVERRIDE = os.environ.get("MALIB_ORACLE_LIB")
 
 TOL_BF16 = 1e-2
 TOL_F32 = 1e-5
@@ -38,6 +41,18 @@ def build(force: bool = True) -> str:
         subprocess.check_call(["gcc", *_CFLAGS, _SRC, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
+
+
+def build_sanitized(path: str) -> str:
+    """Compile oracle.c with AddressSanitizer and UndefinedBehaviorSanitizer
+    (gcc; any UB report aborts) into ``path``, same floating-point flags.  Load
+    it by starting a process with MALIB_ORACLE_LIB=path and gcc's libasan.so
+    in LD_PRELOAD."""
+    flags = [f for f in _CFLAGS if f != "-O2"] + [
+        "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+        "-fno-sanitize-recover=undefined"]
+    subprocess.check_call(["gcc", *flags, _SRC, "-o", path, "-lm"])
+    return path
 
 
 class Config(C.Structure):
@@ -59,9 +74,12 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build()
-        L = C.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            L = C.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build()
+            L = C.CDLL(_LIB)
         L.ora_philox4x64_10.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
         L.ora_lane.restype = C.c_uint32
         L.ora_lane.argtypes = [C.c_uint64, C.c_int64, C.c_int64, C.c_int32, C.c_int32,

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -78,6 +79,31 @@ malib_status fail(malib_status code, const char* fmt, ...)
                         "%s failed: %s", #expr, hipGetErrorString(e_));                   \
     } while (0)
 
+// Allocation-failure hook for tests of the error paths: while the environment
+// variable MALIB_FAULT_ALLOC is set to anything but "" or "0", every device
+// or pinned host allocation of the library fails as out of memory without
+// allocating.  Read at each allocation, so a test can turn it on and off.
+bool fault_alloc()
+{
+    const char* v = getenv("MALIB_FAULT_ALLOC");
+    return v && *v && strcmp(v, "0") != 0;
+}
+
+hipError_t dev_malloc(void** p, size_t bytes)
+{
+    return fault_alloc() ? hipErrorOutOfMemory : hipMalloc(p, bytes);
+}
+
+hipError_t host_malloc(void** p, size_t bytes)
+{
+    return fault_alloc() ? hipErrorOutOfMemory : hipHostMalloc(p, bytes, hipHostMallocDefault);
+}
+
+hipError_t dev_malloc_async(void** p, size_t bytes, hipStream_t s)
+{
+    return fault_alloc() ? hipErrorOutOfMemory : hipMallocAsync(p, bytes, s);
+}
+
 hipError_t ensure(DevBuf& b, size_t bytes)
 {
     if (bytes <= b.bytes)
@@ -93,7 +119,7 @@ hipError_t ensure(DevBuf& b, size_t bytes)
         b.bytes = 0;
     }
     size_t want = std::max(bytes, (size_t)256);
-    hipError_t e = hipMalloc(&b.ptr, want);
+    hipError_t e = dev_malloc(&b.ptr, want);
     if (e == hipSuccess)
         b.bytes = want;
     return e;
@@ -316,7 +342,7 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
     for (int l = 0; l < 4; ++l)
         p->dims[l] = dims[l];
     if (desc->kind == MALIB_POLICY_TABULAR) {
-        TRY(hipMalloc((void**)&p->tab, sizeof(float) * P * A));
+        TRY(dev_malloc((void**)&p->tab, sizeof(float) * P * A));
         TRY(hipMemcpyAsync(p->tab, desc->tab_logits, sizeof(float) * P * A,
                            hipMemcpyDeviceToDevice, s));
     } else {
@@ -324,18 +350,18 @@ malib_status malib_pop_create(const malib_pop_desc* desc, void* stream, malib_po
         for (int l = 0; l < 3; ++l) {
             const int fo = dims[l + 1];
             size_t nb = sizeof(float) * (size_t)P * fo;
-            TRY(hipMalloc((void**)&p->b[l], nb));
+            TRY(dev_malloc((void**)&p->b[l], nb));
             if (desc->biases && desc->biases[l])
                 TRY(hipMemcpyAsync(p->b[l], desc->biases[l], nb, hipMemcpyDeviceToDevice, s));
             else
                 TRY(hipMemsetAsync(p->b[l], 0, nb, s));
-            TRY(hipMalloc(&p->w[l], weight_bytes(*p, l) * P));
+            TRY(dev_malloc(&p->w[l], weight_bytes(*p, l) * P));
             TRY(store_weights(*p, l, desc->weights[l], P, p->w[l], s));
         }
     }
     const size_t PP = (size_t)P * P, acc_bytes = sizeof(unsigned long long) * (3 * PP + 2);
-    TRY(hipMalloc((void**)&p->acc, acc_bytes));
-    TRY(hipHostMalloc((void**)&p->host_acc, acc_bytes, hipHostMallocDefault));
+    TRY(dev_malloc((void**)&p->acc, acc_bytes));
+    TRY(host_malloc((void**)&p->host_acc, acc_bytes));
     p->sum = p->acc;
     p->sumsq = p->acc + PP;
     p->cnt = p->acc + 2 * PP;
@@ -452,7 +478,7 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
     TRY(hipDeviceSynchronize());
     if (pop->kind == MALIB_POLICY_TABULAR) {
         const size_t per = sizeof(float) * A;
-        TRY(hipMalloc((void**)&tab, per * P));
+        TRY(dev_malloc((void**)&tab, per * P));
         TRY(hipMemcpyAsync(tab, pop->tab, per * P0, hipMemcpyDeviceToDevice, s));
         TRY(hipMemcpyAsync(tab + (size_t)P0 * A, add->tab_logits, per * k,
                            hipMemcpyDeviceToDevice, s));
@@ -460,7 +486,7 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
         for (int l = 0; l < 3; ++l) {
             const int fo = dims[l + 1];
             const size_t bper = sizeof(float) * fo;
-            TRY(hipMalloc((void**)&b[l], bper * P));
+            TRY(dev_malloc((void**)&b[l], bper * P));
             TRY(hipMemcpyAsync(b[l], pop->b[l], bper * P0, hipMemcpyDeviceToDevice, s));
             if (add->biases && add->biases[l])
                 TRY(hipMemcpyAsync(b[l] + (size_t)P0 * fo, add->biases[l], bper * k,
@@ -469,14 +495,14 @@ malib_status malib_pop_extend(malib_pop_t pop, const malib_pop_desc* add, void* 
                 TRY(hipMemsetAsync(b[l] + (size_t)P0 * fo, 0, bper * k, s));
             // every layout keeps each policy's weights contiguous, policy-major
             const size_t wper = weight_bytes(*pop, l);
-            TRY(hipMalloc(&w[l], wper * P));
+            TRY(dev_malloc(&w[l], wper * P));
             TRY(hipMemcpyAsync(w[l], pop->w[l], wper * P0, hipMemcpyDeviceToDevice, s));
             TRY(store_weights(*pop, l, add->weights[l], k, (char*)w[l] + wper * P0, s));
         }
     }
     const size_t PP = (size_t)P * P, acc_bytes = sizeof(unsigned long long) * (3 * PP + 2);
-    TRY(hipMalloc((void**)&acc, acc_bytes));
-    TRY(hipHostMalloc((void**)&host_acc, acc_bytes, hipHostMallocDefault));
+    TRY(dev_malloc((void**)&acc, acc_bytes));
+    TRY(host_malloc((void**)&host_acc, acc_bytes));
     TRY(launch_remap_table(pop->acc, P0, acc, P, s));
     // the copies and the remap read the old buffers
     TRY(hipDeviceSynchronize());
@@ -1196,7 +1222,7 @@ malib_status malib_meta_sample(const float* sigma, int32_t n_sigma, int32_t P, i
     // copy is staged synchronously from pageable memory before returning.
     unsigned long long* d_thr = nullptr;
     size_t nb = sizeof(unsigned long long) * thr.size();
-    HIP_TRY(hipMallocAsync((void**)&d_thr, nb, s));
+    HIP_TRY(dev_malloc_async((void**)&d_thr, nb, s));
     HIP_TRY(hipMemcpyAsync(d_thr, thr.data(), nb, hipMemcpyHostToDevice, s));
     HIP_TRY(hipStreamSynchronize(s));
     HIP_TRY(launch_meta_sample(d_thr, default_seat_map(n_sigma), P, n_envs, n_agents, seed,
@@ -1304,7 +1330,8 @@ malib_status malib_meta_sample_device(const float* sigma, int32_t n_sigma, int32
         return MALIB_OK;
     hipStream_t s = (hipStream_t)stream;
     unsigned long long* d_thr = nullptr;
-    HIP_TRY(hipMallocAsync((void**)&d_thr, sizeof(unsigned long long) * (size_t)n_sigma * P, s));
+    HIP_TRY(dev_malloc_async((void**)&d_thr, sizeof(unsigned long long) * (size_t)n_sigma * P,
+                             s));
     HIP_TRY(launch_thresholds(sigma, n_sigma, P, d_thr, s));
     HIP_TRY(launch_meta_sample(d_thr, seat_map, P, n_envs, n_agents, seed, env_offset, out, s));
     HIP_TRY(hipFreeAsync(d_thr, s));

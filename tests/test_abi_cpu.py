@@ -178,3 +178,22 @@ def test_policy_ids_validated_before_device_work():
     assert not h.value
     n = C.c_int32()
     assert L.malib_pop_policy_ids(None, None, 0, C.byref(n)) == B.E_INVAL
+
+
+def test_fault_hook_forces_nomem(monkeypatch):
+    """MALIB_FAULT_ALLOC makes the library's allocations fail as out of memory
+    (here the meta-sampler's threshold buffer, reached after validation with no
+    device work before it); cleared, the same call gets past the hook."""
+    import paper_2106_07551_amd as M
+    L = M.lib()
+    B = M.binding
+    sig = np.array([1.0, 2.0, 3.0], np.float32)
+    out = C.c_void_p(16)   # never dereferenced: the allocation fails first
+    monkeypatch.setenv("MALIB_FAULT_ALLOC", "1")
+    assert L.malib_meta_sample(sig.ctypes.data, 1, 3, 10, 2, 1, 0, out, None) == B.E_NOMEM
+    assert b"out of memory" in L.malib_last_error().lower() or b"dev_malloc_async" in \
+        L.malib_last_error()
+    monkeypatch.setenv("MALIB_FAULT_ALLOC", "0")
+    # without the hook the call reaches the HIP runtime (no GPU here: a HIP error)
+    st = L.malib_meta_sample(sig.ctypes.data, 1, 3, 10, 2, 1, 0, out, None)
+    assert st != B.E_NOMEM and st != B.E_INVAL
