@@ -650,6 +650,58 @@ def test_team_2v2_brute_force_and_reduction():
             assert np.isclose(mean[pids_one[a], pids_one[b]], g.mean())
 
 
+def test_team_4v4_step_vs_numpy():
+    """The 4v4 game's step (R13, R15): s' = tanh(W s + sum over the eight
+    seats of emb[k][a_k]) and r = u . s', against fp64 numpy, for action
+    vectors that differ in every seat (a dropped or repeated seat, a seat
+    read from another seat's table or an action from another seat moves s'
+    far beyond the tolerance)."""
+    wl = W.make(5, P=2, n_envs=4, horizon=1)
+    assert wl.n_agents == 8 and wl.emb.shape == (8, 18, wl.d)
+    s0 = oracle.feature_reset(wl.seed, 3, wl.d)
+    rng = np.random.default_rng(12)
+    for acts in ([0] * 8, list(range(8)), list(range(17, 9, -1)),
+                 rng.integers(0, 18, 8).tolist(), rng.integers(0, 18, 8).tolist()):
+        s1, r = oracle.feature_step(wl, s0, acts)
+        pre = wl.W.astype(np.float64) @ s0
+        for k, a in enumerate(acts):
+            pre = pre + wl.emb[k, a]
+        ref = np.tanh(pre)
+        assert np.abs(s1 - ref).max() <= 2e-6, acts
+        assert abs(r - wl.u.astype(np.float64) @ ref) <= 1e-5
+        # each seat's embedding matters: swapping two seats' different actions
+        # changes the state
+        if acts[0] != acts[7]:
+            sw = list(acts)
+            sw[0], sw[7] = sw[7], sw[0]
+            s_sw, _ = oracle.feature_step(wl, s0, sw)
+            assert np.abs(s_sw - s1).max() > 1e-3
+
+
+def test_team_4v4_reduction_plain_loops():
+    """The 4v4 reduction (R16): every (team +1 seat, team -1 seat) pair of an
+    env adds that env's row-side return to cell (pid_a, pid_b), 16 incidences
+    per env, against plain loops."""
+    wl = W.make(5, P=7, n_envs=4, horizon=1)
+    team = wl.team
+    assert list(team) == [1, 1, 1, 1, -1, -1, -1, -1]
+    rng = np.random.default_rng(13)
+    n, P = 200, 7
+    R = rng.standard_normal((n, 8)).astype(np.float32)
+    R[:, 1:4] = R[:, :1]          # a side's seats share the side's return
+    R[:, 4:] = -R[:, :1]
+    pids = rng.integers(0, P, size=(n, 8))
+    mean, cnt, s, _ = oracle.payoff(R, pids, team, P)
+    S = np.zeros((P, P)); N = np.zeros((P, P), np.int64)
+    for e in range(n):
+        for a in range(4):
+            for b in range(4, 8):
+                S[pids[e, a], pids[e, b]] += float(R[e, a])
+                N[pids[e, a], pids[e, b]] += 1
+    assert cnt.sum() == 16 * n
+    assert np.array_equal(cnt, N) and np.allclose(s, S)
+
+
 # --------------------------------------------------------------------- payoff
 
 def test_payoff_table_plain_loops():
