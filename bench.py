@@ -465,6 +465,10 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device-to-device copies of MIB MiB (the "
                          "reference kernel for scaling HBM byte counters) and exit")
+    ap.add_argument("--envs", type=int, default=0, metavar="N",
+                    help="envs of the batch for the sampled workloads (pursuit, team) "
+                         "instead of the configuration's; e.g. one GPU's share of a "
+                         "table split over several GPUs")
     ap.add_argument("--sweep", default="", metavar="F1,F2,...",
                     help="only run the bandwidth sweep of the env step and the payoff "
                          "reduction at these env-count factors (e.g. 1,8,16,32,64) and exit")
@@ -490,7 +494,14 @@ def main():
         sys.exit(2)
 
     import workloads as W
-    wl = W.make(NAME_TO_C[args.workload])
+    if args.envs:
+        if args.workload not in ("pursuit", "team") or args.envs < 1:
+            print("--envs applies to the sampled workloads (pursuit, team) and must be "
+                  ">= 1", file=sys.stderr)
+            sys.exit(2)
+        wl = W.make(NAME_TO_C[args.workload], n_envs=args.envs)
+    else:
+        wl = W.make(NAME_TO_C[args.workload])
     if not args.no_cpu_baseline:
         cpu_pool_start(wl)        # before anything initialises the GPU
 
@@ -583,7 +594,8 @@ def main():
         flops = policy_flops_per_frame(wl.dims) * n * na        # per launch
         avg_s = policy_avg_us * 1e-6
         ach = flops / avg_s / 1e12
-        traffic, src = profiled_traffic(wl.name)
+        # the committed counters are per launch of the configuration's batch
+        traffic, src = profiled_traffic(wl.name) if not args.envs else (None, None)
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak,
                 "unit": "TFLOP/s", "frac": round(ach / peak, 4),
                 "traffic": traffic, "kernel": "grouped policy forward (" + kname + ")",
