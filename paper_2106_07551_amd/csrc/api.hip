@@ -658,6 +658,7 @@ static malib_status plan_rollout(malib_pop_t pop, const malib_env_desc* env, int
         team[1] = -1;
     }
     EnvArgs& ea = plan.ea;
+    ea.n_cus = pop->n_cus;
     ea.kind = env->kind;
     ea.n_agents = n_agents;
     ea.A = env->n_actions;

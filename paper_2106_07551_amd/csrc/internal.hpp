@@ -185,6 +185,7 @@ struct EnvArgs {
     // (the policy forward gathers these rows: half the bytes, no conversion)
     uint16_t* obs;
     TrajArgs tr;
+    int n_cus = 0;       // compute units of the device (workgroup sizing)
 };
 hipError_t launch_zero_f32(float* x, int64_t n, hipStream_t s);
 hipError_t launch_reset(const EnvArgs& e, int64_t n_envs, uint64_t seed, int64_t env_offset,

@@ -275,7 +275,7 @@ constexpr int kFeatKC = 32;
 // up and drain (d=256: 50 vs 54 us per step of 16384 envs; d=512: -3%).
 constexpr int kFeatWaves = 8, kFeatThreads = 64 * kFeatWaves;
 
-// EPT envs per thread.
+// EPT envs per thread (8, 4, 2 or 1).
 // GW consecutive floats (GW = 1, 2 or 4) as one load or store: outputs are
 // mapped to threads in groups of GW consecutive indices, so the WT reads from
 // LDS, the embedding loads and the state stores are single wide accesses.
@@ -469,14 +469,20 @@ __global__ __launch_bounds__(kFeatThreads) void step_feature_kernel(
                     w[g * GW + j] = t.v[j];
             }
             float sv[EPT];
-            const v4f* sp = reinterpret_cast<const v4f*>(&Ss[c * SSTR + ty * EPT]);
+            if constexpr (EPT % 4 == 0) {
+                const v4f* sp = reinterpret_cast<const v4f*>(&Ss[c * SSTR + ty * EPT]);
 #pragma unroll
-            for (int q = 0; q < EPT / 4; ++q) {
-                v4f t4 = sp[q];
-                sv[4 * q + 0] = t4.x;
-                sv[4 * q + 1] = t4.y;
-                sv[4 * q + 2] = t4.z;
-                sv[4 * q + 3] = t4.w;
+                for (int q = 0; q < EPT / 4; ++q) {
+                    v4f t4 = sp[q];
+                    sv[4 * q + 0] = t4.x;
+                    sv[4 * q + 1] = t4.y;
+                    sv[4 * q + 2] = t4.z;
+                    sv[4 * q + 3] = t4.w;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < EPT; ++i)
+                    sv[i] = Ss[c * SSTR + ty * EPT + i];
             }
 #pragma unroll
             for (int i = 0; i < EPT; ++i)
@@ -601,15 +607,27 @@ hipError_t launch_env_step(const EnvArgs& e, const SampleArgs& sa, int64_t n_env
         float* so = (float*)state_out;
         if (e.A > kMaxActions)
             return hipErrorInvalidValue;
-        // 8 envs per thread for d = 512 (64-env workgroups), 4 below (32 envs)
+        // 8 envs per thread for d = 512 (64-env workgroups), 4 below (32 envs);
+        // at d = 256 a batch too small for one such workgroup per CU takes 2 or
+        // 1 env per thread instead (16- or 8-env workgroups): the step of a
+        // small batch is latency-bound, and more workgroups shorten it (4v4
+        // game: 4096 envs 28.9 -> 25.0 us with 2, 2048 envs 27.3 -> 20.9 us and
+        // 257 envs 26.3 -> 19.0 us with 1; the sums are the same per output)
+        const int64_t cus = e.n_cus > 0 ? e.n_cus : 256;
         const int fb8 = (int)((n_envs + 8 * kFeatWaves - 1) / (8 * kFeatWaves));
         const int fb4 = (int)((n_envs + 4 * kFeatWaves - 1) / (4 * kFeatWaves));
+        const int fb2 = (int)((n_envs + 2 * kFeatWaves - 1) / (2 * kFeatWaves));
+        const int fb1 = (int)((n_envs + kFeatWaves - 1) / kFeatWaves);
         if (e.d == 64)
             step_feature_kernel<64, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
         else if (e.d == 128)
             step_feature_kernel<128, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
-        else if (e.d == 256)
+        else if (e.d == 256 && n_envs >= 4 * kFeatWaves * cus)
             step_feature_kernel<256, 4><<<fb4, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
+        else if (e.d == 256 && n_envs >= 2 * kFeatWaves * cus)
+            step_feature_kernel<256, 2><<<fb2, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
+        else if (e.d == 256)
+            step_feature_kernel<256, 1><<<fb1, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
         else if (e.d == 512)
             step_feature_kernel<512, 8><<<fb8, kFeatThreads, 0, s>>>(e.WT, e.emb, e.u, e, sa, n_envs, si, so, ret);
         else
