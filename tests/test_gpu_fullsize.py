@@ -102,3 +102,20 @@ def test_fullsize_sampled_parity(c):
         assert np.all(g["table"]["counts"] == per)
     if c == 5:
         assert g["table"]["counts"].sum() == 16 * wl.n_envs
+
+
+@pytest.mark.parametrize("n_envs", [5000, 2043])
+def test_team_env_step_workgroup_sizes(n_envs):
+    """The 4v4 game at batch sizes whose env step runs 16-env workgroups (5000
+    envs: 2 per thread, the last workgroup half full) and 8-env workgroups
+    (2043 envs: 1 per thread, the last one with 3): lockstep parity on envs
+    that cover every played policy plus both ends of the batch, the table
+    against the GPU's own returns."""
+    wl = W.make(5, n_envs=n_envs, horizon=12)
+    H = wl.horizon
+    snaps = sorted({0, H // 2, H - 1})
+    g = run_gpu(wl, snaps=snaps)
+    sel = _selection(5, wl, g)
+    rep = check_parity(wl, g, sel)
+    say(f"[team {n_envs} envs] envs {len(sel)}, snapshots {snaps}, {rep}")
+    assert g["table"]["counts"].sum() == 16 * wl.n_envs
