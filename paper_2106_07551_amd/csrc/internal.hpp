@@ -232,11 +232,17 @@ hipError_t launch_mlp_f32(const Pop& pop, const int32_t* perm, const int4* tile_
 // tiles halve the weight traffic per row but leave one workgroup per CU; on
 // the 4v4 and d=512 workloads they measured 12% and 3% slower.)
 constexpr int kBf16TileRows = 64;
-// Threads of a 64-row tile's workgroup: eight wavefronts (two workgroups per
-// CU give four per SIMD to hide the weight-fragment latency; pursuit's forward
-// measured 29.5 -> 23.7 us against four) for hidden widths >= 128; four below,
-// where eight would leave a wavefront no whole tile.
-constexpr int bf16_tile_threads(int hid) { return hid >= 128 ? 512 : 256; }
+// Threads of a 64-row tile's workgroup: eight wavefronts for hidden widths 128
+// and 256 (two workgroups per CU give four per SIMD to hide the
+// weight-fragment latency; pursuit's forward measured 29.5 -> 23.7 us against
+// four); four below, where eight would leave a wavefront no whole tile, and
+// four at 512, where each wavefront then covers 128 output units (four
+// fragment tiles for the same two row tiles: a quarter fewer operand bytes
+// per MFMA, at two wavefronts per SIMD and ~200 registers; 4v4 forward 106.5
+// -> 104.4 us).
+constexpr int bf16_tile_threads(int hid) { return hid >= 128 && hid < 512 ? 512 : 256; }
+// Wavefronts per SIMD the 64-row kernel is compiled for (two workgroups per CU)
+constexpr int bf16_tile_waves_per_simd(int hid) { return hid >= 128 && hid < 512 ? 4 : 2; }
 // Gumbel-max sampling done by the 64-row policy kernel itself (feature
 // observations: no env finishes early): the sampled actions [n_slots], the
 // error flags, the Philox key and the counter parts of the step.

@@ -868,12 +868,12 @@ __device__ __forceinline__ void build_obs(const MlpBf16Args& a, const int* row_s
 }
 
 // MR rows per tile (the library uses 64), two workgroups per CU; eight
-// wavefronts per workgroup for hidden widths >= 128 (four per SIMD in all),
-// four below.
+// wavefronts per workgroup for hidden widths 128 and 256 (four per SIMD in
+// all), four otherwise (bf16_tile_threads).
 // Layers 1 and 2 run from LDS rows; the output layer is fed from the layer-2
 // accumulators (out_from_acc), its partials summed through the row buffer.
 template <int HID, int OBS, int KIN, int MR>
-__global__ __launch_bounds__(bf16_tile_threads(HID), HID >= 128 ? 4 : 2) void mlp_bf16_kernel(
+__global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HID)) void mlp_bf16_kernel(
     MlpBf16Args a)
 {
     constexpr int THREADS = bf16_tile_threads(HID), WAVES = THREADS / 64, RTILES = MR / 32;
