@@ -179,6 +179,31 @@ def test_parity_team_2v2_hidden_widths(hid):
     check_parity(wl, g)
 
 
+_HID512 = {
+    # hidden width 512 (four wavefronts per 64-row tile, 128 output units
+    # each) under every observation build of the 64-row kernel
+    "pursuit_75": lambda: W.with_policies(W.make(3, P=2, n_envs=150, horizon=20), W.MLP_BF16,
+                                          [75, 512, 512, 5]),
+    "iter_24": lambda: W.with_policies(W.make(2, P=3, per_pair=11, horizon=5), W.MLP_BF16,
+                                       [24, 512, 512, 3]),
+    "feature_d64": lambda: W.with_policies(W.team_variant(2, d=64, P=3, n_envs=70, horizon=3),
+                                           W.MLP_BF16, [64, 512, 512, 18]),
+    "feature_d128": lambda: W.with_policies(W.team_variant(4, d=128, P=3, n_envs=60,
+                                                          horizon=3),
+                                            W.MLP_BF16, [128, 512, 512, 18]),
+}
+
+
+@pytest.mark.parametrize("name", sorted(_HID512))
+def test_parity_hidden_width_512_every_observation(name):
+    """Hidden width 512 on the pursuit, iterated-game and narrow feature
+    observations (input widths 80, 32, 64, 128 after padding): ragged and
+    multi-tile buckets, every env against the oracle."""
+    wl = _HID512[name]()
+    g = run_gpu(wl, snaps=[0, wl.horizon - 1])
+    check_parity(wl, g)
+
+
 def test_parity_feature_shared_init_d64():
     wl = W.team_variant(2, d=64, P=3, n_envs=70, horizon=5, dims=[64, 64, 64, 18])
     wl.init_mode = W.INIT_SHARED
