@@ -6,8 +6,8 @@ ctypes and uses torch for device memory and streams.  There is no CPU
 fallback: importing the binding without the built library raises.
 """
 from .binding import (  # noqa: F401
-    MalibError, Population, Env, Trace, Traj, meta_sample, meta_sample_device, solve_fp,
-    solve_alpharank, solve_lp,
+    MalibError, ArgumentError, Population, Env, Trace, Traj, meta_sample,
+    meta_sample_device, solve_fp, solve_alpharank, solve_lp,
     expansion_pairs, aggregate,
     debug_tanh_ref, debug_bf16, debug_philox,
     lib, LIB_PATH, POLICY_TABULAR, POLICY_MLP_F32, POLICY_MLP_BF16, ENV_MATRIX,

@@ -38,6 +38,15 @@ class MalibError(RuntimeError):
         self.status = status
 
 
+class ArgumentError(MalibError, ValueError):
+    """An argument the binding rejects before calling the library (wrong
+    dtype, size, layout or device of a buffer): status MALIB_E_INVAL, as the
+    library itself reports invalid arguments."""
+
+    def __init__(self, msg: str):
+        super().__init__(E_INVAL, msg)
+
+
 class PopDesc(C.Structure):
     _fields_ = [("kind", C.c_int32), ("n_policies", C.c_int32), ("n_actions", C.c_int32),
                 ("n_layers", C.c_int32), ("dims", C.POINTER(C.c_int32)),
@@ -143,11 +152,62 @@ def _stream(stream):
     return C.c_void_p(s.cuda_stream)
 
 
-def _dptr(t) -> Optional[int]:
+def _dptr(t, dtype=None, numel: Optional[int] = None, *, at_least: bool = False,
+          what: str = "tensor") -> Optional[int]:
+    """Device address of a contiguous device tensor (None passes through).
+
+    The library's kernels read and write the buffers it is given with the
+    sizes and element types the header states, so a tensor of another dtype
+    or with fewer elements would be accessed out of bounds on the device:
+    both are errors here (ArgumentError, raised, not asserted), as are host
+    tensors and non-contiguous views.  `numel` is the exact count, or the minimum with
+    `at_least`."""
     if t is None:
         return None
-    assert t.is_cuda and t.is_contiguous(), "expected a contiguous device tensor"
+    _check_buf(t, dtype, numel, at_least, what)
+    if not t.is_cuda:
+        raise ArgumentError(f"{what}: expected a device tensor, got one on {t.device}")
     return t.data_ptr()
+
+
+def _check_buf(t, dtype, numel, at_least, what):
+    """dtype, element count and layout of a buffer (not its device)."""
+    if t is None:
+        return
+    if dtype is not None and t.dtype != dtype:
+        raise ArgumentError(f"{what}: expected dtype {dtype}, got {t.dtype}")
+    if numel is not None:
+        n = t.numel()
+        if (n < numel) if at_least else (n != numel):
+            raise ArgumentError(f"{what}: expected {'at least ' if at_least else ''}{numel} "
+                                f"elements, got {n}")
+    if not t.is_contiguous():
+        raise ArgumentError(f"{what}: expected a contiguous tensor")
+
+
+def _dptrs(*specs):
+    """_dptr over several buffers (t, dtype, numel, at_least, what): every
+    dtype, size and layout is checked before any device, so that the first
+    error reported is the most specific one."""
+    for sp in specs:
+        _check_buf(*sp)
+    return [_dptr(*sp[:3], at_least=sp[3], what=sp[4]) for sp in specs]
+
+
+def _dbytes(t, nbytes: int, what: str) -> Optional[int]:
+    """Like _dptr for buffers whose element type the caller chooses: at least
+    `nbytes` bytes."""
+    if t is None:
+        return None
+    if t.numel() * t.element_size() < nbytes:
+        raise ArgumentError(f"{what}: expected at least {nbytes} bytes, got "
+                         f"{t.numel() * t.element_size()}")
+    return _dptr(t, what=what)
+
+
+def _f32():
+    import torch
+    return torch.float32
 
 
 def _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits,
@@ -158,22 +218,36 @@ def _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits,
     d.kind, d.n_policies, d.n_actions = kind, n_policies, n_actions
     keep = []
     if policy_ids is not None:
+        if len(policy_ids) != n_policies:
+            raise ArgumentError(f"policy_ids: expected {n_policies} ids, got {len(policy_ids)}")
         ids = (C.c_int64 * n_policies)(*[int(x) for x in policy_ids])
-        assert len(policy_ids) == n_policies
         keep.append(ids)
         d.policy_ids = C.cast(ids, C.POINTER(C.c_int64))
     if kind == POLICY_TABULAR:
         d.n_layers = 0
-        d.tab_logits = _dptr(tab_logits)
+        if tab_logits is None:
+            raise ArgumentError("a tabular population needs tab_logits")
+        d.tab_logits = _dptr(tab_logits, _f32(), n_policies * n_actions, what="tab_logits")
     else:
-        d.n_layers = len(dims) - 1
-        dd = (C.c_int32 * len(dims))(*dims)
-        ww = (C.c_void_p * d.n_layers)(*[_dptr(w) for w in weights])
+        if dims is None or len(dims) != 4 or len(weights) != 3:
+            raise ArgumentError("an MLP population needs dims [in, h1, h2, A] and three weights")
+        if biases is not None and len(biases) != 3:
+            raise ArgumentError("biases: expected three entries (each a tensor or None)")
+        d.n_layers = 3
+        f32 = _f32()
+        specs = [(w, f32, n_policies * dims[l + 1] * dims[l], False, f"weights[{l}]")
+                 for l, w in enumerate(weights)]
+        if biases is not None:
+            specs += [(b, f32, n_policies * dims[l + 1], False, f"biases[{l}]")
+                      for l, b in enumerate(biases)]
+        ptrs = _dptrs(*specs)
+        dd = (C.c_int32 * 4)(*dims)
+        ww = (C.c_void_p * 3)(*ptrs[:3])
         keep += [dd, ww]
         d.dims = C.cast(dd, C.POINTER(C.c_int32))
         d.weights = C.cast(ww, C.POINTER(C.c_void_p))
         if biases is not None:
-            bb = (C.c_void_p * d.n_layers)(*[_dptr(b) for b in biases])
+            bb = (C.c_void_p * 3)(*ptrs[3:])
             keep.append(bb)
             d.biases = C.cast(bb, C.POINTER(C.c_void_p))
     return d, keep
@@ -217,7 +291,8 @@ class Population:
         n = C.c_int32()
         out = np.zeros(self.P, np.int64)
         _check(lib().malib_pop_policy_ids(self.handle, out.ctypes.data, self.P, C.byref(n)))
-        assert n.value == self.P
+        if n.value != self.P:
+            raise RuntimeError(f"malib_pop_policy_ids returned {n.value} ids for P = {self.P}")
         return out
 
     def close(self):
@@ -227,29 +302,42 @@ class Population:
 
     __del__ = close
 
+    def _batch_ptrs(self, env: "Env", n_envs: int, pair_assign, returns):
+        """pair_assign int32 [n_envs][n_agents] and returns fp32 [n_agents][n_envs]
+        (at least that many elements; counts the library rejects pass through
+        to it)."""
+        import torch
+        ns = max(int(n_envs), 0) * env.n_agents
+        return (_dptr(pair_assign, torch.int32, ns, at_least=True, what="pair_assign"),
+                _dptr(returns, torch.float32, ns, at_least=True, what="returns"))
+
     def rollout(self, env: "Env", n_envs: int, pair_assign, seed: int, horizon: int, *,
                 env_offset: int = 0, returns=None, trace: "Trace" = None, stream=None):
-        tr = trace.desc if trace is not None else None
+        pa, rp = self._batch_ptrs(env, n_envs, pair_assign, returns)
+        tr = trace.checked(env, n_envs, horizon, self.P, self.A) if trace is not None else None
         _check(lib().malib_rollout_batch(
-            self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
-            horizon, _dptr(returns), C.byref(tr) if tr is not None else None,
+            self.handle, C.byref(env.desc), n_envs, pa, seed, env_offset,
+            horizon, rp, C.byref(tr) if tr is not None else None,
             _stream(stream)))
 
     def rollout_noalloc(self, env: "Env", n_envs: int, pair_assign, seed: int, horizon: int,
                         *, env_offset: int = 0, returns=None, stream=None):
         """malib_rollout_batch_noalloc: the same batch on the library's static
         scratch (no device allocation; calls on one GPU must not overlap)."""
+        pa, rp = self._batch_ptrs(env, n_envs, pair_assign, returns)
         _check(lib().malib_rollout_batch_noalloc(
-            self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
-            horizon, _dptr(returns), _stream(stream)))
+            self.handle, C.byref(env.desc), n_envs, pa, seed, env_offset,
+            horizon, rp, _stream(stream)))
 
     def rollout_traj(self, env: "Env", n_envs: int, pair_assign, seed: int, horizon: int,
                      traj: Traj, *, env_offset: int = 0, returns=None, stream=None):
         """malib_rollout_batch_traj: a rollout that also writes its per-step
         records into `traj` (advancing its cursor)."""
+        pa, rp = self._batch_ptrs(env, n_envs, pair_assign, returns)
+        traj.check(env)
         _check(lib().malib_rollout_batch_traj(
-            self.handle, C.byref(env.desc), n_envs, _dptr(pair_assign), seed, env_offset,
-            horizon, _dptr(returns), C.byref(traj.desc), _stream(stream)))
+            self.handle, C.byref(env.desc), n_envs, pa, seed, env_offset,
+            horizon, rp, C.byref(traj.desc), _stream(stream)))
 
     def payoff_matrix(self, out=None, stream=None):
         """malib_payoff_matrix: the table's means as a device fp64 [P][P] game
@@ -257,7 +345,9 @@ class Population:
         import torch
         if out is None:
             out = torch.empty((self.P, self.P), dtype=torch.float64, device="cuda")
-        _check(lib().malib_payoff_matrix(self.handle, _dptr(out), _stream(stream)))
+        _check(lib().malib_payoff_matrix(
+            self.handle, _dptr(out, torch.float64, self.P * self.P, what="out"),
+            _stream(stream)))
         return out
 
     def payoff(self, reset: bool = False, stream=None, check: bool = True):
@@ -303,12 +393,21 @@ class Env:
             kind, n_agents, n_actions, grid, d, init_mode)
         self._keep = [A, W, emb, u]
         if team is not None:
+            if len(team) != n_agents:
+                raise ArgumentError(f"team: expected {n_agents} entries, got {len(team)}")
             tt = (C.c_int8 * n_agents)(*[int(x) for x in team])
             self._keep.append(tt)
             e.team = C.cast(tt, C.POINTER(C.c_int8))
-        e.A, e.W, e.emb, e.u = _dptr(A), _dptr(W), _dptr(emb), _dptr(u)
+        f32 = _f32()
+        e.A, e.W, e.emb, e.u = _dptrs((A, f32, n_actions * n_actions, False, "A"),
+                                      (W, f32, d * d, False, "W"),
+                                      (emb, f32, n_agents * n_actions * d, False, "emb"),
+                                      (u, f32, d, False, "u"))
         self.desc = e
+        self.kind = kind
         self.n_agents = n_agents
+        self.n_actions = n_actions
+        self.d = d
 
 
 class Traj:
@@ -327,12 +426,29 @@ class Traj:
         if obs_shape is not None:
             self.obs = torch.empty((capacity,) + tuple(obs_shape), dtype=obs_dtype,
                                    device=device)
-        self.desc = TrajDesc(_dptr(self.actions), _dptr(self.rewards), _dptr(self.flags),
-                             _dptr(self.obs), capacity, 0)
+        # its own tensors: the device is checked before each rollout (check)
+        self.desc = TrajDesc(self.actions.data_ptr(), self.rewards.data_ptr(),
+                             self.flags.data_ptr(),
+                             None if self.obs is None else self.obs.data_ptr(), capacity, 0)
 
     @property
     def cursor(self) -> int:
         return self.desc.cursor
+
+    def check(self, env: "Env"):
+        """The ring's buffers against the environment's record layout."""
+        if not 0 <= self.desc.capacity <= self.capacity:
+            raise ArgumentError(f"traj: capacity {self.desc.capacity} is outside the ring's "
+                             f"{self.capacity} records")
+        if self.actions.shape[1] != env.n_agents:
+            raise ArgumentError(f"traj: actions hold {self.actions.shape[1]} seats, the "
+                             f"environment has {env.n_agents}")
+        per = {ENV_ITER_MATRIX: 2, ENV_PURSUIT: 2, ENV_FEATURE: 2 * env.d}.get(env.kind, 0)
+        if self.obs is not None and per:
+            _dbytes(self.obs, self.capacity * per, "traj.obs")
+        if not self.actions.is_cuda:
+            raise ArgumentError(f"traj: expected device tensors, got ones on "
+                                f"{self.actions.device}")
 
 
 class Trace:
@@ -350,6 +466,28 @@ class Trace:
         t.perm, t.offsets = _dptr(perm), _dptr(offsets)
         self._keep = [ss, actions, logits, states, perm, offsets]
         self.desc = t
+        self.n_snap = len(steps)
+        self.actions, self.logits, self.states = actions, logits, states
+        self.perm, self.offsets = perm, offsets
+
+    def checked(self, env: "Env", n_envs: int, horizon: int, P: int, A: int):
+        """The descriptor, after checking each buffer against the batch that
+        will write it (sizes as in malib.h's malib_trace)."""
+        import torch
+        ns = max(int(n_envs), 0) * env.n_agents
+        h = max(int(horizon), 0)
+        per = {ENV_ITER_MATRIX: 2, ENV_PURSUIT: 3, ENV_FEATURE: 4 * env.d}.get(env.kind, 0)
+        st = self.states
+        if st is not None and st.numel() * st.element_size() < self.n_snap * per * max(n_envs, 0):
+            raise ArgumentError(f"trace.states: expected at least "
+                                f"{self.n_snap * per * max(n_envs, 0)} bytes, got "
+                                f"{st.numel() * st.element_size()}")
+        _dptrs((self.actions, torch.uint8, h * ns, True, "trace.actions"),
+               (self.logits, torch.float32, self.n_snap * ns * A, True, "trace.logits"),
+               (st, None, None, True, "trace.states"),
+               (self.perm, torch.int32, ns, True, "trace.perm"),
+               (self.offsets, torch.int32, P + 1, True, "trace.offsets"))
+        return self.desc
 
 
 def meta_sample(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *,
@@ -359,8 +497,9 @@ def meta_sample(sigma, n_policies: int, n_envs: int, n_agents: int, seed: int, *
     s = np.ascontiguousarray(sigma, dtype=np.float32).reshape(-1, n_policies)
     if out is None:
         out = torch.empty((n_envs, n_agents), dtype=torch.int32, device="cuda")
+    op = _dptr(out, torch.int32, max(n_envs, 0) * max(n_agents, 0), at_least=True, what="out")
     _check(lib().malib_meta_sample(s.ctypes.data, s.shape[0], n_policies, n_envs, n_agents,
-                                   seed, env_offset, _dptr(out), _stream(stream)))
+                                   seed, env_offset, op, _stream(stream)))
     return out
 
 
@@ -375,25 +514,36 @@ def expansion_pairs(n_policies: int, first_new: int, per_pair: int, n_agents: in
     tm = None
     if team is not None:
         tm = np.ascontiguousarray(team, dtype=np.int8)
-        assert tm.shape == (n_agents,)
+        if tm.shape != (n_agents,):
+            raise ArgumentError(f"team: expected shape ({n_agents},), got {tm.shape}")
+    op = _dptr(out, torch.int32, max(n, 0) * max(n_agents, 0), at_least=True, what="out")
     _check(lib().malib_expansion_pairs(n_policies, first_new, per_pair, n_agents,
-                                       None if tm is None else tm.ctypes.data, _dptr(out),
+                                       None if tm is None else tm.ctypes.data, op,
                                        _stream(stream)))
     return out
+
+
+def _game(M) -> int:
+    """P of a device fp64 [P][P] game, checked."""
+    import torch
+    if M.dim() != 2 or M.shape[0] != M.shape[1]:
+        raise ArgumentError(f"M: expected a square [P][P] game, got shape {tuple(M.shape)}")
+    _dptr(M, torch.float64, what="M")
+    return int(M.shape[0])
 
 
 def solve_fp(M, iterations: int, *, sigma=None, gap=None, stream=None):
     """malib_solve_fp on a device fp64 [P][P] game: returns (sigma [2][P] play
     counts as fp32, gap [1] fp64), both device tensors."""
     import torch
-    P = M.shape[0]
-    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
+    P = _game(M)
     if sigma is None:
         sigma = torch.empty((2, P), dtype=torch.float32, device=M.device)
     if gap is None:
         gap = torch.empty(1, dtype=torch.float64, device=M.device)
-    _check(lib().malib_solve_fp(_dptr(M), P, iterations, _dptr(sigma), _dptr(gap),
-                                _stream(stream)))
+    _check(lib().malib_solve_fp(_dptr(M), P, iterations,
+                                _dptr(sigma, torch.float32, 2 * P, what="sigma"),
+                                _dptr(gap, torch.float64, 1, what="gap"), _stream(stream)))
     return sigma, gap
 
 
@@ -402,8 +552,7 @@ def solve_lp(M, *, work=None, stream=None):
     x [P] fp64, y [P] fp64, sigma [2][P] fp32, pivots [1] int32), device
     tensors; a workspace is allocated here when P > 96 and none is given."""
     import torch
-    P = M.shape[0]
-    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
+    P = _game(M)
     dev = M.device
     value = torch.empty(1, dtype=torch.float64, device=dev)
     x = torch.empty(P, dtype=torch.float64, device=dev)
@@ -412,7 +561,8 @@ def solve_lp(M, *, work=None, stream=None):
     pivots = torch.empty(1, dtype=torch.int32, device=dev)
     if work is None and P > 96:
         work = torch.empty((P + 1) * (2 * P + 1), dtype=torch.float64, device=dev)
-    _check(lib().malib_solve_lp(_dptr(M), P, _dptr(work), _dptr(value), _dptr(x), _dptr(y),
+    wp = _dptr(work, torch.float64, (P + 1) * (2 * P + 1), at_least=True, what="work")
+    _check(lib().malib_solve_lp(_dptr(M), P, wp, _dptr(value), _dptr(x), _dptr(y),
                                 _dptr(sigma), _dptr(pivots), _stream(stream)))
     return value, x, y, sigma, pivots
 
@@ -422,16 +572,18 @@ def solve_alpharank(M, alpha: float, m: int, *, pi=None, sigma=None, work=None, 
     fp64, sigma [2][P] fp32 weight rows), device tensors; a [P][P] fp64
     workspace is allocated here when P > 128 and none is given."""
     import torch
-    P = M.shape[0]
-    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
+    P = _game(M)
     if pi is None:
         pi = torch.empty(P, dtype=torch.float64, device=M.device)
     if sigma is None:
         sigma = torch.empty((2, P), dtype=torch.float32, device=M.device)
     if work is None and P > 128:
         work = torch.empty((P, P), dtype=torch.float64, device=M.device)
-    _check(lib().malib_solve_alpharank(_dptr(M), P, float(alpha), int(m), _dptr(work),
-                                       _dptr(pi), _dptr(sigma), _stream(stream)))
+    _check(lib().malib_solve_alpharank(
+        _dptr(M), P, float(alpha), int(m),
+        _dptr(work, torch.float64, P * P, at_least=True, what="work"),
+        _dptr(pi, torch.float64, P, what="pi"), _dptr(sigma, torch.float32, 2 * P, what="sigma"),
+        _stream(stream)))
     return pi, sigma
 
 
@@ -439,12 +591,11 @@ def aggregate(M, sigma, br_row: int = -1, br_col: int = -1, *, out=None, stream=
     """malib_aggregate: device fp64 [5] = (nash payoff of the row side, of
     the column side, best-response payoff of br_row, of br_col, improvement)."""
     import torch
-    P = M.shape[0]
-    assert M.dtype == torch.float64 and M.is_contiguous() and tuple(M.shape) == (P, P)
-    assert sigma.dtype == torch.float32 and sigma.is_contiguous() and sigma.numel() == 2 * P
+    P = _game(M)
     if out is None:
         out = torch.empty(5, dtype=torch.float64, device=M.device)
-    _check(lib().malib_aggregate(_dptr(M), P, _dptr(sigma), br_row, br_col, _dptr(out),
+    _check(lib().malib_aggregate(_dptr(M), P, _dptr(sigma, torch.float32, 2 * P, what="sigma"),
+                                 br_row, br_col, _dptr(out, torch.float64, 5, what="out"),
                                  _stream(stream)))
     return out
 
@@ -455,17 +606,22 @@ def meta_sample_device(sigma, n_policies: int, n_envs: int, n_agents: int, seed:
     sigma [n_sigma][P] (fp32); seat k uses row seat_row[k] (default: row 0
     for all seats when there is one row, else row k)."""
     import torch
-    assert sigma.dtype == torch.float32 and sigma.is_contiguous()
+    if n_policies < 1 or sigma.numel() % n_policies or sigma.numel() == 0:
+        raise ArgumentError(f"sigma: expected [n_sigma][{n_policies}] weights, got "
+                         f"{sigma.numel()} elements")
     n_sigma = sigma.numel() // n_policies
-    if out is None:
-        out = torch.empty((n_envs, n_agents), dtype=torch.int32, device=sigma.device)
     sr = None
     if seat_row is not None:
         sr = np.ascontiguousarray(seat_row, dtype=np.int32)
-        assert sr.shape == (n_agents,)
-    _check(lib().malib_meta_sample_device(_dptr(sigma), n_sigma, n_policies, n_envs, n_agents,
+        if sr.shape != (n_agents,):
+            raise ArgumentError(f"seat_row: expected shape ({n_agents},), got {sr.shape}")
+    if out is None:
+        out = torch.empty((n_envs, n_agents), dtype=torch.int32, device=sigma.device)
+    sp, op = _dptrs((sigma, torch.float32, None, False, "sigma"),
+                    (out, torch.int32, max(n_envs, 0) * max(n_agents, 0), True, "out"))
+    _check(lib().malib_meta_sample_device(sp, n_sigma, n_policies, n_envs, n_agents,
                                           None if sr is None else sr.ctypes.data, seed,
-                                          env_offset, _dptr(out), _stream(stream)))
+                                          env_offset, op, _stream(stream)))
     return out
 
 
@@ -473,7 +629,9 @@ def debug_tanh_ref(x, y=None, stream=None):
     import torch
     if y is None:
         y = torch.empty_like(x)
-    _check(lib().malib_debug_tanh_ref(_dptr(x), _dptr(y), x.numel(), _stream(stream)))
+    _check(lib().malib_debug_tanh_ref(_dptr(x, torch.float32, what="x"),
+                                      _dptr(y, torch.float32, x.numel(), what="y"), x.numel(),
+                                      _stream(stream)))
     return y
 
 
@@ -481,13 +639,16 @@ def debug_bf16(x, stream=None):
     """bf16 bit patterns (as int16) of an even-length fp32 device tensor."""
     import torch
     y = torch.empty(x.shape, dtype=torch.int16, device=x.device)
-    _check(lib().malib_debug_bf16(_dptr(x), _dptr(y), x.numel(), _stream(stream)))
+    _check(lib().malib_debug_bf16(_dptr(x, torch.float32, what="x"), _dptr(y), x.numel(),
+                                  _stream(stream)))
     return y
 
 
 def debug_philox(ctr, key0: int, key1: int, stream=None):
     import torch
+    if ctr.dim() != 2 or ctr.shape[1] != 4:
+        raise ArgumentError(f"ctr: expected [n][4] counters, got shape {tuple(ctr.shape)}")
     out = torch.empty_like(ctr)
-    _check(lib().malib_debug_philox(_dptr(ctr), key0, key1, _dptr(out), ctr.shape[0],
-                                    _stream(stream)))
+    _check(lib().malib_debug_philox(_dptr(ctr, torch.int64, what="ctr"), key0, key1, _dptr(out),
+                                    ctr.shape[0], _stream(stream)))
     return out

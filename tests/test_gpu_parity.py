@@ -443,12 +443,23 @@ def test_host_validation_errors():
     bad = M.Env(M.ENV_FEATURE, 2, 18, team=[1, -1], d=96, W=None, emb=None, u=None)
     with pytest.raises(M.MalibError):
         pop.rollout(bad, wl.n_envs, pairs, wl.seed, 2)
-    # widths beyond 1024 are rejected before any device work (the weights
-    # below are never read)
+    # widths beyond 1024 are rejected by the library before any device work
+    # (the weights below, sized as the header requires, are never read)
+    dims = [512, 2048, 2048, 18]
+    ws = [torch.zeros(2 * dims[l + 1] * dims[l], device="cuda") for l in range(3)]
     with pytest.raises(M.MalibError) as e:
-        M.Population(M.POLICY_MLP_BF16, 2, 18, dims=[512, 2048, 2048, 18],
-                     weights=[torch.zeros(1, device="cuda")] * 3)
+        M.Population(M.POLICY_MLP_BF16, 2, 18, dims=dims, weights=ws)
     assert e.value.status == M.binding.E_UNSUPPORTED
+    del ws
+    # buffers of the wrong size or dtype never reach the library
+    with pytest.raises(M.ArgumentError):
+        pop.rollout(env, wl.n_envs, pairs[:-1], wl.seed, 2)
+    with pytest.raises(M.ArgumentError):
+        pop.rollout(env, wl.n_envs, pairs.to(torch.int64), wl.seed, 2)
+    with pytest.raises(M.ArgumentError):
+        pop.rollout(env, wl.n_envs, pairs, wl.seed, 2,
+                    returns=torch.empty(wl.n_envs, device="cuda"))
+    assert pop.payoff()["counts"].sum() == 0
     pop.close()
 
 
