@@ -538,6 +538,33 @@ def test_parity_matrix_many_actions(n_actions):
     check_parity(wl, g)
 
 
+# ------------------------------------------------------------ action counts
+
+@pytest.mark.parametrize("A, hid", [(32, 512), (9, 256), (1, 128)])
+def test_parity_feature_action_counts(A, hid):
+    """The feature game's sampling inside the 64-row kernel at 32 actions
+    (four full Philox blocks per row, every partial-logit register group),
+    9 (a block of one) and 1 (the only action always wins): 2v2 game, d = 128,
+    every env against the oracle."""
+    wl = W.team_variant(4, d=128, P=5, n_envs=90, horizon=3)
+    rng = np.random.default_rng([2106, 7551, 32, A])
+    wl.n_actions = A
+    wl.emb = rng.normal(0.0, np.sqrt(0.1), (wl.n_agents, A, wl.d)).astype(np.float32)
+    wl = W.with_policies(wl, W.MLP_BF16, [wl.d, hid, hid, A], variant=A)
+    g = run_gpu(wl, snaps=[0, 2])
+    check_parity(wl, g)
+    if A == 1:
+        assert (g["actions"] == 0).all()
+
+
+def test_parity_team_max_population():
+    """The 4v4 game with 256 policies (8-bit policy ids, about four rows per
+    policy, every tile ragged), every env against the oracle."""
+    wl = W.make(5, P=256, n_envs=120, horizon=2)
+    g = run_gpu(wl, snaps=[0, 1])
+    check_parity(wl, g)
+
+
 # ------------------------------------------------------------ largest population
 
 def test_parity_max_population_pursuit():
