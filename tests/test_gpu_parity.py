@@ -557,6 +557,18 @@ def test_parity_feature_action_counts(A, hid):
         assert (g["actions"] == 0).all()
 
 
+@pytest.mark.parametrize("team, P", [([1, 1, -1], 6), ([1, -1, -1, 1, -1], 9),
+                                     ([-1, 1, 1, -1, 1, -1, 1], 70)])
+def test_parity_team_odd_sides(team, P):
+    """Odd seat counts with unequal and interleaved sides (3, 5 and 7 seats;
+    70 policies take the bucketed payoff reduction): returns, states, actions
+    and the table against the oracle, every env."""
+    wl = W.team_variant(len(team), d=64, P=P, n_envs=80, horizon=3, team=team,
+                        dims=[64, 128, 128, 18])
+    g = run_gpu(wl, snaps=[0, 2])
+    check_parity(wl, g)
+
+
 def test_parity_team_max_population():
     """The 4v4 game with 256 policies (8-bit policy ids, about four rows per
     policy, every tile ragged), every env against the oracle."""

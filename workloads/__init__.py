@@ -190,9 +190,11 @@ def make(c: int, *, n_envs: Optional[int] = None, horizon: Optional[int] = None,
 
 
 def team_variant(n_agents: int, *, d: int = 256, P: int = 8, n_envs: int = 64,
-                 horizon: int = 4, variant: int = 0, dims=None) -> Workload:
-    """A smaller team game (n_agents/2 per side) on the feature dynamics, used to
-    pin the team reduction by brute force (2v2) and for quick parity cases."""
+                 horizon: int = 4, variant: int = 0, dims=None, team=None) -> Workload:
+    """A smaller team game on the feature dynamics, used to pin the team
+    reduction by brute force (2v2) and for quick parity cases.  Sides: `team`
+    (+1 row side, -1 column side per seat), else the first ceil(n_agents/2)
+    seats against the rest."""
     rng = _rng(50 + n_agents, variant)
     W = _normal(rng, 1.0 / d, (d, d))
     emb = _normal(rng, 0.1, (n_agents, 18, d))
@@ -200,7 +202,10 @@ def team_variant(n_agents: int, *, d: int = 256, P: int = 8, n_envs: int = 64,
     sigma = rng.dirichlet(np.ones(P)).astype(np.float32)[None, :]
     dims = dims or [d, 64, 64, 18]
     Ws, bs = _mlp(rng, P, dims, bf16=True)
-    team = np.array([1] * (n_agents // 2) + [-1] * (n_agents // 2), np.int8)
+    if team is None:
+        team = [1] * ((n_agents + 1) // 2) + [-1] * (n_agents // 2)
+    team = np.array(team, np.int8)
+    assert team.shape == (n_agents,)
     wl = Workload(50 + n_agents, f"team{n_agents}", FEATURE, n_agents, 18, team, horizon,
                   n_envs, MLP_BF16, P, dims, Ws, bs, d=d, W=W, emb=emb, u=u, sigma=sigma)
     wl.seed = ROLLOUT_KEY_BASE + 50 + n_agents + (variant << 8)
