@@ -6,6 +6,7 @@ call goes straight to the C ABI of ``include/malib.h``; names follow it.
 from __future__ import annotations
 
 import ctypes as C
+import sys
 import os
 from typing import Optional, Sequence
 
@@ -263,6 +264,8 @@ class Population:
         d, keep = _pop_desc(kind, n_policies, n_actions, dims, weights, biases, tab_logits,
                             policy_ids)
         h = C.c_void_p()
+        self._destroy = lib().malib_pop_destroy
+        self._finalizing = sys.is_finalizing
         _check(lib().malib_pop_create(C.byref(d), _stream(stream), C.byref(h)))
         del keep
         self.handle = h
@@ -296,9 +299,17 @@ class Population:
         return out
 
     def close(self):
-        if getattr(self, "handle", None):
-            lib().malib_pop_destroy(self.handle)
-            self.handle = None
+        """malib_pop_destroy (also on garbage collection).  At interpreter exit
+        the call is skipped: module globals and the HIP runtime may already be
+        torn down, and the process's device memory is released with it; the
+        functions used here are the ones captured when the handle was made."""
+        h = getattr(self, "handle", None)
+        if not h:
+            return
+        self.handle = None
+        if self._finalizing():
+            return
+        self._destroy(h)
 
     __del__ = close
 

@@ -84,3 +84,28 @@ def test_extend_and_batch_growth_under_forced_nomem(monkeypatch):
     tab = pop.payoff(reset=True)
     assert tab["envs"] == 5 * wl.n_envs and tab["status"] == 0
     pop.close()
+
+
+def test_handle_alive_at_interpreter_exit():
+    """A population still alive when the interpreter exits (a module-level
+    handle) neither raises from its finalizer nor calls into the torn-down
+    runtime: the process exits 0 with nothing on stderr about it."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "import numpy as np, torch, workloads as W\n"
+        "from paper_2106_07551_amd import workload_io as IO\n"
+        "wl = W.make(1, P=3, per_pair=4)\n"
+        "pop = IO.make_population(wl); env = IO.make_env(wl)\n"
+        "pop.rollout(env, wl.n_envs, IO.make_pairs(wl), wl.seed, 1)\n"
+        "assert pop.payoff()['counts'].sum() == wl.n_envs\n"
+        "print('done', flush=True)\n" % root)
+    say("[exit] module-level handle in a child process")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert "done" in r.stdout
+    assert "Exception ignored" not in r.stderr and "Traceback" not in r.stderr, r.stderr[-2000:]
