@@ -961,6 +961,14 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W1, KIN / 16, nt0, rt0, buf, lane,
                                             bias[0], acc);
     ring_fill(ring, W2, HID / 16, nt0, lane);      // overlaps the epilogue
+    // the output layer's weight fragments: in flight during layer 2 below
+    // hidden width 512; at 512 their 32 registers live across layer 2 cost
+    // more than the load's latency after it
+    constexpr bool kW3Early = HID < 512;
+    uint4 w3[S::NT][2];
+    const Frags W3 = frag_src(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16);
+    if constexpr (kW3Early)
+        load_w3<S::NT>(w3, W3, nt0, lane);
     __syncthreads();
     hidden_epilogue<S::NT, S::RT, LDW>(acc, nt0, rt0, buf, lane);
     __syncthreads();
@@ -968,8 +976,8 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W2, HID / 16, nt0, rt0, buf, lane,
                                             bias[1], acc);
     // ---- layer 3 from the accumulators, partial logits summed through LDS
-    uint4 w3[S::NT][2];
-    load_w3<S::NT>(w3, frag_src(a.w3 + (int64_t)p * (HID / 16) * 64, HID / 16), nt0, lane);
+    if constexpr (!kW3Early)
+        load_w3<S::NT>(w3, W3, nt0, lane);
     f32x16 o[S::RT];
     out_from_acc<S::NT, S::RT>(acc, w3, o);
     __syncthreads();   // every wave is done reading the hidden rows: buf takes the partials
