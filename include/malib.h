@@ -6,7 +6,7 @@
  * population and reduces their returns into a mean-return matrix with
  * per-cell counts.  In MALib (arXiv 2106.07551) this is the work of the
  * Actors and the Evaluator: each agent picks a policy from its pool to form a
- * combination Comb_t (Sec. 3.1, "Defining the Task Graph"), rollouts sample
+ * combination Comb_t (Sec. 3.1, task graph), rollouts sample
  * X ~ P(s, a, s' | a ~ Comb_t) (Sec. 3.1, rollout equation), and the
  * Evaluator keeps a payoff table of the evaluation result of every policy
  * combination, on which e.g. PSRO solves for a meta-strategy (Sec. 3.2,

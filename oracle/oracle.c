@@ -7,7 +7,7 @@
  *
  * What it computes (MALib, arXiv 2106.07551):
  *   - each agent picks one policy from its pool, forming a combination
- *     (Sec. 3.1, "Defining the Task Graph");
+ *     (Sec. 3.1, task graph);
  *   - rollouts draw actions from that combination, X ~ P(s,a,s' | a ~ Comb_t)
  *     (Sec. 3.1, rollout equation);
  *   - the evaluator keeps a payoff table of per-combination evaluation results
