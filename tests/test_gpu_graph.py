@@ -194,3 +194,39 @@ def test_caller_capture_of_a_larger_batch_is_refused():
     tab = pop.payoff(reset=True)
     assert tab["envs"] == big.n_envs and tab["status"] == 0
     pop.close()
+
+
+def test_two_handles_on_two_streams_concurrently():
+    """Two handles of the same population, each filling half of a batch on a
+    stream of its own at the same time: their returns and merged table equal
+    one handle's fill of the whole batch (handles share no device state; the
+    fixed-point sums make the merge exact)."""
+    import paper_2106_07551_amd as M
+    from paper_2106_07551_amd import workload_io as IO
+    wl = W.team_variant(8, d=128, P=12, n_envs=2000, horizon=6, dims=[128, 256, 256, 18])
+    n, na = wl.n_envs, wl.n_agents
+    env = IO.make_env(wl)
+    pairs = IO.make_pairs(wl)
+    whole = IO.make_population(wl)
+    ref = torch.empty((na, n), dtype=torch.float32, device="cuda")
+    whole.rollout(env, n, pairs, wl.seed, wl.horizon, returns=ref)
+    t_ref = whole.payoff(reset=True)
+    halves = [IO.make_population(wl) for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    m = n // 2
+    rets = [torch.empty((na, m), dtype=torch.float32, device="cuda") for _ in range(2)]
+    torch.cuda.synchronize()
+    say("[streams] two handles, two streams, halves of 2000 envs")
+    for i in range(2):
+        halves[i].rollout(env, m, pairs[i * m:(i + 1) * m].contiguous(), wl.seed, wl.horizon,
+                          env_offset=i * m, returns=rets[i], stream=streams[i])
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat(rets, dim=1), ref)
+    tabs = [h.payoff(reset=True) for h in halves]
+    cnt = tabs[0]["counts"] + tabs[1]["counts"]
+    assert np.array_equal(cnt, t_ref["counts"])
+    s = sum(np.nan_to_num(t["mean"]) * t["counts"] for t in tabs)
+    merged = np.where(cnt > 0, s / np.maximum(cnt, 1), 0.0)
+    assert np.allclose(merged, np.nan_to_num(t_ref["mean"]), rtol=1e-12, atol=1e-12)
+    for h in halves + [whole]:
+        h.close()
