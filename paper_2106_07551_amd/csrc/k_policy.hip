@@ -467,7 +467,9 @@ __device__ __forceinline__ void ring_fill(WRing<NT, DEPTH>& ring, Frags frag,
 // rows).  acc[nt][rt] register r, lane i holds output unit nt*32 + (r/4)*8 +
 // (i/32)*4 + r%4 of tile row rt*32 + i%32.  The ring must hold k-steps
 // 0..DEPTH-1.  (The fp32 sum order of a unit is the bias, then the k-steps.)
-template <int NT, int RT, int DEPTH, int LDW = kLdw>
+// PRIO: the wave runs the k-loop at the normal issue priority and returns to
+// the raised one after it (see mlp_bf16_kernel).
+template <int NT, int RT, int DEPTH, int LDW = kLdw, bool PRIO = false>
 __device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring, Frags frag, int ksteps,
                                            int nt0,
                                            int rt0, const uint16_t* buf, int lane,
@@ -500,6 +502,8 @@ __device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring, Frags frag, i
     for (int r = 0; r < RT; ++r)
         b[0][r] = *reinterpret_cast<const uint4*>(bp[r]);
 
+    if constexpr (PRIO)
+        __builtin_amdgcn_s_setprio(0);
     for (int k0 = 0; k0 < ksteps; k0 += DEPTH) {
 #pragma unroll
         for (int s = 0; s < DEPTH; ++s) {
@@ -528,6 +532,8 @@ __device__ __forceinline__ void mfma_layer(WRing<NT, DEPTH>& ring, Frags frag, i
             }
         }
     }
+    if constexpr (PRIO)
+        __builtin_amdgcn_s_setprio(2);
 }
 
 // The same layer with one B buffer: row tile r of the next k-step is read
@@ -896,6 +902,14 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     __shared__ float gz[GZ];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // At hidden width 512 the waves run their latency-bound phases (row
+    // indices, noise, gather, epilogue, output and sampling) at a raised issue
+    // priority and their k-loops at the normal one, so that the CU's other
+    // workgroup's k-loops yield issue slots to them (4v4 forward 104.8 ->
+    // 103.8 us over six alternating runs; narrower widths measured slower).
+    constexpr bool kPrio = HID >= 512;
+    if constexpr (kPrio)
+        __builtin_amdgcn_s_setprio(2);
 
     // workgroups are dispatched round-robin over the 8 XCDs: each XCD reads one
     // segment of the striped tile table, an equal share of the tiles in order,
@@ -958,8 +972,8 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
 
     f32x16 acc[S::NT][S::RT];
     // ---- layer 1: KIN -> HID
-    mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W1, KIN / 16, nt0, rt0, buf, lane,
-                                            bias[0], acc);
+    mfma_layer<S::NT, S::RT, S::DEPTH, LDW, kPrio>(ring, W1, KIN / 16, nt0, rt0, buf, lane,
+                                                   bias[0], acc);
     ring_fill(ring, W2, HID / 16, nt0, lane);      // overlaps the epilogue
     // the output layer's weight fragments: in flight during layer 2 below
     // hidden width 512; at 512 their 32 registers live across layer 2 cost
@@ -973,8 +987,8 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     hidden_epilogue<S::NT, S::RT, LDW>(acc, nt0, rt0, buf, lane);
     __syncthreads();
     // ---- layer 2: HID -> HID
-    mfma_layer<S::NT, S::RT, S::DEPTH, LDW>(ring, W2, HID / 16, nt0, rt0, buf, lane,
-                                            bias[1], acc);
+    mfma_layer<S::NT, S::RT, S::DEPTH, LDW, kPrio>(ring, W2, HID / 16, nt0, rt0, buf, lane,
+                                                   bias[1], acc);
     // ---- layer 3 from the accumulators, partial logits summed through LDS
     if constexpr (!kW3Early)
         load_w3<S::NT>(w3, W3, nt0, lane);
