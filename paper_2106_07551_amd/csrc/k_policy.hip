@@ -940,7 +940,6 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     const Frags W2 = frag_src(a.w2 + (int64_t)p * (HID / 32) * (HID / 16) * 64,
                               (HID / 32) * (HID / 16));
     WRing<S::NT, S::DEPTH> ring;
-    ring_fill(ring, W1, KIN / 16, nt0, lane);     // overlaps the observation gather
 
     if (tid < MR) {
         row_slot[tid] = tid < nrows ? a.perm[r0 + tid] : -1;
@@ -951,6 +950,10 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
         bias[1][i] = a.b2[p * HID + i];
     }
     __syncthreads();
+    // the first weight fragments after the row indices (loads complete in
+    // order, so issued earlier they would delay the indices' LDS stores);
+    // they arrive during the noise and the observation gather
+    ring_fill(ring, W1, KIN / 16, nt0, lane);
     if constexpr (OBS == kObsFeature) {
         // the rows' Gumbel noise while the observation rows are fetched: one
         // thread per (row, Philox block of 8 actions), the same stream and
