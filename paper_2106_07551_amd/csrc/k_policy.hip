@@ -712,6 +712,11 @@ __device__ __forceinline__ void out_reduce(const float* red, int row, int slot, 
     }
 }
 
+// Row stride of the tile's Gumbel noise in LDS (gz): one float more than the
+// largest action count, so that the rows start on different banks (with a
+// stride of 32 floats every row's noise sat in the same banks).
+constexpr int kGzStride = kMaxActions + 1;
+
 // out_reduce that also samples the row's action (the four threads of a row,
 // lanes 4r..4r+3, share it): z_u = logit_u + g_u with the Gumbel noise g of
 // the row's slot staged in LDS (gz[row][u]), the first index of the largest z
@@ -741,7 +746,7 @@ __device__ __forceinline__ void out_reduce_sample(const float* red, const float*
         if (live && logits)
             logits[(int64_t)slot * A + u] = l;
         bad |= __builtin_isnan(l);
-        const float z = l + gz[row * kMaxActions + u];
+        const float z = l + gz[row * kGzStride + u];
         if (best < 0 || z > zbest) {
             zbest = z;
             best = u;
@@ -904,8 +909,8 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     // their accumulators from LDS instead of waiting on fresh global loads
     __shared__ __attribute__((aligned(16))) float bias[2][HID];
     // Gumbel noise of the rows' slots when the kernel samples the actions
-    // (feature observations), [MR][kMaxActions]
-    constexpr int GZ = OBS == kObsFeature ? MR * kMaxActions : 1;
+    // (feature observations), [MR][kGzStride]
+    constexpr int GZ = OBS == kObsFeature ? MR * kGzStride : 1;
     __shared__ float gz[GZ];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -971,7 +976,7 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
 #pragma unroll
                     for (int j = 0; j < 8; ++j)
                         if (blk * 8 + j < a.A)
-                            gz[row * kMaxActions + blk * 8 + j] =
+                            gz[row * kGzStride + blk * 8 + j] =
                                 gumbel01(uniform01(block_lane(pb, j)));
                 }
             }
