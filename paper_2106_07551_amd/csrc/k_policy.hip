@@ -678,7 +678,7 @@ __device__ __forceinline__ void out_from_acc(const f32x16 (&acc)[NT][RT],
 // Partials of wave group ng for row tiles rt0.. into red[NG][RTILES][G4][64]
 // (registers of output groups g < G3 only: the real actions; G4 >= 4 G3 is
 // 16 in general and 4 where at most 8 actions are known to be possible).
-template <int RT, int RTILES, int G4 = 16>
+template <int RT, int RTILES, int G4 = 16, int RS = 64>
 __device__ __forceinline__ void out_partials(float* red, const f32x16 (&o)[RT], int ng, int rt0,
                                              int G3, int lane)
 {
@@ -689,12 +689,12 @@ __device__ __forceinline__ void out_partials(float* red, const f32x16 (&o)[RT], 
             if (g < G3)
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                    red[((ng * RTILES + rt0 + rr) * G4 + g * 4 + q) * 64 + lane] = o[rr][g * 4 + q];
+                    red[((ng * RTILES + rt0 + rr) * G4 + g * 4 + q) * RS + lane] = o[rr][g * 4 + q];
 }
 
 // Logit (row, u) = sum over wave groups (in order) + bias; thread (row, u0)
 // writes u0, u0+4, ... of its row.
-template <int NG, int RTILES, int G4 = 16>
+template <int NG, int RTILES, int G4 = 16, int RS = 64>
 __device__ __forceinline__ void out_reduce(const float* red, int row, int slot, int u0, int A,
                                            const float* b3, float* __restrict__ logits)
 {
@@ -707,7 +707,7 @@ __device__ __forceinline__ void out_reduce(const float* red, int row, int slot, 
         float v = 0.0f;
 #pragma unroll
         for (int gq = 0; gq < NG; ++gq)
-            v += red[((gq * RTILES + (row >> 5)) * G4 + reg) * 64 + lr];
+            v += red[((gq * RTILES + (row >> 5)) * G4 + reg) * RS + lr];
         out[u] = v + b3[u];
     }
 }
@@ -725,7 +725,7 @@ constexpr int kGzStride = kMaxActions + 1;
 // gumbel_action.  A NaN logit raises kErrNaN and gives action 0.  Every lane
 // takes part in the shuffles; padding rows (slot < 0) write nothing.  Logits
 // are written when `logits` is not null.
-template <int NG, int RTILES, int G4 = 16>
+template <int NG, int RTILES, int G4 = 16, int RS = 64>
 __device__ __forceinline__ void out_reduce_sample(const float* red, const float* gz, int row,
                                                   int slot, int u0, int A, const float* b3,
                                                   float* __restrict__ logits,
@@ -741,7 +741,7 @@ __device__ __forceinline__ void out_reduce_sample(const float* red, const float*
         float v = 0.0f;
 #pragma unroll
         for (int gq = 0; gq < NG; ++gq)
-            v += red[((gq * RTILES + (row >> 5)) * G4 + reg) * 64 + lr];
+            v += red[((gq * RTILES + (row >> 5)) * G4 + reg) * RS + lr];
         const float l = v + b3[u];
         if (live && logits)
             logits[(int64_t)slot * A + u] = l;
@@ -900,7 +900,10 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     // partial-logit registers kept per (wave group, row tile): pursuit (5
     // actions) and the iterated game (<= 3) need one accumulator group
     constexpr int G4 = OBS == kObsFeature ? 16 : 4;
-    constexpr int PART = HidSplit<HID, WAVES, RTILES>::NGROUPS * RTILES * G4 * 64 * 2;   // in bf16
+    // partial logits at a row stride of 65 floats: the four threads of a row
+    // then read different banks in out_reduce (at 64 they shared one)
+    constexpr int RS = 65;
+    constexpr int PART = HidSplit<HID, WAVES, RTILES>::NGROUPS * RTILES * G4 * RS * 2;   // in bf16
     constexpr int BUF = MR * LDW > PART ? MR * LDW : PART;
     __shared__ __attribute__((aligned(16))) uint16_t buf[BUF];
     __shared__ int row_slot[MR];
@@ -1011,7 +1014,7 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
     out_from_acc<S::NT, S::RT>(acc, w3, o);
     __syncthreads();   // every wave is done reading the hidden rows: buf takes the partials
     float* red = reinterpret_cast<float*>(buf);
-    out_partials<S::RT, RTILES, G4>(red, o, wave % S::NGROUPS, rt0, (a.A + 7) >> 3, lane);
+    out_partials<S::RT, RTILES, G4, RS>(red, o, wave % S::NGROUPS, rt0, (a.A + 7) >> 3, lane);
     __syncthreads();
     {
         const int row = tid >> 2;
@@ -1019,13 +1022,13 @@ __global__ __launch_bounds__(bf16_tile_threads(HID), bf16_tile_waves_per_simd(HI
         if constexpr (OBS == kObsFeature) {
             if (a.actions) {
                 if (row < MR)
-                    out_reduce_sample<S::NGROUPS, RTILES, G4>(red, gz, row, slot, tid & 3, a.A,
+                    out_reduce_sample<S::NGROUPS, RTILES, G4, RS>(red, gz, row, slot, tid & 3, a.A,
                                                               a.b3 + p * a.A, a.logits,
                                                               a.actions, a.flags);
                 return;
             }
         }
-        out_reduce<S::NGROUPS, RTILES, G4>(red, row, slot, tid & 3, a.A, a.b3 + p * a.A,
+        out_reduce<S::NGROUPS, RTILES, G4, RS>(red, row, slot, tid & 3, a.A, a.b3 + p * a.A,
                                            a.logits);
     }
 }
